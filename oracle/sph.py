@@ -1,0 +1,310 @@
+"""Plain fp64 CPU reference of SPHQuant's representation and its decode-and-multiply.
+
+TEST INFRASTRUCTURE ONLY. Only the test-suite, the smoke check of ``__graft_entry__`` and
+the CPU-baseline leg of ``bench.py`` may import this module; the library never does. It
+shares no code with the HIP path: it reads the logical codes (see ``synth``) and
+computes with NumPy in fp64, step by step in the paper's order and notation.
+
+References are to the SPHQuant paper: Sec. 1 (introduction, worked radius example),
+Sec. 3.1 (spherical quantisation, Eq. 3-7), Sec. 3.3 (angular codebook, Eq. 9-10),
+Sec. 3.4 and App. D (W2 packed layout and fused decode), App. B (payload accounting),
+Tab. 7 (codebook sizes by vector dimension).
+
+Every function here is pinned by a test in ``tests/test_oracle_pins.py`` against values
+the paper prints, closed forms, invariants or brute force; none is "parity unpinned".
+"""
+from __future__ import annotations
+
+import numpy as np
+
+VEC = 8                # Sec. 3.1: rows are cut along d_in into contiguous 8-D vectors
+GROUP = 128            # Sec. 3.1: a radius group is 128 consecutive scalars of one row
+VPG = GROUP // VEC     # = 16 vectors per group
+EPS = 1e-12            # Eq. 3's epsilon (its value is not printed; reading: 1e-12 in fp64)
+
+
+# ----------------------------------------------------------------------------- helpers
+
+def f16_to_f64(bits) -> np.ndarray:
+    """fp16 bit patterns (uint16) -> exact fp64 values."""
+    return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float64)
+
+
+def f64_to_f16(a) -> np.ndarray:
+    """fp64 -> nearest fp16, returned as bit patterns (uint16)."""
+    return np.asarray(a, dtype=np.float64).astype(np.float16).view(np.uint16)
+
+
+# ------------------------------------------------------------- bit budget (Sec. 3.1, App. B)
+
+def dir_bits_for(bits_per_weight: int, dim: int = VEC) -> int:
+    """Direction-index width. Sec. 3.1 gives 7B bits to the 7 angular degrees of freedom of
+    an 8-D vector and spends 8 of them on the sign bits, K_dir = 7B - 8. For a k-D vector the
+    same accounting reads (k-1)B - k (this generalisation is what Tab. 7's codebook sizes
+    imply: 32 B, 1 KiB and 512 KiB for 4-D, 8-D and 16-D at B = 2)."""
+    return (dim - 1) * bits_per_weight - dim
+
+
+def codebook_bytes(dir_bits: int, dim: int = VEC, signed: bool = False) -> int:
+    """fp16 storage of a 2**dir_bits-entry codebook; a signed-direction codebook needs 2**dim
+    times more entries (Sec. 3.1)."""
+    entries = (1 << dir_bits) * ((1 << dim) if signed else 1)
+    return entries * dim * 2
+
+
+def payload_bits_per_weight(bits_per_weight: int, radius_bits: int) -> float:
+    """Encoded payload of an 8-D vector code, (7B + V)/8 bits per weight (App. B). Excludes
+    group parameters and the codebook."""
+    return (7 * bits_per_weight + radius_bits) / 8.0
+
+
+# --------------------------------------------------------- spherical coordinates (Eq. 1)
+
+def spherical_coordinates(w) -> tuple[np.ndarray, np.ndarray]:
+    """Eq. 1: radius r = ||w||_2 and the k-1 angles of a k-D vector (last axis)."""
+    w = np.asarray(w, dtype=np.float64)
+    k = w.shape[-1]
+    r = np.sqrt(np.sum(w * w, axis=-1))
+    phi = np.empty(w.shape[:-1] + (k - 1,))
+    for i in range(k - 2):
+        tail = np.sqrt(np.sum(w[..., i:] ** 2, axis=-1))
+        with np.errstate(invalid="ignore", divide="ignore"):
+            c = np.where(tail > 0, w[..., i] / np.where(tail > 0, tail, 1.0), 1.0)
+        phi[..., i] = np.arccos(np.clip(c, -1.0, 1.0))
+    phi[..., k - 2] = np.arctan2(w[..., k - 1], w[..., k - 2])
+    return r, phi
+
+
+def from_spherical(r, phi) -> np.ndarray:
+    """Inverse of Eq. 1 (standard hyperspherical parameterisation)."""
+    r = np.asarray(r, dtype=np.float64)
+    phi = np.asarray(phi, dtype=np.float64)
+    k = phi.shape[-1] + 1
+    out = np.empty(phi.shape[:-1] + (k,))
+    sprod = np.ones(phi.shape[:-1])
+    for i in range(k - 1):
+        out[..., i] = sprod * np.cos(phi[..., i])
+        sprod = sprod * np.sin(phi[..., i])
+    out[..., k - 1] = sprod
+    return r[..., None] * out
+
+
+# ------------------------------------------------------------------ encoder (Eq. 3, 5-7)
+
+def decompose(w):
+    """Eq. 3 on the last axis: signs, positive-orthant vector, radius and unit direction.
+
+    Returns (neg, w_plus, r, d) with neg[..., j] True where w_j < 0. Reading: a zero (or
+    negative zero) coordinate counts as positive, since sign(0) is not defined by Eq. 3."""
+    w = np.asarray(w, dtype=np.float64)
+    neg = w < 0
+    w_plus = np.abs(w)
+    r = np.sqrt(np.sum(w_plus * w_plus, axis=-1))
+    d = w_plus / np.maximum(r, EPS)[..., None]
+    return neg, w_plus, r, d
+
+
+def assign_directions(d, codebook, chunk: int = 4096) -> np.ndarray:
+    """Eq. 5: z_i = argmax_k <d_i, c_k>; ties go to the lowest index (reading)."""
+    d = np.asarray(d, dtype=np.float64).reshape(-1, VEC)
+    c = np.asarray(codebook, dtype=np.float64)
+    z = np.empty(d.shape[0], dtype=np.int64)
+    for a in range(0, d.shape[0], chunk):
+        z[a:a + chunk] = np.argmax(d[a:a + chunk] @ c.T, axis=1)
+    return z
+
+
+def ls_radius(w_plus, c_z) -> np.ndarray:
+    """Eq. 6: pre-quantisation radius <w_+, c_z> (the least-squares scale along a unit c_z).
+    Reading: the stored fp16 codebook entry is used as is, not renormalised."""
+    return np.sum(np.asarray(w_plus, np.float64) * np.asarray(c_z, np.float64), axis=-1)
+
+
+def group_offset_step(r_tilde, radius_bits: int):
+    """Eq. 7's per-group offset and step: min over the group, (max - min)/(2**V - 1).
+    ``r_tilde`` is [..., groups, 16]; returns fp16 bit patterns (reading: both stored as fp16).
+    """
+    r_tilde = np.asarray(r_tilde, dtype=np.float64)
+    lo = r_tilde.min(axis=-1)
+    hi = r_tilde.max(axis=-1)
+    step = (hi - lo) / ((1 << radius_bits) - 1)
+    return f64_to_f16(lo), f64_to_f16(step)
+
+
+def quantize_radius(r_tilde, gmin_bits, gstep_bits, radius_bits: int) -> np.ndarray:
+    """Eq. 7: q = clip(round((r~ - min)/Delta), 0, 2**V - 1) with the stored (fp16) group
+    parameters. ``r_tilde`` is [..., groups, 16], params [..., groups]. Readings: round half
+    to even; a zero step gives q = 0."""
+    r_tilde = np.asarray(r_tilde, dtype=np.float64)
+    lo = f16_to_f64(gmin_bits)[..., None]
+    step = f16_to_f64(gstep_bits)[..., None]
+    safe = np.where(step > 0, step, 1.0)
+    t = np.where(step > 0, np.rint((r_tilde - lo) / safe), 0.0)
+    return np.clip(t, 0, (1 << radius_bits) - 1).astype(np.uint8)
+
+
+def signs_to_bits(neg) -> np.ndarray:
+    """Pack the 8 negative-flags of a vector into one byte, bit j <-> coordinate j."""
+    neg = np.asarray(neg, dtype=bool)
+    weights = (1 << np.arange(VEC)).astype(np.uint16)
+    return (neg.astype(np.uint16) * weights).sum(axis=-1).astype(np.uint8)
+
+
+def encode(w, codebook_bits, radius_bits: int, params=None) -> dict:
+    """Spherical quantisation of a weight matrix W[n][k] (Sec. 3.1; App. A steps 4-6, 10,
+    with a fixed codebook instead of k-means and without fine-tuning).
+
+    Per 8-D vector: Eq. 3 decomposition, Eq. 5 direction, Eq. 6 radius, Eq. 7 group
+    quantisation. ``params`` = (gmin_bits, gstep_bits) forces the group parameters; by
+    default they come from the data as in Eq. 7. Returns the logical codes."""
+    w = np.asarray(w, dtype=np.float64)
+    n, k = w.shape
+    if k % GROUP:
+        raise ValueError("k must be a multiple of 128")
+    c = f16_to_f64(codebook_bits)
+    vecs = w.reshape(n, k // VEC, VEC)
+    neg, w_plus, _r, d = decompose(vecs)
+    z = assign_directions(d, c).reshape(n, k // VEC)
+    r_tilde = ls_radius(w_plus, c[z])
+    rg = r_tilde.reshape(n, k // GROUP, VPG)
+    if params is None:
+        gmin, gstep = group_offset_step(rg, radius_bits)
+    else:
+        gmin = np.broadcast_to(np.asarray(params[0], np.uint16), (n, k // GROUP)).copy()
+        gstep = np.broadcast_to(np.asarray(params[1], np.uint16), (n, k // GROUP)).copy()
+    q = quantize_radius(rg, gmin, gstep, radius_bits).reshape(n, k // VEC)
+    return {"signs": signs_to_bits(neg), "dir": z.astype(np.uint16), "q": q,
+            "gmin": gmin, "gstep": gstep}
+
+
+# ---------------------------------------------------------------- decoder (Eq. 4 and 7)
+
+def sign_factors(signs) -> np.ndarray:
+    """Byte of sign bits -> the +-1 factors s of Eq. 3/4, shape [..., 8]."""
+    b = np.asarray(signs, dtype=np.uint8)[..., None]
+    bit = (b >> np.arange(VEC, dtype=np.uint8)) & 1
+    return 1.0 - 2.0 * bit.astype(np.float64)
+
+
+def dequantize_radius(q, gmin_bits, gstep_bits) -> np.ndarray:
+    """Eq. 7: r^ = min_G + q * Delta_G, per vector; params are per group of 16 vectors."""
+    q = np.asarray(q, dtype=np.float64)
+    n, nv = q.shape
+    lo = np.repeat(f16_to_f64(gmin_bits), VPG, axis=1)[:, :nv]
+    step = np.repeat(f16_to_f64(gstep_bits), VPG, axis=1)[:, :nv]
+    return lo + q * step
+
+
+def decode(codes: dict, codebook_bits) -> np.ndarray:
+    """Eq. 4: w^ = r^ * s (.) c_z, assembled into the dense fp64 matrix W^[n][k]."""
+    c = f16_to_f64(codebook_bits)
+    r_hat = dequantize_radius(codes["q"], codes["gmin"], codes["gstep"])
+    s = sign_factors(codes["signs"])
+    vec = r_hat[..., None] * s * c[np.asarray(codes["dir"], dtype=np.int64)]
+    n, nv = r_hat.shape
+    return vec.reshape(n, nv * VEC)
+
+
+def _rows(codes: dict, a: int, b: int) -> dict:
+    return {key: np.asarray(v)[a:b] for key, v in codes.items()}
+
+
+def gemm(codes: dict, codebook_bits, x_bits, row_chunk: int = 256) -> np.ndarray:
+    """Y[m][n] = sum_k W^[n][k] * x[m][k] in fp64 (the linear layer y = W x of Sec. 3.4 with
+    fp16 activations), decoding W^ a block of rows at a time."""
+    x = f16_to_f64(x_bits)
+    if x.ndim == 1:
+        x = x[None, :]
+    n = np.asarray(codes["q"]).shape[0]
+    y = np.empty((x.shape[0], n))
+    for a in range(0, n, row_chunk):
+        b = min(n, a + row_chunk)
+        y[:, a:b] = x @ decode(_rows(codes, a, b), codebook_bits).T
+    return y
+
+
+def gemv(codes: dict, codebook_bits, x_bits) -> np.ndarray:
+    """Batch-1 case of ``gemm``: y[n]."""
+    return gemm(codes, codebook_bits, np.asarray(x_bits).reshape(1, -1))[0]
+
+
+def gemm_rows(codes: dict, codebook_bits, x_bits, rows) -> np.ndarray:
+    """``gemm`` restricted to a list of output rows: Y[m][len(rows)]."""
+    rows = np.asarray(rows, dtype=np.int64)
+    sub = {key: np.asarray(v)[rows] for key, v in codes.items()}
+    x = f16_to_f64(x_bits)
+    if x.ndim == 1:
+        x = x[None, :]
+    return x @ decode(sub, codebook_bits).T
+
+
+# ---------------------------------------------- the W2 packed layout (Sec. 3.4, App. D)
+
+def paper_pack_w2(signs, dir_idx, q):
+    """Sec. 3.4 / App. D / Fig. 3b, W2 (D = 6, V = 4).
+
+    One 16-bit base word per vector: bits [7:0] sign bits, [13:8] direction index,
+    [15:14] the low two bits of the radius level. One 32-bit word per 128-weight group holds
+    the two extra (high) radius bits of its 16 vectors; reading: vector i of the group sits at
+    bits [2i+1:2i]."""
+    signs = np.asarray(signs, dtype=np.uint32)
+    dir_idx = np.asarray(dir_idx, dtype=np.uint32)
+    q = np.asarray(q, dtype=np.uint32)
+    if dir_idx.max(initial=0) >= 64 or q.max(initial=0) >= 16:
+        raise ValueError("W2 codes out of range")
+    base = (signs | (dir_idx << 8) | ((q & 3) << 14)).astype(np.uint16)
+    n, nv = q.shape
+    hi = ((q >> 2) & 3).reshape(n, nv // VPG, VPG)
+    shifts = (2 * np.arange(VPG)).astype(np.uint32)
+    aux = np.bitwise_or.reduce(hi << shifts, axis=-1).astype(np.uint32)
+    return base, aux
+
+
+def paper_unpack_w2(base, aux):
+    """Inverse of ``paper_pack_w2``."""
+    base = np.asarray(base, dtype=np.uint32)
+    aux = np.asarray(aux, dtype=np.uint32)
+    n, nv = base.shape
+    signs = (base & 0xFF).astype(np.uint8)
+    dir_idx = ((base >> 8) & 0x3F).astype(np.uint16)
+    shifts = (2 * np.arange(VPG)).astype(np.uint32)
+    hi = ((aux[..., None] >> shifts) & 3).reshape(n, nv)
+    q = ((base >> 14) & 3) | (hi << 2)
+    return signs, dir_idx, q.astype(np.uint8)
+
+
+# --------------------------------------------------- angular codebook (Eq. 9 and Eq. 10)
+
+def angles_from_logits(phi, eps: float = 1e-4) -> np.ndarray:
+    """Eq. 10: theta_j = eps + (pi/2 - 2 eps) * sigmoid(phi_j), which keeps every angle
+    strictly inside (0, pi/2). The value of eps is not printed; 1e-4 is the reading."""
+    phi = np.asarray(phi, dtype=np.float64)
+    return eps + (np.pi / 2 - 2 * eps) / (1.0 + np.exp(-phi))
+
+
+def angular_codebook(theta) -> np.ndarray:
+    """Eq. 9: a unit 8-D direction from seven hyperspherical angles,
+    c_1 = cos t_1, c_i = (prod_{j<i} sin t_j) cos t_i for 2 <= i <= 7, c_8 = prod sin t_j."""
+    theta = np.asarray(theta, dtype=np.float64)
+    out = np.empty(theta.shape[:-1] + (VEC,))
+    sprod = np.ones(theta.shape[:-1])
+    for i in range(VEC - 1):
+        out[..., i] = sprod * np.cos(theta[..., i])
+        sprod = sprod * np.sin(theta[..., i])
+    out[..., VEC - 1] = sprod
+    return out
+
+
+# ----------------------------------------------------------------- comparison metric
+
+def rel_err(y, y_ref) -> float:
+    """Max over outputs of |y - y*| / max(|y*|, rms of y* over its output row).
+
+    Element-wise relative error is ill-posed where y* is near zero; the row RMS floors the
+    denominator (reading of "max relative error")."""
+    y = np.atleast_2d(np.asarray(y, dtype=np.float64))
+    y_ref = np.atleast_2d(np.asarray(y_ref, dtype=np.float64))
+    rms = np.sqrt(np.mean(y_ref * y_ref, axis=1, keepdims=True))
+    den = np.maximum(np.abs(y_ref), rms)
+    den = np.where(den > 0, den, 1.0)
+    return float(np.max(np.abs(y - y_ref) / den)) if y.size else 0.0

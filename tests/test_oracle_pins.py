@@ -1,0 +1,508 @@
+"""Pins of the fp64 oracle against what the paper and mathematics fix.
+
+Each ``pin_*`` function checks one part of the oracle against something other than
+itself: values the paper prints (golden fixtures with citations), closed forms,
+invariants, library routines for special cases, exact rational arithmetic, and brute
+force over every code of tiny codebooks. ``test_mutants_are_caught`` plants plausible
+mistakes in a copy of the oracle and requires that some pin fails for each.
+"""
+from __future__ import annotations
+
+import itertools
+import types
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import sph as O
+from tests.conftest import read_golden
+
+
+def _ns(**override):
+    ns = types.SimpleNamespace(**{k: getattr(O, k) for k in dir(O) if not k.startswith("__")})
+    for k, v in override.items():
+        setattr(ns, k, v)
+    return ns
+
+
+# A codebook of exactly-unit, non-negative 8-D directions: the 8 axes and the 56 first
+# 4-subsets of coordinates at 1/2 (4 * 1/4 = 1). All values are exact in fp16.
+def exact_unit_codebook(entries=64):
+    rows = [np.eye(8)[j] for j in range(8)]
+    for sub in itertools.combinations(range(8), 4):
+        v = np.zeros(8)
+        v[list(sub)] = 0.5
+        rows.append(v)
+    return synth.f16_bits(np.array(rows[:entries]))
+
+
+# ------------------------------------------------------------------------- pins
+
+def pin_worked_radius(o):
+    """Sec. 1: radius of (1,..,1) is 2*sqrt(2); with one coordinate at 5 it is 4*sqrt(2)."""
+    for coords, mult in read_golden("worked_radius.txt"):
+        w = np.array([float(t) for t in coords.split()])
+        r_sph, _ = o.spherical_coordinates(w)
+        _, _, r_dec, _ = o.decompose(w)
+        want = float(mult) * np.sqrt(2.0)
+        assert abs(r_sph - want) < 1e-14 and abs(r_dec - want) < 1e-14
+
+
+def pin_spherical_roundtrip(o):
+    """Eq. 1 round trip through the textbook inverse, and the angle ranges."""
+    g = np.random.default_rng(1)
+    w = g.standard_normal((500, 8))
+    r, phi = o.spherical_coordinates(w)
+    assert np.allclose(o.from_spherical(r, phi), w, atol=1e-12)
+    assert np.all(phi[:, :6] >= 0) and np.all(phi[:, :6] <= np.pi)
+    assert np.allclose(r, np.linalg.norm(w, axis=1), rtol=1e-14)
+
+
+def pin_bit_budget(o):
+    """Storage figures of Sec. 1, 3.1, 3.2, 4.1, App. B, Tab. 7 and Tab. 12."""
+    for key, args, want, _src in read_golden("bit_budget.txt"):
+        a = dict(t.split("=") for t in args.split())
+        a = {k: int(v) for k, v in a.items()}
+        want = float(want)
+        if key == "dir_bits":
+            got = o.dir_bits_for(a["B"], a["dim"])
+        elif key == "codebook_bytes":
+            got = o.codebook_bytes(a["D"], a["dim"], bool(a["signed"]))
+        elif key == "codebook_bytes_tab7":
+            got = o.codebook_bytes(o.dir_bits_for(a["B"], a["dim"]), a["dim"])
+        elif key == "payload":
+            got = o.payload_bits_per_weight(a["B"], a["V"])
+        elif key == "extra_payload_pct":
+            got = 100.0 * (o.payload_bits_per_weight(a["B"], a["V"]) / a["B"] - 1.0)
+        else:
+            raise AssertionError(key)
+        assert abs(got - want) < 1e-12, (key, args, got, want)
+
+
+def pin_decompose(o):
+    """Eq. 3: w = r * s (.) d exactly up to rounding, d on the positive unit sphere, sign of
+    zero is +, and the zero vector gets r = 0 and d = 0."""
+    g = np.random.default_rng(2)
+    w = g.standard_normal((300, 8)) * np.exp(g.standard_normal((300, 1)))
+    neg, wp, r, d = o.decompose(w)
+    s = np.where(neg, -1.0, 1.0)
+    assert np.allclose(r[:, None] * s * d, w, rtol=1e-14, atol=1e-300)
+    assert np.all(d >= 0) and np.allclose(np.linalg.norm(d, axis=1), 1.0, atol=1e-14)
+    assert np.array_equal(wp, np.abs(w))
+    neg0, _, r0, d0 = o.decompose(np.array([0.0, -0.0, 1.0, 0, 0, 0, 0, -2.0]))
+    assert list(neg0) == [False, False, False, False, False, False, False, True]
+    _, _, rz, dz = o.decompose(np.zeros(8))
+    assert rz == 0 and np.all(dz == 0)
+
+
+def pin_assign(o):
+    """Eq. 5: the direction of a codebook entry is assigned to that entry; the cosine
+    argmax is the nearest entry in angle (checked by brute-force arccos); ties -> lowest."""
+    g = np.random.default_rng(3)
+    cb = synth.random_codebook(6, g)
+    c = O.f16_to_f64(cb)
+    own = c / np.linalg.norm(c, axis=1, keepdims=True)
+    assert np.array_equal(o.assign_directions(own, c), np.arange(64))
+    d = np.abs(g.standard_normal((400, 8)))
+    d /= np.linalg.norm(d, axis=1, keepdims=True)
+    z = o.assign_directions(d, c)
+    cn = c / np.linalg.norm(c, axis=1, keepdims=True)
+    ang = np.arccos(np.clip(d @ cn.T, -1, 1))
+    # Entries are not exactly unit after fp16; the cosine argmax may differ from the angle
+    # argmin only when two angles agree to within the norm error.
+    best = ang.min(axis=1)
+    assert np.all(ang[np.arange(400), z] <= best + 2e-3)
+    dup = np.vstack([c[:3], c[1:2], c[3:]])
+    assert o.assign_directions(own[1:2], dup)[0] == 1
+
+
+def pin_ls_radius(o):
+    """Eq. 6: <w_+, c> is the least-squares scale along a unit c (checked with lstsq on
+    exactly-unit entries) and never exceeds ||w_+|| (Cauchy-Schwarz)."""
+    g = np.random.default_rng(4)
+    c = O.f16_to_f64(exact_unit_codebook(64))
+    for _ in range(50):
+        wp = np.abs(g.standard_normal(8))
+        cz = c[g.integers(0, 64)]
+        alpha = np.linalg.lstsq(cz[:, None], wp, rcond=None)[0][0]
+        assert abs(o.ls_radius(wp, cz) - alpha) < 1e-13
+        assert o.ls_radius(wp, cz) <= np.linalg.norm(wp) + 1e-15
+        assert o.ls_radius(wp, cz) >= 0
+
+
+def pin_radius_quant(o):
+    """Eq. 7 on a grid: radii min + j*Delta get levels j and their own (min, Delta) back;
+    values outside [min, max] clip; a zero step gives level 0; V = 3 has 8 levels."""
+    for v_bits, lo, step in ((4, 0.5, 0.125), (3, 0.25, 0.0625), (2, 1.0, 0.5), (8, 0.0, 2**-6)):
+        grid = lo + np.arange(16) % (1 << v_bits) * step
+        grid[0], grid[-1] = lo, lo + ((1 << v_bits) - 1) * step
+        gmin, gstep = o.group_offset_step(grid[None, :], v_bits)
+        assert O.f16_to_f64(gmin)[0] == lo and O.f16_to_f64(gstep)[0] == step
+        q = o.quantize_radius(grid[None, :], gmin, gstep, v_bits)[0]
+        want = np.arange(16) % (1 << v_bits)
+        want[-1] = (1 << v_bits) - 1
+        assert np.array_equal(q, want), (v_bits, q, want)
+        out = o.quantize_radius(np.array([[lo - 5 * step, lo + ((1 << v_bits) + 50) * step]]), gmin, gstep, v_bits)
+        assert list(out[0]) == [0, (1 << v_bits) - 1]
+        r_hat = o.dequantize_radius(q[None, :].astype(np.uint8),
+                                    np.array([gmin]), np.array([gstep]))[0]
+        assert np.array_equal(r_hat, grid)
+    gmin, gstep = o.group_offset_step(np.full((1, 16), 0.75), 4)
+    assert O.f16_to_f64(gstep)[0] == 0
+    assert np.all(o.quantize_radius(np.full((1, 16), 0.75), gmin, gstep, 4) == 0)
+
+
+def pin_decode_norm_and_sign(o):
+    """Eq. 4: ||w^|| = r^ ||c_z|| and sign(w^_j) = s_j wherever c_z,j > 0."""
+    g = np.random.default_rng(5)
+    cb = synth.random_codebook(6, g)
+    codes = synth.uniform_codes(8, 256, 6, 4, g)
+    codes["gmin"], codes["gstep"] = synth.row_scale_group_params(8, 256, 4, g)
+    w = o.decode(codes, cb).reshape(8, 32, 8)
+    c = O.f16_to_f64(cb)
+    r_hat = o.dequantize_radius(codes["q"], codes["gmin"], codes["gstep"])
+    norms = np.linalg.norm(c[codes["dir"].astype(int)], axis=-1)
+    assert np.allclose(np.linalg.norm(w, axis=-1), r_hat * norms, rtol=1e-14)
+    bits = (codes["signs"][..., None] >> np.arange(8)) & 1
+    assert np.all((w < 0) == (bits == 1))
+
+
+def pin_decode_one_hot(o):
+    """Eq. 4 with the axis codebook c_k = e_(k mod 8): every vector has one non-zero,
+    +-r^ at coordinate z mod 8 (written out by hand below)."""
+    g = np.random.default_rng(6)
+    cb = synth.f16_bits(np.eye(8)[np.arange(16) % 8])
+    n, k = 3, 256
+    codes = synth.uniform_codes(n, k, 4, 4, g)
+    codes["gmin"], codes["gstep"] = synth.row_scale_group_params(n, k, 4, g)
+    w = o.decode(codes, cb)
+    for r in range(n):
+        for v in range(k // 8):
+            s = int(codes["signs"][r, v])
+            z = int(codes["dir"][r, v])
+            grp = v // 16
+            rh = O.f16_to_f64(codes["gmin"][r, grp]) + int(codes["q"][r, v]) * \
+                O.f16_to_f64(codes["gstep"][r, grp])
+            want = np.zeros(8)
+            j = z % 8
+            want[j] = -rh if (s >> j) & 1 else rh
+            assert np.array_equal(w[r, 8 * v:8 * v + 8], want)
+
+
+def pin_gemm_exact_rational(o):
+    """Y = W^ x against exact rational arithmetic (every fp16 input is a dyadic rational),
+    one scalar term at a time; the oracle must agree within a few fp64 roundings."""
+    g = np.random.default_rng(7)
+    n, k, m = 3, 256, 2
+    cb = synth.random_codebook(6, g)
+    codes = synth.uniform_codes(n, k, 6, 4, g)
+    codes["gmin"], codes["gstep"] = synth.row_scale_group_params(n, k, 4, g)
+    codes["gmin"][1, 0] = synth.f16_bits([-0.375])[0]      # a negative offset is accepted too
+    x = synth.activations(m, k, g)
+    y = o.gemm(codes, cb, x)
+    fr = lambda b: Fraction(float(O.f16_to_f64(b)))  # noqa: E731
+    for b in range(m):
+        for r in range(n):
+            acc = Fraction(0)
+            bound = 0.0
+            for col in range(k):
+                v, j = divmod(col, 8)
+                grp = col // 128
+                radius = fr(codes["gmin"][r, grp]) + int(codes["q"][r, v]) * fr(codes["gstep"][r, grp])
+                sgn = -1 if (int(codes["signs"][r, v]) >> j) & 1 else 1
+                term = radius * sgn * fr(cb[int(codes["dir"][r, v]), j]) * fr(x[b, col])
+                acc += term
+                bound += abs(float(term))
+            assert abs(y[b, r] - float(acc)) <= 8 * k * 2.0**-53 * bound + 1e-300
+
+
+def pin_gemm_special_cases(o):
+    """x = e_col returns column col of W^; a zero step with the exact direction
+    (1/2,1/2,1/2,1/2,0,0,0,0) and positive signs gives y = min/2 * (sum of x_j, j<4 per vector)."""
+    g = np.random.default_rng(8)
+    n, k = 5, 384
+    cb = synth.random_codebook(4, g)
+    codes = synth.uniform_codes(n, k, 4, 4, g)
+    codes["gmin"], codes["gstep"] = synth.row_scale_group_params(n, k, 4, g)
+    w = o.decode(codes, cb)
+    for col in (0, 7, 8, 200, 383):
+        e = np.zeros((1, k))
+        e[0, col] = 1.0
+        assert np.array_equal(o.gemm(codes, cb, synth.f16_bits(e))[0], w[:, col])
+    half = np.zeros((16, 8))
+    half[:, :4] = 0.5
+    codes2 = {"signs": np.zeros((n, k // 8), np.uint8), "dir": codes["dir"],
+              "q": codes["q"], "gmin": codes["gmin"],
+              "gstep": np.zeros_like(codes["gstep"])}
+    x = synth.activations(2, k, g)
+    xf = O.f16_to_f64(x)
+    y = o.gemm(codes2, synth.f16_bits(half), x)
+    mins = O.f16_to_f64(codes["gmin"])[:, 0]
+    want = mins[None, :] * 0.5 * xf.reshape(2, k // 8, 8)[:, :, :4].sum(axis=(1, 2))[:, None]
+    assert np.allclose(y, want, rtol=1e-13)
+
+
+def _all_codes(dir_bits, radius_bits, k=128):
+    combos = np.array(list(itertools.product(range(256), range(1 << dir_bits),
+                                             range(1 << radius_bits))), dtype=np.int64)
+    nvec = combos.shape[0]
+    per_row = k // 8
+    n = -(-nvec // per_row)
+    pad = n * per_row - nvec
+    combos = np.vstack([combos, np.zeros((pad, 3), np.int64)])
+    return {"signs": combos[:, 0].astype(np.uint8).reshape(n, per_row),
+            "dir": combos[:, 1].astype(np.uint16).reshape(n, per_row),
+            "q": combos[:, 2].astype(np.uint8).reshape(n, per_row)}
+
+
+def pin_encode_roundtrip_bruteforce(o):
+    """decode then encode returns the same codes, for every (sign byte, direction, level)
+    of tiny codebooks (D = 2, 4, 6; V = 4 and 3) with fixed group parameters."""
+    for d_bits, v_bits in ((2, 4), (4, 4), (6, 4), (4, 3)):
+        g = np.random.default_rng(10 + d_bits)
+        cb = synth.random_codebook(d_bits, g)
+        assert np.all(O.f16_to_f64(cb) > 0)
+        codes = _all_codes(d_bits, v_bits)
+        n = codes["q"].shape[0]
+        gmin = np.full((n, 1), synth.f16_bits(0.5), np.uint16)
+        gstep = np.full((n, 1), synth.f16_bits(0.1), np.uint16)
+        codes["gmin"], codes["gstep"] = gmin, gstep
+        w = o.decode(codes, cb)
+        back = o.encode(w, cb, v_bits, params=(gmin, gstep))
+        for key in ("signs", "dir", "q"):
+            assert np.array_equal(back[key], codes[key]), (d_bits, v_bits, key)
+
+
+def pin_encode_group_params_recovered(o):
+    """With exactly-unit directions and every group using both extreme levels, the
+    data-derived (min, Delta) of Eq. 7 are the ones that generated the radii, and the codes
+    come back (signs canonicalised to + where the direction coordinate is 0)."""
+    g = np.random.default_rng(20)
+    cb = exact_unit_codebook(64)
+    c = O.f16_to_f64(cb)
+    n, k, v_bits = 6, 512, 4
+    codes = synth.uniform_codes(n, k, 6, v_bits, g)
+    q = codes["q"].reshape(n, k // 128, 16)
+    q[..., 0], q[..., 5] = 0, 15
+    codes["q"] = q.reshape(n, k // 8)
+    lo = np.array([0.5, 0.25, 1.0, 2.0, 0.125, 0.75])
+    codes["gmin"] = synth.f16_bits(np.repeat(lo[:, None], k // 128, axis=1))
+    codes["gstep"] = synth.f16_bits(np.repeat((lo / 8)[:, None], k // 128, axis=1))
+    back = o.encode(o.decode(codes, cb), cb, v_bits)
+    zero = c[codes["dir"].astype(int)] == 0
+    bits = (codes["signs"][..., None] >> np.arange(8)) & 1
+    canon = ((bits * ~zero) << np.arange(8)).sum(axis=-1).astype(np.uint8)
+    assert np.array_equal(back["signs"], canon)
+    for key in ("dir", "q", "gmin", "gstep"):
+        assert np.array_equal(back[key], codes[key]), key
+
+
+def pin_w2_layout(o):
+    """Sec. 3.4 / App. D / Fig. 3b field positions, on hand-worked words; plus a bit-exact
+    pack/unpack round trip on random codes."""
+    rows = read_golden("w2_layout.txt")
+    for fields, want in rows:
+        vals = fields.split()
+        if len(vals) == 3:
+            s, d, q = int(vals[0], 0), int(vals[1]), int(vals[2])
+            sig = np.zeros((1, 16), np.uint8)
+            dd = np.zeros((1, 16), np.uint16)
+            qq = np.zeros((1, 16), np.uint8)
+            sig[0, 0], dd[0, 0], qq[0, 0] = s, d, q
+            base, _ = o.paper_pack_w2(sig, dd, qq)
+            assert int(base[0, 0]) == int(want, 16), (fields, hex(int(base[0, 0])))
+        else:
+            qq = np.array([[int(t) for t in vals]], np.uint8)
+            _, aux = o.paper_pack_w2(np.zeros((1, 16), np.uint8), np.zeros((1, 16), np.uint16), qq)
+            assert int(aux[0, 0]) == int(want, 16), (fields, hex(int(aux[0, 0])))
+    g = np.random.default_rng(30)
+    codes = synth.uniform_codes(7, 512, 6, 4, g)
+    base, aux = o.paper_pack_w2(codes["signs"], codes["dir"], codes["q"])
+    assert base.dtype == np.uint16 and aux.shape == (7, 4)
+    s, d, q = o.paper_unpack_w2(base, aux)
+    assert np.array_equal(s, codes["signs"]) and np.array_equal(d, codes["dir"])
+    assert np.array_equal(q, codes["q"])
+
+
+def pin_angular_codebook(o):
+    """Eq. 9/10: unit norm and strictly positive entries for any logits; the angles that
+    give the uniform direction (1/sqrt 8, ...) produce it; theta = 0 gives the first axis."""
+    g = np.random.default_rng(40)
+    phi = g.standard_normal((1000, 7)) * 4
+    th = o.angles_from_logits(phi)
+    assert np.all(th > 0) and np.all(th < np.pi / 2)
+    c = o.angular_codebook(th)
+    assert np.allclose(np.linalg.norm(c, axis=1), 1.0, atol=1e-14)
+    assert np.all(c > 0)
+    theta_u = np.array([np.arccos(1 / np.sqrt(8 - i)) for i in range(7)])
+    assert np.allclose(o.angular_codebook(theta_u), np.full(8, 1 / np.sqrt(8)), atol=1e-15)
+    assert np.allclose(o.angular_codebook(np.zeros(7)), np.eye(8)[0])
+
+
+def pin_rel_err(o):
+    """The comparison metric: zero on equal inputs, scale invariant, floored by row RMS."""
+    y = np.array([[1.0, -2.0, 0.0, 4.0]])
+    assert o.rel_err(y, y) == 0
+    assert abs(o.rel_err(y * 1.001, y) - 1e-3) < 1e-12
+    z = y.copy()
+    z[0, 2] = 1e-3
+    rms = np.sqrt(np.mean(y * y))
+    assert abs(o.rel_err(z, y) - 1e-3 / rms) < 1e-15
+
+
+PINS = [pin_worked_radius, pin_spherical_roundtrip, pin_bit_budget, pin_decompose,
+        pin_assign, pin_ls_radius, pin_radius_quant, pin_decode_norm_and_sign,
+        pin_decode_one_hot, pin_gemm_exact_rational, pin_gemm_special_cases,
+        pin_encode_roundtrip_bruteforce, pin_encode_group_params_recovered, pin_w2_layout,
+        pin_angular_codebook, pin_rel_err]
+
+
+@pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
+def test_pin(pin):
+    pin(_ns())
+
+
+# ----------------------------------------------------------------- planted mistakes
+
+def _mut_sign_order(signs):
+    b = np.asarray(signs, dtype=np.uint8)[..., None]
+    bit = (b >> np.arange(7, -1, -1, dtype=np.uint8)) & 1      # reversed bit order
+    return 1.0 - 2.0 * bit.astype(np.float64)
+
+
+def _mut_drop_min(q, gmin, gstep):
+    return O.dequantize_radius(q, np.zeros_like(gmin), gstep)   # dropped offset term
+
+
+def _mut_level_off_by_one(q, gmin, gstep):
+    return O.dequantize_radius(np.asarray(q) + 1, gmin, gstep)
+
+
+def _mut_decode_transposed(codes, cb):
+    c = O.f16_to_f64(cb)
+    r_hat = O.dequantize_radius(codes["q"], codes["gmin"], codes["gstep"])
+    s = O.sign_factors(codes["signs"])
+    cz = c[np.asarray(codes["dir"], dtype=np.int64)][..., ::-1]  # coordinates reversed
+    n, nv = r_hat.shape
+    return (r_hat[..., None] * s * cz).reshape(n, nv * 8)
+
+
+def _mut_step_denominator(r_tilde, v_bits):
+    r_tilde = np.asarray(r_tilde, dtype=np.float64)
+    lo, hi = r_tilde.min(axis=-1), r_tilde.max(axis=-1)
+    return O.f64_to_f16(lo), O.f64_to_f16((hi - lo) / (1 << v_bits))   # 2**V, not 2**V - 1
+
+
+def _mut_ls_norm(wp, cz):
+    return np.linalg.norm(np.asarray(wp, np.float64), axis=-1)     # radius instead of Eq. 6
+
+
+def _mut_aux_order(signs, dir_idx, q):
+    base, aux = O.paper_pack_w2(signs, dir_idx, np.asarray(q))
+    base = (np.asarray(base, np.uint32) & 0x3FFF) | (((np.asarray(q, np.uint32) >> 2) & 3) << 14)
+    lo = np.asarray(q, np.uint32) & 3
+    n, nv = lo.shape
+    aux = np.bitwise_or.reduce(lo.reshape(n, nv // 16, 16) << (2 * np.arange(16)), axis=-1)
+    return base.astype(np.uint16), aux.astype(np.uint32)             # low/high bits swapped
+
+
+def _mut_assign_last_tie(d, cb, chunk=4096):
+    d = np.asarray(d, dtype=np.float64).reshape(-1, 8)
+    c = np.asarray(cb, dtype=np.float64)
+    sc = d @ c.T
+    return (c.shape[0] - 1 - np.argmax(sc[:, ::-1], axis=1)).astype(np.int64)
+
+
+def _mut_gemm_x_transposed(codes, cb, x_bits, row_chunk=256):
+    x = O.f16_to_f64(x_bits)
+    if x.ndim == 1:
+        x = x[None, :]
+    w = O.decode(codes, cb)
+    xr = x.reshape(x.shape[0], -1, 8)[:, :, ::-1].reshape(x.shape)  # x read reversed per vector
+    return xr @ w.T
+
+
+MUTANTS = {
+    "sign_bit_order": dict(sign_factors=_mut_sign_order),
+    "dropped_group_offset": dict(dequantize_radius=_mut_drop_min),
+    "level_off_by_one": dict(dequantize_radius=_mut_level_off_by_one),
+    "codebook_coords_reversed": dict(decode=_mut_decode_transposed),
+    "step_denominator": dict(group_offset_step=_mut_step_denominator),
+    "ls_radius_is_norm": dict(ls_radius=_mut_ls_norm),
+    "aux_bits_swapped": dict(paper_pack_w2=_mut_aux_order),
+    "assign_ties_last": dict(assign_directions=_mut_assign_last_tie),
+    "gemm_activation_order": dict(gemm=_mut_gemm_x_transposed),
+}
+
+
+def _rebind(ns):
+    """Make the mutated helpers visible to the functions that call them (decode, encode,
+    gemm use module globals): run pins against thin wrappers built on the namespace."""
+    def decode(codes, cb):
+        c = O.f16_to_f64(cb)
+        r_hat = ns.dequantize_radius(codes["q"], codes["gmin"], codes["gstep"])
+        s = ns.sign_factors(codes["signs"])
+        vec = r_hat[..., None] * s * c[np.asarray(codes["dir"], dtype=np.int64)]
+        n, nv = r_hat.shape
+        return vec.reshape(n, nv * 8)
+
+    def encode(w, cb, v_bits, params=None):
+        w = np.asarray(w, dtype=np.float64)
+        n, k = w.shape
+        c = O.f16_to_f64(cb)
+        vecs = w.reshape(n, k // 8, 8)
+        neg, wp, _r, d = ns.decompose(vecs)
+        z = ns.assign_directions(d, c).reshape(n, k // 8)
+        rt = ns.ls_radius(wp, c[z]).reshape(n, k // 128, 16)
+        if params is None:
+            gmin, gstep = ns.group_offset_step(rt, v_bits)
+        else:
+            gmin = np.broadcast_to(np.asarray(params[0], np.uint16), (n, k // 128)).copy()
+            gstep = np.broadcast_to(np.asarray(params[1], np.uint16), (n, k // 128)).copy()
+        q = ns.quantize_radius(rt, gmin, gstep, v_bits).reshape(n, k // 8)
+        return {"signs": O.signs_to_bits(neg), "dir": z.astype(np.uint16), "q": q,
+                "gmin": gmin, "gstep": gstep}
+
+    def gemm(codes, cb, x_bits, row_chunk=256):
+        x = O.f16_to_f64(x_bits)
+        if x.ndim == 1:
+            x = x[None, :]
+        return x @ ns.decode(codes, cb).T
+
+    if ns.decode is O.decode:
+        ns.decode = decode
+    if ns.encode is O.encode:
+        ns.encode = encode
+    if ns.gemm is O.gemm:
+        ns.gemm = gemm
+    return ns
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutants_are_caught(name):
+    ns = _rebind(_ns(**MUTANTS[name]))
+    failed = []
+    for pin in PINS:
+        try:
+            pin(ns)
+        except (AssertionError, ValueError, IndexError):
+            failed.append(pin.__name__)
+    assert failed, f"no pin caught mutant {name}"
+
+
+def test_unmutated_rebind_passes():
+    """The wrapper used for mutants is itself faithful: with no mutation every pin passes."""
+    ns = _rebind(_ns())
+    for pin in PINS:
+        pin(ns)
+
+
+def test_synthetic_codebook_on_positive_sphere():
+    """Generated codebooks lie on S^7_+ up to fp16 rounding (each coordinate within 2^-11
+    relative), as the representation requires (Sec. 3.1)."""
+    for d_bits in (4, 6, 8, 13):
+        c = O.f16_to_f64(synth.random_codebook(d_bits, synth.rng(d_bits)))
+        assert np.all(c >= 0)
+        assert np.all(np.abs(np.linalg.norm(c, axis=1) - 1.0) <= 2.0**-10)

@@ -1,0 +1,163 @@
+// Host side of the library: argument validation and packing of logical SPHQuant codes
+// (Sec. 3.1, Eq. 3-7) into the device layout described in sph_layout.h. Pure C++: no HIP
+// headers, so it also builds and runs with g++ on a machine without a GPU.
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "sph_layout.h"
+#include "sph_host.h"
+
+static inline uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+static bool f16_finite(uint16_t b) { return ((b >> 10) & 0x1F) != 0x1F; }
+static bool f16_sign(uint16_t b) { return (b >> 15) != 0; }
+
+int sph_host_check_format(const sph_format* fmt) {
+  if (!fmt) return SPH_ERR_NULL;
+  if (fmt->vec_dim != SPH_VEC || fmt->group_size != SPH_GROUP) return SPH_ERR_UNSUPPORTED_FORMAT;
+  if (sph_kind_of(fmt->dir_bits, fmt->radius_bits) == SPH_KIND_NONE) return SPH_ERR_UNSUPPORTED_FORMAT;
+  return SPH_OK;
+}
+
+int sph_host_check_shape(int64_t n, int64_t k) {
+  if (n < 1 || n > (int64_t(1) << 24)) return SPH_ERR_SHAPE;
+  if (k < SPH_GROUP || k % SPH_GROUP != 0 || k > (int64_t(1) << 20)) return SPH_ERR_SHAPE;
+  return SPH_OK;
+}
+
+int sph_host_layout(const sph_format* fmt, int64_t n, int64_t k, uint64_t off[8], uint64_t* total) {
+  int st = sph_host_check_format(fmt);
+  if (st) return st;
+  st = sph_host_check_shape(n, k);
+  if (st) return st;
+  const int kind = sph_kind_of(fmt->dir_bits, fmt->radius_bits);
+  const uint64_t nt = (uint64_t)((n + SPH_TILE_ROWS - 1) / SPH_TILE_ROWS);
+  const uint64_t nv = (uint64_t)(k / SPH_VEC), ng = (uint64_t)(k / SPH_GROUP);
+  uint64_t p = 0;
+  for (int i = 0; i < 8; ++i) off[i] = 0;
+  off[SPH_OFF_A] = p;
+  p = align_up(p + nt * nv * 4 * sph_a_dwords(kind), SPH_ALIGN);
+  off[SPH_OFF_B] = p;
+  p = align_up(p + nt * nv * 4 * sph_b_dwords(kind), SPH_ALIGN);
+  off[SPH_OFF_PARAMS] = p;
+  p = align_up(p + nt * ng * SPH_TILE_ROWS * 4, SPH_ALIGN);
+  off[SPH_OFF_TABLES] = p;
+  p = align_up(p + sph_table_bytes(kind, fmt->dir_bits), SPH_ALIGN);
+  off[SPH_OFF_CODEBOOK] = p;
+  p = align_up(p + ((uint64_t)16 << fmt->dir_bits), SPH_ALIGN);
+  *total = p;
+  return SPH_OK;
+}
+
+int sph_host_check_codes(const sph_format* fmt, int64_t n, int64_t k, const uint8_t* signs,
+                         const uint16_t* dir_idx, const uint8_t* radius_code, const uint16_t* gmin,
+                         const uint16_t* gstep, const uint16_t* codebook) {
+  if (!signs || !dir_idx || !radius_code || !gmin || !gstep || !codebook) return SPH_ERR_NULL;
+  const int64_t nvec = n * (k / SPH_VEC), ngrp = n * (k / SPH_GROUP);
+  const uint32_t dmax = 1u << fmt->dir_bits, qmax = 1u << fmt->radius_bits;
+  for (int64_t i = 0; i < nvec; ++i)
+    if (dir_idx[i] >= dmax || radius_code[i] >= qmax) return SPH_ERR_CODE_RANGE;
+  for (int64_t i = 0; i < ngrp; ++i) {
+    if (!f16_finite(gmin[i])) return SPH_ERR_BAD_VALUE;
+    if (!f16_finite(gstep[i]) || f16_sign(gstep[i])) return SPH_ERR_BAD_VALUE;
+  }
+  for (int64_t i = 0; i < ((int64_t)SPH_VEC << fmt->dir_bits); ++i)
+    if (!f16_finite(codebook[i]) || f16_sign(codebook[i])) return SPH_ERR_BAD_VALUE;
+  return SPH_OK;
+}
+
+// One row's code, or zeros for a padding row.
+struct Code {
+  uint32_t s, z, q;
+};
+
+void sph_host_pack(const sph_format* fmt, int64_t n, int64_t k, const uint8_t* signs,
+                   const uint16_t* dir_idx, const uint8_t* radius_code, const uint16_t* gmin,
+                   const uint16_t* gstep, const uint16_t* codebook, const uint64_t off[8],
+                   uint8_t* blob) {
+  const int kind = sph_kind_of(fmt->dir_bits, fmt->radius_bits);
+  const int D = fmt->dir_bits;
+  const int64_t nt = (n + SPH_TILE_ROWS - 1) / SPH_TILE_ROWS, nv = k / SPH_VEC, ng = k / SPH_GROUP;
+  const int adw = sph_a_dwords(kind), bdw = sph_b_dwords(kind);
+  uint32_t* A = (uint32_t*)(blob + off[SPH_OFF_A]);
+  uint32_t* B = (uint32_t*)(blob + off[SPH_OFF_B]);
+  uint32_t* P = (uint32_t*)(blob + off[SPH_OFF_PARAMS]);
+
+  for (int64_t t = 0; t < nt; ++t) {
+    for (int64_t v = 0; v < nv; ++v) {
+      Code c[SPH_TILE_ROWS];
+      for (int r = 0; r < SPH_TILE_ROWS; ++r) {
+        const int64_t row = t * SPH_TILE_ROWS + r;
+        if (row < n) {
+          const int64_t i = row * nv + v;
+          c[r] = {signs[i], dir_idx[i], radius_code[i]};
+        } else {
+          c[r] = {0, 0, 0};
+        }
+      }
+      uint32_t* a = A + (t * nv + v) * adw;
+      uint32_t* b = B + (t * nv + v) * bdw;
+      for (int i = 0; i < adw; ++i) a[i] = 0;
+      for (int i = 0; i < bdw; ++i) b[i] = 0;
+      switch (kind) {
+        case SPH_KIND_W2:
+          for (int i = 0; i < 8; ++i) {
+            const Code& e = c[2 * i];
+            const Code& o = c[2 * i + 1];
+            const uint32_t fe = (e.s & 15) | (e.z << 4) | ((e.s >> 4) << 10);
+            const uint32_t fo = (o.s & 15) | (o.z << 4) | ((o.s >> 4) << 10);
+            a[i] = fe | (fo << 14) | (e.q << 28);
+            b[0] |= o.q << (4 * i);
+          }
+          break;
+        case SPH_KIND_NIB16:
+          for (int r = 0; r < 16; ++r) {
+            const uint32_t f = (c[r].s & 15) | (c[r].z << 4) | ((c[r].s >> 4) << (4 + D)) | (c[r].q << (8 + D));
+            a[r / 2] |= (f & 0xFFFF) << (16 * (r % 2));
+          }
+          break;
+        case SPH_KIND_NIB16Q8:
+          for (int r = 0; r < 16; ++r) {
+            const uint32_t f = (c[r].s & 15) | (c[r].z << 4) | ((c[r].s >> 4) << 12);
+            a[r / 2] |= (f & 0xFFFF) << (16 * (r % 2));
+            b[r / 4] |= (c[r].q & 0xFF) << (8 * (r % 4));
+          }
+          break;
+        case SPH_KIND_CB13:
+          for (int r = 0; r < 16; ++r) {
+            a[r / 4] |= (c[r].s & 0xFF) << (8 * (r % 4));
+            b[r / 2] |= ((c[r].z & 0x1FFF) | (c[r].q << 13)) << (16 * (r % 2));
+          }
+          break;
+      }
+    }
+    for (int64_t g = 0; g < ng; ++g)
+      for (int r = 0; r < SPH_TILE_ROWS; ++r) {
+        const int64_t row = t * SPH_TILE_ROWS + r;
+        uint32_t pr = 0;
+        if (row < n) pr = (uint32_t)gmin[row * ng + g] | ((uint32_t)gstep[row * ng + g] << 16);
+        P[(t * ng + g) * SPH_TILE_ROWS + r] = pr;
+      }
+  }
+
+  // Lookup tables derived from the codebook.
+  uint16_t* T = (uint16_t*)(blob + off[SPH_OFF_TABLES]);
+  const uint32_t entries = 1u << D;
+  if (kind == SPH_KIND_CB13) {
+    for (uint32_t z = 0; z < entries; ++z)
+      for (int j = 0; j < 8; ++j) T[z * 8 + j] = codebook[z * 8 + j];
+  } else {
+    uint16_t* Tlo = T;
+    uint16_t* Thi = T + (size_t)entries * 16 * 4;
+    for (uint32_t z = 0; z < entries; ++z)
+      for (uint32_t s = 0; s < 16; ++s)
+        for (int j = 0; j < 4; ++j) {
+          const uint16_t flip = ((s >> j) & 1) ? 0x8000 : 0;
+          Tlo[(z * 16 + s) * 4 + j] = codebook[z * 8 + j] ^ flip;
+          Thi[(s * entries + z) * 4 + j] = codebook[z * 8 + 4 + j] ^ flip;
+        }
+  }
+  uint16_t* C = (uint16_t*)(blob + off[SPH_OFF_CODEBOOK]);
+  std::memcpy(C, codebook, sizeof(uint16_t) * 8 * entries);
+}

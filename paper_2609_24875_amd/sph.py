@@ -1,0 +1,223 @@
+"""Python binding of libsph (include/sph.h): argument marshalling only.
+
+Every step of the decode path runs in the HIP kernels of ``libsph.so``; PyTorch supplies device
+memory and the current stream. There is no CPU fallback: if the library has not been built,
+importing works but every call raises ``SphLibraryMissing``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsph.so")
+
+SPH_F16, SPH_F32 = 0, 1
+
+STATUS = {
+    0: "SPH_OK", 1: "SPH_ERR_NULL", 2: "SPH_ERR_SHAPE", 3: "SPH_ERR_UNSUPPORTED_FORMAT",
+    4: "SPH_ERR_CODE_RANGE", 5: "SPH_ERR_BAD_VALUE", 6: "SPH_ERR_BUFFER_TOO_SMALL",
+    7: "SPH_ERR_HIP", 8: "SPH_ERR_BAD_DESCRIPTOR",
+}
+
+# Every symbol include/sph.h declares.
+EXPORTS = ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
+           "sph_workspace_bytes", "sph_unpack", "sph_format_supported", "sph_status_str")
+
+FORMATS = {
+    "W2": (6, 4), "W3": (13, 3), "W2_cfg": (4, 4), "W3_cfg": (8, 8), "W2_16": (6, 2),
+}
+
+
+class SphLibraryMissing(RuntimeError):
+    pass
+
+
+class SphError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {STATUS.get(status, status)} ({status})")
+
+
+class CFormat(ctypes.Structure):
+    _fields_ = [("vec_dim", ctypes.c_int32), ("dir_bits", ctypes.c_int32),
+                ("radius_bits", ctypes.c_int32), ("group_size", ctypes.c_int32)]
+
+
+class CWeights(ctypes.Structure):
+    _fields_ = [("fmt", CFormat), ("n", ctypes.c_int64), ("k", ctypes.c_int64),
+                ("d_base", ctypes.c_void_p), ("bytes", ctypes.c_size_t),
+                ("off", ctypes.c_uint64 * 8), ("layout_version", ctypes.c_uint32),
+                ("magic", ctypes.c_uint32)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libsph.so and declare its signatures. Raises SphLibraryMissing if not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise SphLibraryMissing(f"{path} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(path)
+    P, I64, SZ, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t, ctypes.c_int
+    pf, pw = ctypes.POINTER(CFormat), ctypes.POINTER(CWeights)
+    lib.sph_packed_bytes.argtypes = [pf, I64, I64, ctypes.POINTER(SZ)]
+    lib.sph_pack_weights.argtypes = [pf, I64, I64, P, P, P, P, P, P, P, SZ, P, pw]
+    lib.sph_gemv.argtypes = [pw, P, P, I32, P, SZ, P]
+    lib.sph_gemm_small.argtypes = [pw, P, I64, I64, P, I64, I32, P, SZ, P]
+    lib.sph_workspace_bytes.argtypes = [pw, I64, ctypes.POINTER(SZ)]
+    lib.sph_unpack.argtypes = [pw, P, P, P, P]
+    lib.sph_format_supported.argtypes = [pf]
+    lib.sph_format_supported.restype = I32
+    lib.sph_status_str.argtypes = [I32]
+    lib.sph_status_str.restype = ctypes.c_char_p
+    for name in ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
+                 "sph_workspace_bytes", "sph_unpack"):
+        getattr(lib, name).restype = I32
+    _lib = lib
+    return lib
+
+
+def _check(st: int, what: str):
+    if st != 0:
+        raise SphError(st, what)
+
+
+def make_format(dir_bits: int, radius_bits: int, vec_dim: int = 8, group_size: int = 128) -> CFormat:
+    return CFormat(vec_dim, dir_bits, radius_bits, group_size)
+
+
+def format_supported(dir_bits: int, radius_bits: int) -> bool:
+    return bool(load_library().sph_format_supported(ctypes.byref(make_format(dir_bits, radius_bits))))
+
+
+def status_str(status: int) -> str:
+    return load_library().sph_status_str(status).decode()
+
+
+def packed_bytes(dir_bits: int, radius_bits: int, n: int, k: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().sph_packed_bytes(ctypes.byref(make_format(dir_bits, radius_bits)),
+                                           n, k, ctypes.byref(out)), "sph_packed_bytes")
+    return out.value
+
+
+def _stream_handle(stream=None) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _host(a, dtype) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a), dtype=dtype)
+
+
+@dataclass
+class SphWeights:
+    """A packed matrix: the device buffer (a torch uint8 tensor) and the C descriptor."""
+    desc: CWeights
+    buffer: object
+    n: int
+    k: int
+    dir_bits: int
+    radius_bits: int
+
+    @property
+    def nbytes(self) -> int:
+        return int(self.desc.bytes)
+
+
+def pack(dir_bits: int, radius_bits: int, codes: dict, codebook, device="cuda", stream=None,
+         buffer=None) -> SphWeights:
+    """Pack logical codes (see ``synth``) into a device buffer (allocated unless ``buffer`` is
+    given) with sph_pack_weights."""
+    import torch
+    lib = load_library()
+    signs = _host(codes["signs"], np.uint8)
+    n, nv = signs.shape
+    k = nv * 8
+    dirs = _host(codes["dir"], np.uint16)
+    q = _host(codes["q"], np.uint8)
+    gmin = _host(codes["gmin"], np.uint16)
+    gstep = _host(codes["gstep"], np.uint16)
+    cb = _host(codebook, np.uint16)
+    fmt = make_format(dir_bits, radius_bits)
+    need = packed_bytes(dir_bits, radius_bits, n, k)
+    if buffer is None:
+        buffer = torch.empty(need, dtype=torch.uint8, device=device)
+    w = CWeights()
+    st = lib.sph_pack_weights(ctypes.byref(fmt), n, k, signs.ctypes.data, dirs.ctypes.data,
+                              q.ctypes.data, gmin.ctypes.data, gstep.ctypes.data, cb.ctypes.data,
+                              buffer.data_ptr(), buffer.numel(), _stream_handle(stream),
+                              ctypes.byref(w))
+    _check(st, "sph_pack_weights")
+    return SphWeights(w, buffer, n, k, dir_bits, radius_bits)
+
+
+def workspace_bytes(w: SphWeights, m: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().sph_workspace_bytes(ctypes.byref(w.desc), m, ctypes.byref(out)),
+           "sph_workspace_bytes")
+    return out.value
+
+
+def _workspace(w: SphWeights, m: int, device):
+    import torch
+    nb = workspace_bytes(w, m)
+    if nb == 0:
+        return None, 0
+    ws = torch.zeros(nb, dtype=torch.uint8, device=device)
+    return ws, nb
+
+
+def gemv(w: SphWeights, x, out=None, out_dtype=None, stream=None):
+    """y = W^ x for a device fp16 vector x[k] (sph_gemv)."""
+    import torch
+    out_dtype = out_dtype or torch.float32
+    if out is None:
+        out = torch.empty(w.n, dtype=out_dtype, device=x.device)
+    ws, nb = _workspace(w, 1, x.device)
+    st = load_library().sph_gemv(ctypes.byref(w.desc), x.data_ptr(), out.data_ptr(),
+                                 SPH_F16 if out.dtype == torch.float16 else SPH_F32,
+                                 ws.data_ptr() if ws is not None else None, nb,
+                                 _stream_handle(stream))
+    _check(st, "sph_gemv")
+    return out
+
+
+def gemm_small(w: SphWeights, x, out=None, out_dtype=None, stream=None):
+    """Y = X W^T for device fp16 X[m][k], 1 <= m <= 32 (sph_gemm_small)."""
+    import torch
+    out_dtype = out_dtype or torch.float32
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, w.n), dtype=out_dtype, device=x.device)
+    ws, nb = _workspace(w, m, x.device)
+    st = load_library().sph_gemm_small(ctypes.byref(w.desc), x.data_ptr(), m, x.stride(0),
+                                       out.data_ptr(), out.stride(0),
+                                       SPH_F16 if out.dtype == torch.float16 else SPH_F32,
+                                       ws.data_ptr() if ws is not None else None, nb,
+                                       _stream_handle(stream))
+    _check(st, "sph_gemm_small")
+    return out
+
+
+def unpack(w: SphWeights, stream=None) -> dict:
+    """Logical codes read back through the kernels' field extraction (sph_unpack)."""
+    import torch
+    dev = w.buffer.device
+    nv = w.k // 8
+    s = torch.empty((w.n, nv), dtype=torch.uint8, device=dev)
+    d = torch.empty((w.n, nv), dtype=torch.int16, device=dev)
+    q = torch.empty((w.n, nv), dtype=torch.uint8, device=dev)
+    st = load_library().sph_unpack(ctypes.byref(w.desc), s.data_ptr(), d.data_ptr(), q.data_ptr(),
+                                   _stream_handle(stream))
+    _check(st, "sph_unpack")
+    torch.cuda.synchronize(dev)
+    return {"signs": s.cpu().numpy(), "dir": d.cpu().numpy().view(np.uint16), "q": q.cpu().numpy()}

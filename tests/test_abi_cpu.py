@@ -1,0 +1,141 @@
+"""CPU checks of the C-ABI library: it loads, exports every function include/sph.h declares, and
+its host-side validation returns the documented status codes before any HIP call is made.
+No call here launches a kernel or copies memory."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth
+import paper_2609_24875_amd as pkg
+from paper_2609_24875_amd import sph as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sph.h")
+
+needs_lib = pytest.mark.skipif(not os.path.exists(pkg.LIB_PATH), reason="libsph.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sph_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_binding_exports():
+    assert declared_functions() == sorted(pkg.EXPORTS)
+
+
+@needs_lib
+def test_library_exports_every_declared_symbol():
+    lib = pkg.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+@needs_lib
+def test_status_strings():
+    for code in range(9):
+        assert pkg.status_str(code) and pkg.status_str(code) != "unknown status"
+    assert pkg.status_str(99) == "unknown status"
+
+
+@needs_lib
+@pytest.mark.parametrize("d,v,ok", [(6, 4, True), (13, 3, True), (4, 4, True), (8, 8, True),
+                                    (6, 2, True), (5, 3, True), (6, 3, False), (13, 4, False),
+                                    (2, 4, False), (16, 4, False)])
+def test_format_supported(d, v, ok):
+    assert pkg.format_supported(d, v) == ok
+
+
+@needs_lib
+def test_packed_bytes_accounts_for_every_stream():
+    # W2 4096 x 12288: records 36 B per 16 rows x 8 columns; params 4 B per 16 rows x 128 cols.
+    n, k = 4096, 12288
+    got = pkg.packed_bytes(6, 4, n, k)
+    codes = (n // 16) * (k // 8) * 36           # 36 B per (16 rows x 8 columns) record
+    params = n * (k // 128) * 4                  # fp16 (offset, step) per row and group
+    tables = 2 * 64 * 16 * 8 + 64 * 16          # nibble tables + raw codebook
+    assert codes + params + tables <= got <= codes + params + tables + 5 * 256
+    # padding to 16-row tiles
+    assert pkg.packed_bytes(6, 4, 17, 128) == pkg.packed_bytes(6, 4, 32, 128)
+
+
+@needs_lib
+@pytest.mark.parametrize("n,k", [(0, 128), (-1, 128), (16, 0), (16, 100), (16, 130), (1 << 25, 128)])
+def test_packed_bytes_shape_errors(n, k):
+    with pytest.raises(pkg.SphError) as e:
+        pkg.packed_bytes(6, 4, n, k)
+    assert e.value.status == 2
+
+
+def _codes(n=20, k=256, D=6, V=4, seed=0):
+    g = synth.rng(seed)
+    c = synth.uniform_codes(n, k, D, V, g)
+    c["gmin"], c["gstep"] = synth.row_scale_group_params(n, k, V, g)
+    return c, synth.random_codebook(D, g)
+
+
+def _pack_status(codes, cb, D=6, V=4, buf=0x10000, nbytes=1 << 30, fmt=None):
+    lib = pkg.load_library()
+    fmt = fmt or B.make_format(D, V)
+    n, nv = codes["signs"].shape
+    arrs = [np.ascontiguousarray(codes[key]) for key in ("signs", "dir", "q", "gmin", "gstep")]
+    cb = np.ascontiguousarray(cb)
+    w = B.CWeights()
+    return lib.sph_pack_weights(ctypes.byref(fmt), n, nv * 8, *[a.ctypes.data for a in arrs],
+                                cb.ctypes.data, buf, nbytes, None, ctypes.byref(w))
+
+
+@needs_lib
+def test_pack_validation_errors():
+    codes, cb = _codes()
+    assert _pack_status(codes, cb, fmt=B.make_format(6, 4, vec_dim=4)) == 3
+    assert _pack_status(codes, cb, fmt=B.make_format(6, 4, group_size=64)) == 3
+    assert _pack_status(codes, cb, fmt=B.make_format(7, 4)) == 3
+    bad = dict(codes, dir=codes["dir"].copy())
+    bad["dir"][3, 5] = 64
+    assert _pack_status(bad, cb) == 4
+    bad = dict(codes, q=codes["q"].copy())
+    bad["q"][0, 0] = 16
+    assert _pack_status(bad, cb) == 4
+    for key, val in (("gstep", 0xBC00), ("gstep", 0x7C00), ("gmin", 0x7E00)):
+        bad = dict(codes, **{key: codes[key].copy()})
+        bad[key][1, 1] = val                   # -1.0, +inf, NaN
+        assert _pack_status(bad, cb) == 5, (key, hex(val))
+    bcb = cb.copy()
+    bcb[2, 3] = 0x8000 | bcb[2, 3]             # negative entry
+    assert _pack_status(codes, bcb) == 5
+    assert _pack_status(codes, cb, nbytes=100) == 6
+    assert _pack_status(codes, cb, buf=0x10001) == 2
+    assert _pack_status(codes, cb, buf=0) == 1
+
+
+@needs_lib
+def test_compute_calls_reject_bad_descriptor_before_any_hip_call():
+    lib = pkg.load_library()
+    w = B.CWeights()                           # never filled by sph_pack_weights
+    assert lib.sph_gemv(ctypes.byref(w), 0x10000, 0x20000, 1, None, 0, None) == 8
+    assert lib.sph_gemm_small(ctypes.byref(w), 0x10000, 4, 256, 0x20000, 256, 1, None, 0, None) == 8
+    assert lib.sph_unpack(ctypes.byref(w), 0x1000, 0x2000, 0x3000, None) == 8
+    assert lib.sph_gemv(None, 0x10000, 0x20000, 1, None, 0, None) == 1
+    out = ctypes.c_size_t(0)
+    assert lib.sph_workspace_bytes(ctypes.byref(w), 1, ctypes.byref(out)) == 8
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(pkg.SphLibraryMissing):
+        _load_fresh(str(tmp_path / "missing.so"))
+
+
+def _load_fresh(path):
+    saved = B._lib
+    B._lib = None
+    try:
+        return B.load_library(path)
+    finally:
+        B._lib = saved

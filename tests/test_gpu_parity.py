@@ -1,0 +1,175 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Bars: unpacked codes bit-exact; outputs within rel_err <= 2e-3 (max |y - y*| over
+max(|y*|, row RMS of y*)), the tolerance the target states for fp32 accumulation against the
+fp64 oracle. The vector-ALU path (m <= 8) forms exact fp16 products and only rounds its fp32
+sums, so it is also held to a much tighter a-priori bound.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import sph as O
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2609_24875_amd as pkg  # noqa: E402
+
+DEV = torch.device("cuda:0")
+TOL = 2e-3
+FMTS = ["W2", "W3", "W2_cfg", "W3_cfg", "W2_16"]
+
+
+def to_dev_f16(bits: np.ndarray):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(DEV).view(torch.float16)
+
+
+def uniform_case(fmt, n, k, seed):
+    D, V = synth.FORMATS[fmt]
+    g = synth.rng(seed, n, k, synth.STREAM_CODES)
+    codes = synth.uniform_codes(n, k, D, V, g)
+    codes["gmin"], codes["gstep"] = synth.row_scale_group_params(n, k, V, g)
+    cb = synth.random_codebook(D, synth.rng(seed, n, k, synth.STREAM_CODEBOOK))
+    return D, V, codes, cb
+
+
+def encoded_case(fmt, n, k, seed):
+    D, V = synth.FORMATS[fmt]
+    cb = synth.random_codebook(D, synth.rng(seed, n, k, synth.STREAM_CODEBOOK))
+    w = synth.outlier_gaussian_weights(n, k, synth.rng(seed, n, k, synth.STREAM_WEIGHTS))
+    return D, V, O.encode(w, cb, V), cb
+
+
+def apriori_bound(codes, cb, x):
+    """sum_k |w^_nk x_k| per output: the scale of fp32 summation error."""
+    w = np.abs(O.decode(codes, cb))
+    return np.abs(O.f16_to_f64(x)) @ w.T
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_unpack_bit_exact(fmt):
+    D, V, codes, cb = uniform_case(fmt, 87, 640, 1)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    back = pkg.unpack(w)
+    for key in ("signs", "dir", "q"):
+        assert np.array_equal(back[key], codes[key]), key
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("n,k", [(87, 640), (16, 128), (1, 256), (300, 2048)])
+def test_gemv_parity(fmt, n, k):
+    D, V, codes, cb = uniform_case(fmt, n, k, 2)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = synth.activations(1, k, synth.rng(2, n, k, synth.STREAM_X))
+    y = pkg.gemv(w, to_dev_f16(x)[0]).cpu().numpy()
+    ref = O.gemv(codes, cb, x)
+    assert O.rel_err(y, ref) <= TOL
+    # exact products + fp32 sums: |error| <= K * 2^-23 * sum|w x| (a loose a-priori bound)
+    bound = apriori_bound(codes, cb, x)[0]
+    assert np.all(np.abs(y - ref) <= k * 2.0**-23 * bound + 1e-30)
+    y16 = pkg.gemv(w, to_dev_f16(x)[0], out_dtype=torch.float16).cpu().numpy().astype(np.float64)
+    assert np.array_equal(y16, y.astype(np.float16).astype(np.float64))
+
+
+@pytest.mark.parametrize("fmt", ["W2", "W3", "W2_cfg", "W3_cfg"])
+def test_gemv_parity_encoded(fmt):
+    D, V, codes, cb = encoded_case(fmt, 70, 1024, 3)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = synth.activations(1, 1024, synth.rng(3, 0, 0, synth.STREAM_X))
+    y = pkg.gemv(w, to_dev_f16(x)[0]).cpu().numpy()
+    assert O.rel_err(y, O.gemv(codes, cb, x)) <= TOL
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("m", [2, 3, 4, 5, 8, 9, 16, 17, 24, 32])
+def test_gemm_small_parity(fmt, m):
+    n, k = 75, 1152
+    D, V, codes, cb = uniform_case(fmt, n, k, 4)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = synth.activations(m, k, synth.rng(4, m, k, synth.STREAM_X))
+    y = pkg.gemm_small(w, to_dev_f16(x)).cpu().numpy()
+    ref = O.gemm(codes, cb, x)
+    err = O.rel_err(y, ref)
+    assert err <= TOL, err
+    if m <= 8:
+        bound = apriori_bound(codes, cb, x)
+        assert np.all(np.abs(y - ref) <= k * 2.0**-23 * bound + 1e-30)
+
+
+def test_gemm_small_strided_and_fp16_out():
+    D, V, codes, cb = uniform_case("W2", 48, 512, 5)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    for m in (3, 20):
+        x = synth.activations(m, 512, synth.rng(5, m, 0, synth.STREAM_X))
+        big = torch.zeros((m, 512 + 64), dtype=torch.float16, device=DEV)
+        big[:, :512] = to_dev_f16(x)
+        out = torch.full((m, 64), 7.0, dtype=torch.float16, device=DEV)
+        pkg.gemm_small(w, big[:, :512], out=out[:, :48])
+        ref = O.gemm(codes, cb, x)
+        assert O.rel_err(out[:, :48].float().cpu().numpy(), ref) <= TOL
+        assert torch.all(out[:, 48:] == 7.0)            # nothing written past n
+
+
+def test_unit_activation_returns_decoded_column():
+    """x = e_c picks column c of W^: every weight the kernel rebuilds is checked (Eq. 4)."""
+    D, V, codes, cb = uniform_case("W2", 33, 256, 6)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    dense = O.decode(codes, cb)
+    eye = np.eye(256)
+    for c0 in range(0, 256, 32):
+        x = synth.f16_bits(eye[c0:c0 + 8])                         # 8 unit vectors at once
+        y = pkg.gemm_small(w, to_dev_f16(x)).cpu().numpy()
+        assert np.array_equal(y, dense[:, c0:c0 + 8].T.astype(np.float32))
+
+
+def test_deterministic():
+    D, V, codes, cb = uniform_case("W2", 500, 4096, 7)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = to_dev_f16(synth.activations(1, 4096, synth.rng(7)))[0]
+    a = pkg.gemv(w, x).clone()
+    b = pkg.gemv(w, x).clone()
+    assert torch.equal(a, b)
+
+
+def test_bad_batch_raises():
+    D, V, codes, cb = uniform_case("W2", 16, 128, 8)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = torch.zeros((33, 128), dtype=torch.float16, device=DEV)
+    with pytest.raises(pkg.SphError):
+        pkg.gemm_small(w, x)
+
+
+# --------------------------------------------------------------- full-size workloads
+
+FULL = [
+    ("W2", 1024, 1024, "uniform", 1),        # smallest workload: every output checked
+    ("W2", 4096, 4096, "encoded", 1),        # encoded outlier-laden weights
+    ("W3", 12288, 4096, "uniform", 1),       # 8B-class gate/up, W3
+    ("W3", 4096, 12288, "uniform", 1),       # 8B-class down, W3
+    ("W2", 25600, 5120, "uniform", 8),       # 32B-class gate/up, batch 8
+    ("W2", 5120, 25600, "uniform", 4),       # 32B-class down, batch 4
+    ("W2", 12288, 4096, "uniform", 32),      # matrix-core path
+    ("W3", 4096, 12288, "uniform", 16),
+]
+
+
+@pytest.mark.parametrize("fmt,n,k,kind,m", FULL)
+def test_full_size_sampled(fmt, n, k, kind, m):
+    D, V, codes, cb = (uniform_case if kind == "uniform" else encoded_case)(fmt, n, k, 9)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = synth.activations(m, k, synth.rng(9, m, k, synth.STREAM_X))
+    xd = to_dev_f16(x)
+    y = (pkg.gemv(w, xd[0])[None, :] if m == 1 else pkg.gemm_small(w, xd)).cpu().numpy()
+    g = np.random.default_rng(n + k)
+    rows = np.unique(np.concatenate([[0, n - 1], g.integers(0, n, 48)]))
+    if n * k <= 1 << 21:
+        rows = np.arange(n)
+    ref = O.gemm_rows(codes, cb, x, rows)
+    # Row RMS for the metric's floor is taken over the sampled outputs.
+    assert O.rel_err(y[:, rows], ref) <= TOL

@@ -1,0 +1,252 @@
+"""Benchmark of the SPHQuant decode path on one MI355X.
+
+A step is one decode forward through every linear layer of a backbone: for each of the L layers
+the seven projections (q, k, v, o, gate, up, down) run as sph_gemv (batch 1) or
+sph_gemm_small (batch > 1) on their own packed copy in HBM, so the weight stream is never served
+from the 256 MB Infinity Cache. The step is captured once in a HIP graph and replayed.
+
+Default workload: W2 (8 sign + 6 direction + 4 radius bits per 8-vector), 32B-class shapes
+(q/o 5120x5120, k/v 1024x5120, gate/up 25600x5120, down 5120x25600), 64 layers, batch 1:
+9.12 GB of packed weights per step.
+
+Prints one JSON line: whole-step packed-weight GB/s (`value`), linear-layer tokens/s, the
+roofline of the dominant kernel (the batch-1 GEMV on the 25600x5120 / 5120x25600 shapes), and
+the fp64 CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=3, help="workload id in synth.WORKLOADS")
+    ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--layers", type=int, default=0, help="override layer count (0: workload's)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
+    return ap.parse_args()
+
+
+def make_layer0(wl, fmt, m):
+    """Codes, codebooks and activations of layer 0's matrices (seeded, uniform codes)."""
+    D, V = synth.FORMATS[fmt]
+    mats = []
+    for mi, (label, n, k) in enumerate(wl.shapes):
+        g = synth.rng(wl_id(wl), 0, mi, synth.STREAM_CODES)
+        codes = synth.uniform_codes(n, k, D, V, g)
+        codes["gmin"], codes["gstep"] = synth.row_scale_group_params(n, k, V, g)
+        cb = synth.random_codebook(D, synth.rng(wl_id(wl), 0, mi, synth.STREAM_CODEBOOK))
+        x = synth.activations(m, k, synth.rng(wl_id(wl), 0, mi, synth.STREAM_X))
+        mats.append((label, n, k, codes, cb, x))
+    return mats
+
+
+def wl_id(wl):
+    for i, w in synth.WORKLOADS.items():
+        if w is wl:
+            return i
+    return 99
+
+
+def cpu_baseline(mats, budget_s, step_bytes_total, per_mat_bytes, layers):
+    """Time the fp64 oracle (decode + dot) on whole matrices of layer 0 until the budget is
+    used; report packed-weight GB/s over the matrices it finished."""
+    from oracle import sph as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = int(os.environ.get("OMP_NUM_THREADS") or os.cpu_count())
+    done_bytes = 0
+    names = []
+    t0 = time.perf_counter()
+    for (label, n, k, codes, cb, x), nbytes in zip(mats, per_mat_bytes):
+        O.gemm(codes, cb, x)
+        done_bytes += nbytes
+        names.append(f"{label} {n}x{k}")
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    gbs = done_bytes / dt / 1e9
+    return {
+        "value": round(gbs, 4),
+        "unit": "GB/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"layer 0 matrices [{', '.join(names)}] of {layers} layers, {dt:.1f} s; "
+                  f"step-equivalent {step_bytes_total / gbs / 1e9 * 1e3:.0f} ms",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+
+    import paper_2609_24875_amd as pkg
+
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    wl = synth.WORKLOADS[args.workload]
+    fmt = wl.fmt
+    D, V = synth.FORMATS[fmt]
+    m = args.batch
+    layers = args.layers or wl.layers
+    pkg.load_library()
+
+    # ---- inputs: layer 0 generated and packed, then replicated per layer (distinct buffers)
+    t_setup = time.perf_counter()
+    mats = make_layer0(wl, fmt, m)
+    packed = []
+    for label, n, k, codes, cb, x in mats:
+        w0 = pkg.pack(D, V, codes, cb, device=dev)
+        copies = [w0] + [clone_weights(pkg, w0) for _ in range(layers - 1)]
+        xd = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.float16)
+        ys = [torch.empty((m, n), dtype=torch.float32, device=dev) for _ in range(layers)]
+        packed.append((label, n, k, copies, xd, ys))
+    step_bytes = sum(len(p[3]) * p[3][0].nbytes for p in packed)
+    per_mat_bytes = [p[3][0].nbytes for p in packed]
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+
+    def run_step():
+        for li in range(layers):
+            for label, n, k, copies, xd, ys in packed:
+                if m == 1:
+                    pkg.gemv(copies[li], xd[0], out=ys[li][0])
+                else:
+                    pkg.gemm_small(copies[li], xd, out=ys[li])
+
+    run_step()                                  # first calls outside capture
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        run_step()
+    torch.cuda.synchronize()
+
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):             # replays, and the events, on one stream
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    gbs = step_bytes / (ms / 1e3) / 1e9
+
+    # ---- dominant kernel: batch-m decode on the largest shapes, launched back to back over the
+    # per-layer copies inside a graph; average launch duration from HIP events on its stream.
+    big = [p for p in packed if p[1] * p[2] == max(q[1] * q[2] for q in packed)]
+    dom_launches = []
+    for label, n, k, copies, xd, ys in big:
+        for li in range(layers):
+            dom_launches.append((copies[li], xd, ys[li]))
+    g2 = torch.cuda.CUDAGraph()
+    s2 = torch.cuda.Stream()
+    with torch.cuda.graph(g2, stream=s2):
+        for w, xd, y in dom_launches:
+            if m == 1:
+                pkg.gemv(w, xd[0], out=y[0])
+            else:
+                pkg.gemm_small(w, xd, out=y)
+    torch.cuda.synchronize()
+    reps = max(3, args.steps // 2)
+    d0 = torch.cuda.Event(enable_timing=True)
+    d1 = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s2):
+        for _ in range(2):
+            g2.replay()
+        torch.cuda.synchronize()
+        d0.record(s2)
+        for _ in range(reps):
+            g2.replay()
+        d1.record(s2)
+    torch.cuda.synchronize()
+    dom_us = d0.elapsed_time(d1) * 1e3 / (reps * len(dom_launches))
+    dom_bytes = sum(w.nbytes for w, _, _ in dom_launches) / len(dom_launches)
+    dom_gbs = dom_bytes / (dom_us * 1e-6) / 1e9
+
+    out = {
+        "metric": "packed-weight GB/s & % HBM peak for W2/W3 sph_gemv; linear-layer tokens/s",
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16 activations, fp32 accumulation",
+        "data": "synthetic: seeded uniform codes and per-row radius scales, random positive "
+                "unit codebook, fp16 N(0,1) activations",
+        "config": {
+            "workload": f"{wl.name}-m{m}",
+            "format": f"{fmt} (8 sign + {D} direction + {V} radius bits per 8-vector)",
+            "layers": layers,
+            "shapes": [f"{label} {n}x{k}" for label, n, k, *_ in packed],
+            "batch": m,
+            "packed_bytes_per_step": step_bytes,
+            "launches_per_step": layers * len(packed),
+            "graph": True,
+        },
+        "tokens_per_s": round(m / (ms / 1e3), 2),
+        "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "roofline": {
+            "kernel": f"k_gemm_valu<W2,M={m}> on {', '.join(f'{p[1]}x{p[2]}' for p in big)}"
+            if m <= 8 else f"k_gemm_mfma<W2> on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
+            "bound": "hbm",
+            "achieved": round(dom_gbs, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "avg_launch_us": round(dom_us, 3),
+            "bytes_per_launch": int(dom_bytes),
+        },
+        "setup_s": round(setup_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        mats_cpu = [(label, n, k, codes, cb, x) for label, n, k, codes, cb, x in mats]
+        out["cpu_baseline"] = cpu_baseline(mats_cpu, args.cpu_sample_seconds, step_bytes,
+                                           per_mat_bytes, layers)
+    print(json.dumps(out), flush=True)
+
+
+def clone_weights(pkg, w):
+    """A second packed copy in its own device buffer (same layout, new base pointer)."""
+    buf = w.buffer.clone()
+    d = type(w.desc).from_buffer_copy(w.desc)
+    d.d_base = buf.data_ptr()
+    return pkg.SphWeights(d, buf, w.n, w.k, w.dir_bits, w.radius_bits)
+
+
+if __name__ == "__main__":
+    main()

@@ -98,7 +98,9 @@ sph_status sph_pack_weights(const sph_format* fmt, int64_t n, int64_t k, const u
 /* y = W^ x for one fp16 activation vector (batch 1): the fused dequantise-and-multiply GEMV of
  * Sec. 3.4 / App. D. d_x: device fp16[k]; d_y: device [n] of y_dtype (fp32 accumulation, then
  * rounded to fp16 when y_dtype is SPH_F16). d_ws/ws_bytes: device workspace of at least
- * sph_workspace_bytes(w, 1) bytes (may be NULL when that is 0). Asynchronous on `stream`. */
+ * sph_workspace_bytes(w, 1) bytes (see there; may be NULL when that is 0). The split-K sums are
+ * combined in a fixed order, so repeated calls give bitwise identical results.
+ * Asynchronous on `stream`. */
 sph_status sph_gemv(const sph_weights* w, const void* d_x, void* d_y, sph_dtype y_dtype,
                     void* d_ws, size_t ws_bytes, void* stream);
 
@@ -110,7 +112,11 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
                           int64_t ldy, sph_dtype y_dtype, void* d_ws, size_t ws_bytes,
                           void* stream);
 
-/* Device workspace needed by sph_gemv (m = 1) or sph_gemm_small for this matrix and batch. */
+/* Device workspace needed by sph_gemv (m = 1) or sph_gemm_small for this matrix and batch on
+ * the current device (0 when the call needs none; d_ws may then be NULL). The workspace holds
+ * split-K partial sums and one arrival counter per 16-row tile: it must be 256-byte aligned and
+ * zero-filled before its first use, every call leaves it zero-filled again, and calls that may
+ * run concurrently must not share one. */
 sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes);
 
 /* Read the packed matrix back as logical codes, on the device, with the same bit extraction the

@@ -8,15 +8,16 @@
 //  - vector-ALU path (batch 1..8): a lane owns one vector position of a tile and decodes up to
 //    16 rows of it from 16-byte loads; signs are folded into two nibble-indexed lookup tables in
 //    LDS, so the signed direction costs two 8-byte LDS reads and no sign arithmetic; products
-//    use v_dot2_f32_f16 (exact fp16 products, fp32 sums); the waves of a workgroup split K and
-//    meet in LDS, so the reduction order is fixed and results are bitwise reproducible;
+//    use v_dot2_f32_f16 (exact fp16 products, fp32 sums); persistent waves walk balanced
+//    (tile, K-segment) items and split-K partial sums are added in a fixed order, so results
+//    are bitwise reproducible;
 //  - matrix-core path (batch 9..32): each lane decodes one (row, vector) into the A operand of
 //    v_mfma_f32_16x16x32_f16 (weights rounded once to fp16), activations form the B operand.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <cstring>
-#include <mutex>
 #include <vector>
 
 #include "sph_host.h"
@@ -39,7 +40,11 @@ struct KArgs {
   int64_t ldy;
   int y_f16;
   int n, nt, nv, ng, m;
-  int wpt;            // waves per tile
+  int wpt;            // waves per tile (matrix-core kernel)
+  // vector-ALU work plan: items = nt * S, each `cps` chunks of one tile
+  int nc, cps, S, items;
+  int wpb, gw;        // waves per workgroup, waves in the grid
+  uint64_t* ws_slot;  // [nt][S][M][16] tagged partial sums (S > 1), flags zero between calls
 };
 
 // ------------------------------------------------------------------------------------------
@@ -149,32 +154,6 @@ __device__ __forceinline__ void load_dw(uint32_t (&d)[N], const uint32_t* p) {
   }
 }
 
-// Reduce-scatter of CNT values across the lanes that differ in bits DMIN..32 of the lane id:
-// after it, every lane holds CNT >> steps sums (flattened indices base .. base+CNT'-1) and the
-// steps left once a single value remains are plain butterfly all-reductions.
-template <int CNT, int DIST, int DMIN>
-__device__ __forceinline__ void reduce_scatter(float* v, int lane, int& base) {
-  if constexpr (DIST >= DMIN) {
-    if constexpr (CNT > 1) {
-      constexpr int HALF = CNT / 2;
-      const bool bit = (lane & DIST) != 0;
-#pragma unroll
-      for (int i = 0; i < HALF; ++i) {
-        const float send = bit ? v[i] : v[i + HALF];
-        const float keep = bit ? v[i + HALF] : v[i];
-        v[i] = keep + __shfl_xor(send, DIST);
-      }
-      if (bit) base += HALF;
-      reduce_scatter<HALF, DIST / 2, DMIN>(v, lane, base);
-    } else {
-      v[0] += __shfl_xor(v[0], DIST);
-      reduce_scatter<1, DIST / 2, DMIN>(v, lane, base);
-    }
-  }
-}
-
-__host__ __device__ constexpr int ilog2c(int x) { return x <= 1 ? 0 : 1 + ilog2c(x / 2); }
-
 __device__ __forceinline__ void store_y(const KArgs& a, int b, int row, float v) {
   if (a.y_f16) ((f16*)a.y)[(int64_t)b * a.ldy + row] = (f16)v;
   else ((float*)a.y)[(int64_t)b * a.ldy + row] = v;
@@ -182,105 +161,313 @@ __device__ __forceinline__ void store_y(const KArgs& a, int b, int row, float v)
 
 // ------------------------------------------------------------------------------------------
 // Vector-ALU kernel: batch M (1, 2, 4 or 8), RPL rows of a record per lane.
+//
+// Persistent waves walk a balanced list of work items. An item is one tile (16 rows) and a
+// segment of `cps` consecutive chunks of its vector positions; a chunk is 64/H positions, one
+// per lane group. The next record's loads are issued before the current record is computed.
+// An item's partial sums go straight to y when the tile has a single segment; otherwise they
+// are written to tagged workspace slots, and the wave that ran the tile's first segment adds
+// the segments in a fixed order once its own items are done, so results do not depend on
+// scheduling and no wave ever waits while it still owes partial sums to others.
 // ------------------------------------------------------------------------------------------
-template <int KIND, int D, int M, int RPL>
-__global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
-  extern __shared__ __align__(16) unsigned char lds[];
-  constexpr int H = 16 / RPL;                                          // lanes per record
-  constexpr int ADW = (KIND == SPH_KIND_CB13) ? RPL / 4 : RPL / 2;     // A dwords per lane
-  constexpr int BDW = (KIND == SPH_KIND_NIB16Q8) ? RPL / 4 : (KIND == SPH_KIND_CB13) ? RPL / 2 : 1;
+template <int KIND, int D>
+struct Tables {
+  static constexpr uint32_t bytes = (KIND == SPH_KIND_CB13) ? ((16u << D) + 128u) : (256u << D);
+};
+
+template <int KIND, int M, int RPL>
+struct Rec {
+  static constexpr int ADW = (KIND == SPH_KIND_CB13) ? RPL / 4 : RPL / 2;
+  static constexpr int BDW = (KIND == SPH_KIND_NIB16Q8) ? RPL / 4 : (KIND == SPH_KIND_CB13) ? RPL / 2 : 1;
+  uint32_t ra[ADW];
+  uint32_t rb[BDW];
+  uint32_t pw;        // one group-parameter word of the chunk, staged through LDS at compute time
+  uint4 xv[M];
+  bool ok;            // vector position inside the row; else x is taken as 0
+};
+
+// Loads of one step. Branch-free so that the compiler can count outstanding loads across the
+// software pipeline: positions past the end of the row read a valid record and contribute
+// through x = 0. The chunk's group parameters (VPC/16 groups x 16 rows = VPC words, contiguous)
+// are spread one word per lane.
+template <int KIND, int M, int RPL>
+__device__ __forceinline__ void load_rec(Rec<KIND, M, RPL>& R, const KArgs& a, int t, int c, int h, int vloc,
+                                         int lane) {
+  constexpr int H = 16 / RPL, VPC = 64 / H;
   constexpr int ADW_REC = (KIND == SPH_KIND_CB13) ? 4 : 8;
   constexpr int BDW_REC = (KIND == SPH_KIND_W2) ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
-  constexpr int NVAL = M * RPL;
+  constexpr int ADW = Rec<KIND, M, RPL>::ADW, BDW = Rec<KIND, M, RPL>::BDW;
+  const int v0 = c * VPC + vloc;
+  const bool ok = v0 < a.nv;
+  const int v = ok ? v0 : a.nv - 1;
+  const int64_t rec = (int64_t)t * a.nv + v;
+  load_dw<ADW>(R.ra, a.A + rec * ADW_REC + h * ADW);
+  if constexpr (KIND == SPH_KIND_W2) R.rb[0] = a.B[rec];
+  else if constexpr (KIND != SPH_KIND_NIB16) load_dw<BDW>(R.rb, a.B + rec * BDW_REC + h * BDW);
+  // parameter word `lane` of the chunk: group c*VPC/16 + lane/16, row lane%16 (clamped to the row)
+  const int pg = min(c * (VPC / 16) + (lane & (VPC - 1)) / 16, a.ng - 1);
+  R.pw = a.P[((int64_t)t * a.ng + pg) * 16 + (lane & 15)];
+#pragma unroll
+  for (int b = 0; b < M; ++b) {
+    const int bb = (M == 1 || b < a.m) ? b : 0;
+    R.xv[b] = *(const uint4*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v);
+  }
+  R.ok = ok;
+}
 
+// Rows of the record in batches of RB: all table lookups of a batch are issued before any
+// of its arithmetic, so one LDS round trip serves RB rows.
+template <int KIND, int D, int M, int RPL>
+__device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL>& R, float (&acc)[M][RPL],
+                                            const unsigned char* lds, uint32_t mask_off, uint32_t* pstage,
+                                            int lane, int h, int vloc, int m) {
+  constexpr int RB = RPL < 4 ? RPL : 4;
+  // group parameters: stage the chunk's words in this wave's LDS slot, read back this lane's rows
+  pstage[lane] = R.pw;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  uint32_t pp[RPL];
+  const uint32_t* src = pstage + (vloc >> 4) * 16 + h * RPL;
+#pragma unroll
+  for (int i = 0; i < RPL; i += 4) {
+    const uint4 u = *(const uint4*)(src + i);
+    pp[i] = u.x; pp[i + 1] = u.y; pp[i + 2] = u.z; pp[i + 3] = u.w;
+  }
+  uint4 xv[M];
+#pragma unroll
+  for (int b = 0; b < M; ++b) {
+    const bool use = R.ok && (M == 1 || b < m);
+    xv[b] = use ? R.xv[b] : make_uint4(0, 0, 0, 0);
+  }
+  uint32_t qodd = 0;
+  if constexpr (KIND == SPH_KIND_W2) qodd = R.rb[0] >> (4 * (h * RPL / 2));
+#pragma unroll
+  for (int r0 = 0; r0 < RPL; r0 += RB) {
+    uint4 tt[RB];
+    float qf[RB];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int r = r0 + i;
+      uint32_t q;
+      if constexpr (KIND == SPH_KIND_CB13) {
+        uint32_t s, z;
+        decode_cb13(R.ra[r / 4], r % 4, R.rb[r / 2], r & 1, s, z, q);
+        tt[i] = signed_dir_cb13(lds, mask_off, s, z);
+      } else {
+        uint32_t lo, hi, qx = 0;
+        if constexpr (KIND == SPH_KIND_W2) qx = (qodd >> (4 * (r / 2))) & 15u;
+        if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (R.rb[r / 4] >> (8 * (r % 4))) & 0xFFu;
+        decode_nib<KIND, D>(R.ra[r / 2], r & 1, qx, lo, hi, q);
+        tt[i] = signed_dir_nib<KIND, D>(lds, lo, hi);
+      }
+      qf[i] = (float)q;
+    }
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      const int r = r0 + i;
+      const float rh = fmaf(qf[i], f16hi(pp[r]), f16lo(pp[r]));
+#pragma unroll
+      for (int b = 0; b < M; ++b) acc[b][r] = fmaf(rh, dot8(tt[i], xv[b]), acc[b][r]);
+    }
+  }
+}
+
+// Exchange-and-add across lanes l and l^DIST: lanes with bit DIST clear end with
+// lo_keep[l] + lo_keep[l^DIST], the others with hi_keep[l] + hi_keep[l^DIST]. (The gfx950
+// permlane-swap builtins would do this in one instruction, but this compiler version folds the
+// sum of their two results into twice one of them, so they are not used.)
+template <int DIST>
+__device__ __forceinline__ float xchg_add(float lo_keep, float hi_keep, int lane) {
+  const bool bit = (lane & DIST) != 0;
+  const float send = bit ? lo_keep : hi_keep;
+  const float keep = bit ? hi_keep : lo_keep;
+  return keep + __shfl_xor(send, DIST);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_add(float v) {
+  return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum an item's accumulators over the lanes sharing h: a scatter over lane bits 5 and 4 with
+// lane exchanges, then all-reductions inside 16-lane rows with DPP rotations. Afterwards every
+// lane holds NVAL/4 totals, value i being flattened index i + (NVAL/2)*bit5 + (NVAL/4)*bit4.
+template <int NVAL, int H>
+__device__ __forceinline__ void wave_reduce(float (&v)[NVAL], int lane) {
+  constexpr int N2 = NVAL / 2, N4 = NVAL / 4;
+#pragma unroll
+  for (int i = 0; i < N2; ++i) v[i] = xchg_add<32>(v[i], v[i + N2], lane);
+#pragma unroll
+  for (int i = 0; i < N4; ++i) v[i] = xchg_add<16>(v[i], v[i + N4], lane);
+#pragma unroll
+  for (int i = 0; i < N4; ++i) {
+    float x = dpp_add<0x128>(v[i]);                      // row_ror:8
+    x = dpp_add<0x124>(x);                                // row_ror:4
+    if constexpr (H <= 2) x = dpp_add<0x122>(x);          // row_ror:2
+    if constexpr (H <= 1) x = dpp_add<0x121>(x);          // row_ror:1
+    v[i] = x;
+  }
+}
+
+// Split-K slots: one 64-bit word per (tile, segment, batch row, tile row) holding the fp32
+// partial sum in the low half and a valid flag in the high half, written and read with
+// device-coherent (agent-scope) atomics so that a single load sees value and flag together.
+__device__ __forceinline__ void slot_store(uint64_t* p, float v) {
+  __hip_atomic_store(p, (uint64_t)__builtin_bit_cast(uint32_t, v) | (1ull << 32), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Emit a finished item: straight to y when its tile has a single segment, else as partial sums
+// in the tile's slots (the tile's reducer adds them at the end of its own work).
+template <int M, int RPL>
+__device__ __forceinline__ void emit_item(const KArgs& a, float (&acc)[M][RPL], int t, int s, int lane, int h) {
+  constexpr int H = 16 / RPL;
+  constexpr int NVAL = M * RPL, N4 = NVAL / 4;
+  float vals[NVAL];
+#pragma unroll
+  for (int b = 0; b < M; ++b)
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) {
+      vals[b * RPL + r] = acc[b][r];
+      acc[b][r] = 0.0f;
+    }
+  wave_reduce<NVAL, H>(vals, lane);
+  const int base = ((lane >> 5) & 1) * (NVAL / 2) + ((lane >> 4) & 1) * N4;
+  if ((lane & 15) >= H) return;              // one writer lane per h in each 16-lane row
+  if (a.S == 1) {
+#pragma unroll
+    for (int i = 0; i < N4; ++i) {
+      const int f = base + i, b = f / RPL, row = h * RPL + f % RPL;
+      const int grow = t * 16 + row;
+      if (b < a.m && grow < a.n) store_y(a, b, grow, vals[i]);
+    }
+  } else {
+    uint64_t* slot = a.ws_slot + ((int64_t)t * a.S + s) * (M * 16);
+#pragma unroll
+    for (int i = 0; i < N4; ++i) {
+      const int f = base + i, b = f / RPL, row = h * RPL + f % RPL;
+      slot_store(slot + b * 16 + row, vals[i]);
+    }
+  }
+}
+
+// Reducer of tile t: wait for every segment's slot to be valid (the segments are written by
+// waves that never wait before finishing their own items), add the segments in order, clear the
+// slots for the next call, write y. The wait is bounded by a deadline on the constant 100 MHz
+// real-time counter (about 50 ms, thousands of times a whole launch); a wait that runs out (not
+// expected) writes NaN rather than hanging.
+template <int M>
+__device__ __forceinline__ void reduce_tile(const KArgs& a, int t, int lane) {
+  uint64_t* slots = a.ws_slot + (int64_t)t * a.S * (M * 16);
+  const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + 5000000ull;
+  for (int j = lane; j < M * 16; j += 64) {
+    float sum = 0.0f;
+    bool ok = true;
+    for (int sg = 0; sg < a.S; ++sg) {
+      uint64_t* p = slots + sg * (M * 16) + j;
+      uint64_t w = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      while ((w >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline) {
+        __builtin_amdgcn_s_sleep(2);
+        w = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      ok = ok && (w >> 32) != 0;
+      sum += __builtin_bit_cast(float, (uint32_t)w);
+      __hip_atomic_store(p, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const int b = j / 16, grow = t * 16 + (j % 16);
+    if (b < a.m && grow < a.n) store_y(a, b, grow, ok ? sum : __builtin_nanf(""));
+  }
+}
+
+// A wave's position in its sequence of (item, chunk) steps; wave-uniform.
+struct Pos {
+  int item, t, s, c, cend;
+  bool live;
+};
+
+__device__ __forceinline__ Pos first_pos(const KArgs& a, int item) {
+  Pos p;
+  item = __builtin_amdgcn_readfirstlane(item);
+  p.item = item;
+  p.live = item < a.items;
+  p.t = item / a.S;
+  p.s = item % a.S;
+  p.c = p.s * a.cps;
+  p.cend = min(a.nc, p.c + a.cps);
+  return p;
+}
+
+__device__ __forceinline__ Pos next_pos(const KArgs& a, const Pos& p) {
+  if (p.c + 1 < p.cend) {
+    Pos q = p;
+    q.c = p.c + 1;
+    return q;
+  }
+  return first_pos(a, p.item + a.gw);
+}
+
+// Persistent waves walk balanced items (a tile and a run of chunks) in steps of one record.
+// Two record buffers in ping-pong: the loads of step i+1 are in flight while step i is computed,
+// and no register copy ever waits on loads still in flight; the step after the last one
+// re-reads a valid record so that the loads stay unconditional. Emitting an item never waits
+// on memory, so the pipeline runs through item boundaries; split tiles are reduced at the end.
+template <int KIND, int D, int M, int RPL>
+__global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
+  __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes];
+  __shared__ __align__(16) uint32_t pstage_all[16 * 64];
+  __shared__ int red_list[16 * 32];
+  constexpr int H = 16 / RPL;
+  stage_tables<KIND>(lds, a);
   const uint32_t mask_off = a.t_bytes;
-  const uint32_t red_off = stage_tables<KIND>(lds, a);
-  float* red = (float*)(lds + red_off);
   __syncthreads();
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, W = a.wpt;
+  const int lane = threadIdx.x & 63;
+  // wave-uniform by construction; readfirstlane keeps the schedule in SGPRs. Items are striped
+  // over workgroups first so that every CU gets a share.
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  Pos p0 = first_pos(a, wave * (int)gridDim.x + blockIdx.x);
+  if (!p0.live) return;                        // no barrier follows
+  uint32_t* pstage = pstage_all + wave * 64;
+  int* reds = red_list + wave * 32;
+  int nred = 0;
   const int h = lane % H, vloc = lane / H;
-  const int vstep = (64 / H) * W;
 
-  for (int t = blockIdx.x; t < a.nt; t += gridDim.x) {
-    float acc[M][RPL];
+  float acc[M][RPL];
 #pragma unroll
-    for (int b = 0; b < M; ++b)
+  for (int b = 0; b < M; ++b)
 #pragma unroll
-      for (int r = 0; r < RPL; ++r) acc[b][r] = 0.0f;
+    for (int r = 0; r < RPL; ++r) acc[b][r] = 0.0f;
 
-    for (int v = wave * (64 / H) + vloc; v < a.nv; v += vstep) {
-      const int64_t rec = (int64_t)t * a.nv + v;
-      uint32_t ra[ADW], rb[BDW];
-      load_dw<ADW>(ra, a.A + rec * ADW_REC + h * ADW);
-      if constexpr (KIND == SPH_KIND_W2) rb[0] = a.B[rec];
-      else if constexpr (KIND != SPH_KIND_NIB16) load_dw<BDW>(rb, a.B + rec * BDW_REC + h * BDW);
-      uint32_t pp[RPL];
-      load_dw<RPL>(pp, a.P + ((int64_t)t * a.ng + (v >> 4)) * 16 + h * RPL);
-      uint4 xv[M];
-#pragma unroll
-      for (int b = 0; b < M; ++b) {
-        if (M == 1 || b < a.m) xv[b] = *(const uint4*)(a.x + (int64_t)b * a.ldx + 8 * (int64_t)v);
-        else xv[b] = make_uint4(0, 0, 0, 0);
-      }
-      uint32_t qodd = 0;
-      if constexpr (KIND == SPH_KIND_W2) qodd = rb[0] >> (4 * (h * RPL / 2));
-#pragma unroll
-      for (int r = 0; r < RPL; ++r) {
-        uint4 tt;
-        uint32_t q;
-        if constexpr (KIND == SPH_KIND_CB13) {
-          uint32_t s, z;
-          decode_cb13(ra[r / 4], r % 4, rb[r / 2], r & 1, s, z, q);
-          tt = signed_dir_cb13(lds, mask_off, s, z);
-        } else {
-          uint32_t lo, hi, qx = 0;
-          if constexpr (KIND == SPH_KIND_W2) qx = (qodd >> (4 * (r / 2))) & 15u;
-          if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (rb[r / 4] >> (8 * (r % 4))) & 0xFFu;
-          decode_nib<KIND, D>(ra[r / 2], r & 1, qx, lo, hi, q);
-          tt = signed_dir_nib<KIND, D>(lds, lo, hi);
-        }
-        const float rh = fmaf((float)q, f16hi(pp[r]), f16lo(pp[r]));
-#pragma unroll
-        for (int b = 0; b < M; ++b) acc[b][r] = fmaf(rh, dot8(tt, xv[b]), acc[b][r]);
+  Rec<KIND, M, RPL> r0, r1;
+  load_rec<KIND, M, RPL>(r0, a, p0.t, p0.c, h, vloc, lane);
+  while (true) {
+    const Pos p1 = next_pos(a, p0);
+    load_rec<KIND, M, RPL>(r1, a, p1.live ? p1.t : p0.t, p1.live ? p1.c : p0.c, h, vloc, lane);
+    compute_rec<KIND, D, M, RPL>(r0, acc, lds, mask_off, pstage, lane, h, vloc, a.m);
+    if (p0.c + 1 >= p0.cend) {
+      emit_item<M, RPL>(a, acc, p0.t, p0.s, lane, h);
+      if (a.S > 1 && p0.s == 0) {
+        if (lane == 0) reds[nred] = p0.t;
+        ++nred;
       }
     }
-
-    // Wave reduction over the lanes that share h, then across waves in LDS (fixed order).
-    float vals[NVAL];
-#pragma unroll
-    for (int b = 0; b < M; ++b)
-#pragma unroll
-      for (int r = 0; r < RPL; ++r) vals[b * RPL + r] = acc[b][r];
-    int base = 0;
-    reduce_scatter<NVAL, 32, H>(vals, lane, base);
-    constexpr int STEPS = ilog2c(64 / H), LV = ilog2c(NVAL);
-    constexpr int LEFT = (LV < STEPS) ? (NVAL >> LV) : (NVAL >> STEPS);
-    bool writer = true;
-    if constexpr (LV < STEPS) {
-      // bits of the all-reduced distances (32 >> LV down to H) must be zero
-      constexpr int hi_dist = 32 >> LV;
-      constexpr int mask = (2 * hi_dist - 1) & ~(H - 1);
-      writer = (lane & mask) == 0;
-    }
-    if (writer) {
-#pragma unroll
-      for (int i = 0; i < LEFT; ++i) {
-        const int f = base + i;
-        const int b = f / RPL, r = f % RPL;
-        red[(wave * M + b) * 16 + h * RPL + r] = vals[i];
+    if (!p1.live) break;
+    const Pos p2 = next_pos(a, p1);
+    load_rec<KIND, M, RPL>(r0, a, p2.live ? p2.t : p1.t, p2.live ? p2.c : p1.c, h, vloc, lane);
+    compute_rec<KIND, D, M, RPL>(r1, acc, lds, mask_off, pstage, lane, h, vloc, a.m);
+    if (p1.c + 1 >= p1.cend) {
+      emit_item<M, RPL>(a, acc, p1.t, p1.s, lane, h);
+      if (a.S > 1 && p1.s == 0) {
+        if (lane == 0) reds[nred] = p1.t;
+        ++nred;
       }
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < M * 16; i += blockDim.x) {
-      const int b = i / 16, row = i % 16;
-      float s = 0.0f;
-      for (int w = 0; w < W; ++w) s += red[(w * M + b) * 16 + row];
-      const int grow = t * 16 + row;
-      if (b < a.m && grow < a.n) store_y(a, b, grow, s);
-    }
-    __syncthreads();
+    if (!p2.live) break;
+    p0 = p2;
   }
+  // The reducer role comes last, after this wave has produced all of its own partial sums.
+  for (int i = 0; i < nred; ++i) reduce_tile<M>(a, __builtin_amdgcn_readfirstlane(reds[i]), lane);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -316,7 +503,8 @@ __device__ __forceinline__ uint32_t scale_pack(uint32_t t, float rh) {
 
 template <int KIND, int D, int NB>
 __global__ void __launch_bounds__(1024) k_gemm_mfma(KArgs a) {
-  extern __shared__ __align__(16) unsigned char lds[];
+  constexpr int WMAX = (KIND == SPH_KIND_CB13) ? 8 : 16;
+  __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes + WMAX * NB * 1024];
   const uint32_t mask_off = a.t_bytes;
   const uint32_t red_off = stage_tables<KIND>(lds, a);
   float* red = (float*)(lds + red_off);
@@ -408,9 +596,11 @@ namespace {
 
 struct Launch {
   const void* fn;
-  int wpt;
+  int block;          // threads per workgroup
   int grid;
-  uint32_t lds;
+  int wpt;            // matrix-core kernel: waves per tile
+  int nc, cps, S, items;
+  size_t ws_bytes;    // workspace the launch needs
 };
 
 KArgs make_args(const sph_weights* w) {
@@ -471,54 +661,80 @@ const void* unpack_fn(int D, int V) {
   return nullptr;
 }
 
-int g_num_cus = 0;
+std::atomic<int> g_num_cus{0};
 
 int num_cus() {
-  if (g_num_cus == 0) {
+  int c = g_num_cus.load();
+  if (c == 0) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
-      g_num_cus = cus;
+      c = cus;
     else
-      g_num_cus = 256;
+      c = 256;
+    g_num_cus.store(c);
   }
-  return g_num_cus;
+  return c;
 }
 
-uint32_t lds_tables(const sph_weights* w) {
-  const int kind = sph_kind_of(w->fmt.dir_bits, w->fmt.radius_bits);
-  uint32_t b = (uint32_t)sph_table_bytes(kind, w->fmt.dir_bits);
-  if (kind == SPH_KIND_CB13) b += 128;
-  return (b + 15u) & ~15u;
-}
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
-// Waves per tile: enough vector positions per lane to amortise the reduction, at most 16.
+// Work plan. Vector-ALU path: persistent waves filling every CU to the occupancy the kernel
+// allows.
+// The chunks-per-item count minimises the rounds of items times their length plus a fixed
+// cost per item for its reduction.
 Launch plan(const sph_weights* w, int m) {
   Launch L{};
   const int64_t nv = w->k / 8, nt = (w->n + 15) / 16;
-  const bool mfma = m > 8;
   const int kind = sph_kind_of(w->fmt.dir_bits, w->fmt.radius_bits);
-  int wpt;
-  if (!mfma) {
+  const int cus = num_cus();
+  if (m <= 8) {
     const int M = m <= 1 ? 1 : m <= 2 ? 2 : m <= 4 ? 4 : 8;
     const int H = M <= 2 ? 1 : M == 4 ? 2 : 4;
-    const int64_t per_wave = (64 / H) * 4;      // ~4 records per lane
-    wpt = (int)((nv + per_wave - 1) / per_wave);
-    wpt = wpt < 1 ? 1 : wpt > 16 ? 16 : wpt;
+    const int vpc = 64 / H;
+    const int wpb = 16;                         // one 16-wave workgroup per CU
+    const int grid = cus;
+    const int64_t gw = (int64_t)grid * wpb;
+    const int64_t nc = (nv + vpc - 1) / vpc;
+    // Cost of a plan: rounds of items times (record batches per item + a fixed cost per batch
+    // and per item). Split plans (S > 1) pay an extra reduction at the end of the waves' work.
+    int64_t best_cps = 1;
+    double best = 1e300;
+    for (int64_t cps = 1; cps <= nc; ++cps) {
+      const int64_t S = (nc + cps - 1) / cps;
+      const int64_t items = nt * S;
+      const int64_t rounds = (items + gw - 1) / gw;
+      if (S > 1 && rounds > 32) continue;       // reducer list bound per wave
+      // steps of the busiest wave, plus a small cost per item (its reduction) and one for the
+      // split reduction at the end of the waves' work
+      const double cost = (double)rounds * ((double)cps + 0.5) + (S > 1 ? 2.0 : 0.0);
+      if (cost < best - 1e-9) {
+        best = cost;
+        best_cps = cps;
+      }
+    }
     L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, false, M);
-    L.lds = lds_tables(w) + (uint32_t)(wpt * M * 16 * 4);
+    L.block = 64 * wpb;
+    L.nc = (int)nc;
+    L.cps = (int)best_cps;
+    L.S = (int)((nc + best_cps - 1) / best_cps);
+    L.items = (int)(nt * L.S);
+    const int64_t need = (L.items + wpb - 1) / wpb;
+    L.grid = (int)(need < grid ? need : grid);
+    L.ws_bytes = L.S > 1 ? (size_t)nt * L.S * M * 16 * 8 : 0;
   } else {
     const int NB = m <= 16 ? 1 : 2;
     const int64_t per_wave = 4 * 8;             // 8 MFMA steps per wave
-    wpt = (int)((nv + per_wave - 1) / per_wave);
+    int wpt = (int)((nv + per_wave - 1) / per_wave);
     const int wmax = (kind == SPH_KIND_CB13) ? 8 : 16;
     wpt = wpt < 1 ? 1 : wpt > wmax ? wmax : wpt;
     L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, true, NB);
-    L.lds = lds_tables(w) + (uint32_t)(wpt * NB * 64 * 4 * 4);
+    L.wpt = wpt;
+    L.block = 64 * wpt;
+    const int64_t cap = (int64_t)cus * 4;
+    L.grid = (int)(nt < cap ? nt : cap);
+    L.ws_bytes = 0;
   }
-  L.wpt = wpt;
-  const int64_t cap = (int64_t)num_cus() * 4;
-  L.grid = (int)(nt < cap ? nt : cap);
   return L;
 }
 
@@ -532,25 +748,10 @@ bool valid_desc(const sph_weights* w) {
   return true;
 }
 
-std::mutex g_attr_mu;
-std::vector<const void*> g_attr_set;
-
-// Kernels whose LDS exceeds the default 64 KiB get the gfx950 maximum, once per function.
-bool allow_big_lds(const void* fn) {
-  std::lock_guard<std::mutex> lk(g_attr_mu);
-  for (const void* f : g_attr_set)
-    if (f == fn) return true;
-  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess) return false;
-  g_attr_set.push_back(fn);
-  return true;
-}
-
 sph_status launch(const Launch& L, const KArgs& a, hipStream_t s) {
-  if (L.lds > 160 * 1024) return SPH_ERR_HIP;
-  if (L.lds > 64 * 1024 && !allow_big_lds(L.fn)) return SPH_ERR_HIP;
   KArgs args = a;
   void* kargs[] = {&args};
-  if (hipLaunchKernel(L.fn, dim3(L.grid), dim3(64 * L.wpt), kargs, L.lds, s) != hipSuccess) return SPH_ERR_HIP;
+  if (hipLaunchKernel(L.fn, dim3(L.grid), dim3(L.block), kargs, 0, s) != hipSuccess) return SPH_ERR_HIP;
   if (hipGetLastError() != hipSuccess) return SPH_ERR_HIP;
   return SPH_OK;
 }
@@ -623,14 +824,12 @@ sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes) {
   if (!w || !bytes) return SPH_ERR_NULL;
   if (!valid_desc(w)) return SPH_ERR_BAD_DESCRIPTOR;
   if (m < 1 || m > 32) return SPH_ERR_SHAPE;
-  *bytes = 0;
+  *bytes = plan(w, (int)m).ws_bytes;
   return SPH_OK;
 }
 
 sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y,
                           int64_t ldy, sph_dtype y_dtype, void* d_ws, size_t ws_bytes, void* stream) {
-  (void)d_ws;
-  (void)ws_bytes;
   if (!w || !d_x || !d_y) return SPH_ERR_NULL;
   if (!valid_desc(w)) return SPH_ERR_BAD_DESCRIPTOR;
   if (m < 1 || m > 32) return SPH_ERR_SHAPE;
@@ -639,7 +838,19 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
   if ((uintptr_t)d_x % 16 != 0 || (uintptr_t)d_y % 4 != 0) return SPH_ERR_SHAPE;
   const Launch L = plan(w, (int)m);
   if (!L.fn) return SPH_ERR_UNSUPPORTED_FORMAT;
+  if (L.ws_bytes > 0) {
+    if (!d_ws) return SPH_ERR_NULL;
+    if (ws_bytes < L.ws_bytes) return SPH_ERR_BUFFER_TOO_SMALL;
+    if ((uintptr_t)d_ws % 256 != 0) return SPH_ERR_SHAPE;
+  }
   KArgs a = make_args(w);
+  a.nc = L.nc;
+  a.wpb = L.block / 64;
+  a.gw = L.grid * (L.block / 64);
+  a.cps = L.cps;
+  a.S = L.S;
+  a.items = L.items;
+  if (L.ws_bytes > 0) a.ws_slot = (uint64_t*)d_ws;
   a.x = (const uint16_t*)d_x;
   a.ldx = ldx;
   a.y = d_y;

@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from dataclasses import dataclass
+from dataclasses import dataclass, field
 
 import numpy as np
 
@@ -127,6 +127,7 @@ class SphWeights:
     k: int
     dir_bits: int
     radius_bits: int
+    workspaces: dict = field(default_factory=dict)
 
     @property
     def nbytes(self) -> int:
@@ -168,11 +169,16 @@ def workspace_bytes(w: SphWeights, m: int) -> int:
 
 
 def _workspace(w: SphWeights, m: int, device):
+    """Zero-filled workspace for (w, m), allocated once and kept with the weights (the library
+    leaves it zero-filled after every call)."""
     import torch
     nb = workspace_bytes(w, m)
     if nb == 0:
         return None, 0
-    ws = torch.zeros(nb, dtype=torch.uint8, device=device)
+    ws = w.workspaces.get(m)
+    if ws is None or ws.numel() < nb:
+        ws = torch.zeros(nb, dtype=torch.uint8, device=device)
+        w.workspaces[m] = ws
     return ws, nb
 
 

@@ -13,7 +13,8 @@
  * registers, no dequantised weights ever written to memory).
  *
  * Conventions shared by every entry point:
- *  - W is n x k (n = d_out rows, k = d_in columns). k must be a multiple of 128 and n >= 1.
+ *  - W is n x k (n = d_out rows, k = d_in columns). k must be a multiple of 128 with
+ *    128 <= k <= 2^20, 1 <= n <= 2^24, and ceil(n/16) * k/8 < 2^31.
  *  - Logical codes are row-major: signs/dir/q are [n][k/8], group params are [n][k/128].
  *    Sign bit j of a vector belongs to element 8v+j (least significant bit first); a set bit
  *    means the element is negative.

@@ -41,10 +41,14 @@ struct KArgs {
   int y_f16;
   int n, nt, nv, ng, m;
   int wpt;            // waves per tile (matrix-core kernel)
-  // vector-ALU work plan: items = nt * S, each `cps` chunks of one tile
-  int nc, cps, S, items;
-  int wpb, gw;        // waves per workgroup, waves in the grid
-  uint64_t* ws_slot;  // [nt][S][M][16] tagged partial sums (S > 1), flags zero between calls
+  // vector-ALU work plan: ts = nt * nc steps in tile-major order, cut into gwa contiguous and
+  // balanced wave ranges
+  int nc;             // steps (chunks of vector positions) per tile
+  int gwa;            // waves with work
+  int wpb;            // waves per workgroup
+  int pmax;           // slot parts per tile
+  int ts;
+  uint64_t* ws_slot;  // [nt][pmax][M][16] tagged partial sums of split tiles, zero between calls
 };
 
 // ------------------------------------------------------------------------------------------
@@ -84,17 +88,18 @@ __device__ __forceinline__ void decode_cb13(uint32_t sdw, int sbyte, uint32_t zd
 // The signed direction s (.) c_z of one vector as 4 half2 words, looked up in LDS.
 template <int KIND, int D>
 __device__ __forceinline__ uint4 signed_dir_nib(const unsigned char* lds, uint32_t lo, uint32_t hi) {
-  constexpr uint32_t THI = (16u << D) * 8u;
-  const uint2 a = *(const uint2*)(lds + lo * 8u);
-  const uint2 b = *(const uint2*)(lds + THI + hi * 8u);
+  constexpr uint32_t THI = 16u << D;          // entries of T_lo
+  const uint2 a = ((const uint2*)lds)[lo];
+  const uint2 b = ((const uint2*)lds)[THI + hi];
   return make_uint4(a.x, a.y, b.x, b.y);
 }
 
 __device__ __forceinline__ uint4 signed_dir_cb13(const unsigned char* lds, uint32_t mask_off, uint32_t s,
                                                  uint32_t z) {
-  const uint4 c = *(const uint4*)(lds + z * 16u);
-  const uint2 ml = *(const uint2*)(lds + mask_off + (s & 15u) * 8u);
-  const uint2 mh = *(const uint2*)(lds + mask_off + (s >> 4) * 8u);
+  const uint4 c = ((const uint4*)lds)[z];
+  const uint2* mask = (const uint2*)(lds + mask_off);
+  const uint2 ml = mask[s & 15u];
+  const uint2 mh = mask[s >> 4];
   return make_uint4(c.x ^ ml.x, c.y ^ ml.y, c.z ^ mh.x, c.w ^ mh.y);
 }
 
@@ -102,11 +107,11 @@ __device__ __forceinline__ float f16lo(uint32_t u) { return (float)__builtin_bit
 __device__ __forceinline__ float f16hi(uint32_t u) { return (float)__builtin_bit_cast(f16, (uint16_t)(u >> 16)); }
 __device__ __forceinline__ f16x2 as_h2(uint32_t u) { return __builtin_bit_cast(f16x2, u); }
 
-__device__ __forceinline__ float dot8(uint4 t, uint4 x) {
-  float p = __builtin_amdgcn_fdot2(as_h2(t.x), as_h2(x.x), 0.0f, false);
-  p = __builtin_amdgcn_fdot2(as_h2(t.y), as_h2(x.y), p, false);
-  p = __builtin_amdgcn_fdot2(as_h2(t.z), as_h2(x.z), p, false);
-  return __builtin_amdgcn_fdot2(as_h2(t.w), as_h2(x.w), p, false);
+__device__ __forceinline__ float dot8(uint4 t, const uint32_t (&x)[4]) {
+  float p = __builtin_amdgcn_fdot2(as_h2(t.x), as_h2(x[0]), 0.0f, false);
+  p = __builtin_amdgcn_fdot2(as_h2(t.y), as_h2(x[1]), p, false);
+  p = __builtin_amdgcn_fdot2(as_h2(t.z), as_h2(x[2]), p, false);
+  return __builtin_amdgcn_fdot2(as_h2(t.w), as_h2(x[3]), p, false);
 }
 
 // Stage the lookup tables (and for the codebook kind the 16-entry sign-mask table, placed right
@@ -162,13 +167,15 @@ __device__ __forceinline__ void store_y(const KArgs& a, int b, int row, float v)
 // ------------------------------------------------------------------------------------------
 // Vector-ALU kernel: batch M (1, 2, 4 or 8), RPL rows of a record per lane.
 //
-// Persistent waves walk a balanced list of work items. An item is one tile (16 rows) and a
-// segment of `cps` consecutive chunks of its vector positions; a chunk is 64/H positions, one
-// per lane group. The next record's loads are issued before the current record is computed.
-// An item's partial sums go straight to y when the tile has a single segment; otherwise they
-// are written to tagged workspace slots, and the wave that ran the tile's first segment adds
-// the segments in a fixed order once its own items are done, so results do not depend on
-// scheduling and no wave ever waits while it still owes partial sums to others.
+// The work is ts = nt * nc steps: step (t, c) is chunk c (64/H consecutive vector positions, one
+// per lane group) of tile t (16 rows). The steps, in tile-major order, are cut into contiguous
+// ranges of equal length (to one step), one per wave, in the manner of stream-K. A tile that
+// lies wholly inside a range is stored straight to y. A tile cut by range boundaries has parts
+// in consecutive waves: each later part is handed over through tagged workspace slots, and the
+// wave holding chunk 0 (whose range ends inside the tile) adds the parts in chunk order and
+// stores y. Later parts sit at the start of their waves' ranges, so they are normally written
+// long before that wave reaches its end; the order of the sum is fixed, so results do not depend
+// on scheduling.
 // ------------------------------------------------------------------------------------------
 template <int KIND, int D>
 struct Tables {
@@ -182,14 +189,15 @@ struct Rec {
   uint32_t ra[ADW];
   uint32_t rb[BDW];
   uint32_t pw;        // one group-parameter word of the chunk, staged through LDS at compute time
-  uint4 xv[M];
-  bool ok;            // vector position inside the row; else x is taken as 0
+  uint32_t xv[M][4];  // the activation vector(s) of this lane's position
+  bool pok;           // pw belongs to a group inside the row; else the group's radii are taken as 0
 };
 
-// Loads of one step. Branch-free so that the compiler can count outstanding loads across the
-// software pipeline: positions past the end of the row read a valid record and contribute
-// through x = 0. The chunk's group parameters (VPC/16 groups x 16 rows = VPC words, contiguous)
-// are spread one word per lane.
+// Loads of one step. Branch-free, and no loaded value is ever selected or copied before use, so
+// that the compiler can count outstanding loads across the software pipeline. Vector positions
+// past the end of the row (whole groups, since k is a multiple of 128) read a valid record and
+// contribute nothing because their group parameters are taken as zero. The chunk's group
+// parameters (VPC/16 groups x 16 rows = VPC words, contiguous) are spread one word per lane.
 template <int KIND, int M, int RPL>
 __device__ __forceinline__ void load_rec(Rec<KIND, M, RPL>& R, const KArgs& a, int t, int c, int h, int vloc,
                                          int lane) {
@@ -197,22 +205,21 @@ __device__ __forceinline__ void load_rec(Rec<KIND, M, RPL>& R, const KArgs& a, i
   constexpr int ADW_REC = (KIND == SPH_KIND_CB13) ? 4 : 8;
   constexpr int BDW_REC = (KIND == SPH_KIND_W2) ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
   constexpr int ADW = Rec<KIND, M, RPL>::ADW, BDW = Rec<KIND, M, RPL>::BDW;
-  const int v0 = c * VPC + vloc;
-  const bool ok = v0 < a.nv;
-  const int v = ok ? v0 : a.nv - 1;
+  const int v = min(c * VPC + vloc, a.nv - 1);
   const int64_t rec = (int64_t)t * a.nv + v;
   load_dw<ADW>(R.ra, a.A + rec * ADW_REC + h * ADW);
   if constexpr (KIND == SPH_KIND_W2) R.rb[0] = a.B[rec];
   else if constexpr (KIND != SPH_KIND_NIB16) load_dw<BDW>(R.rb, a.B + rec * BDW_REC + h * BDW);
   // parameter word `lane` of the chunk: group c*VPC/16 + lane/16, row lane%16 (clamped to the row)
-  const int pg = min(c * (VPC / 16) + (lane & (VPC - 1)) / 16, a.ng - 1);
+  const int pg0 = c * (VPC / 16) + (lane & (VPC - 1)) / 16;
+  const int pg = min(pg0, a.ng - 1);
   R.pw = a.P[((int64_t)t * a.ng + pg) * 16 + (lane & 15)];
+  R.pok = pg0 < a.ng;
 #pragma unroll
   for (int b = 0; b < M; ++b) {
     const int bb = (M == 1 || b < a.m) ? b : 0;
-    R.xv[b] = *(const uint4*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v);
+    load_dw<4>(R.xv[b], (const uint32_t*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v));
   }
-  R.ok = ok;
 }
 
 // Rows of the record in batches of RB: all table lookups of a batch are issued before any
@@ -220,10 +227,10 @@ __device__ __forceinline__ void load_rec(Rec<KIND, M, RPL>& R, const KArgs& a, i
 template <int KIND, int D, int M, int RPL>
 __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL>& R, float (&acc)[M][RPL],
                                             const unsigned char* lds, uint32_t mask_off, uint32_t* pstage,
-                                            int lane, int h, int vloc, int m) {
+                                            int lane, int h, int vloc) {
   constexpr int RB = RPL < 4 ? RPL : 4;
   // group parameters: stage the chunk's words in this wave's LDS slot, read back this lane's rows
-  pstage[lane] = R.pw;
+  pstage[lane] = R.pok ? R.pw : 0u;
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -233,12 +240,6 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL>& R, float (&
   for (int i = 0; i < RPL; i += 4) {
     const uint4 u = *(const uint4*)(src + i);
     pp[i] = u.x; pp[i + 1] = u.y; pp[i + 2] = u.z; pp[i + 3] = u.w;
-  }
-  uint4 xv[M];
-#pragma unroll
-  for (int b = 0; b < M; ++b) {
-    const bool use = R.ok && (M == 1 || b < m);
-    xv[b] = use ? R.xv[b] : make_uint4(0, 0, 0, 0);
   }
   uint32_t qodd = 0;
   if constexpr (KIND == SPH_KIND_W2) qodd = R.rb[0] >> (4 * (h * RPL / 2));
@@ -268,7 +269,7 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL>& R, float (&
       const int r = r0 + i;
       const float rh = fmaf(qf[i], f16hi(pp[r]), f16lo(pp[r]));
 #pragma unroll
-      for (int b = 0; b < M; ++b) acc[b][r] = fmaf(rh, dot8(tt[i], xv[b]), acc[b][r]);
+      for (int b = 0; b < M; ++b) acc[b][r] = fmaf(rh, dot8(tt[i], R.xv[b]), acc[b][r]);
     }
   }
 }
@@ -318,10 +319,19 @@ __device__ __forceinline__ void slot_store(uint64_t* p, float v) {
                      __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Emit a finished item: straight to y when its tile has a single segment, else as partial sums
-// in the tile's slots (the tile's reducer adds them at the end of its own work).
-template <int M, int RPL>
-__device__ __forceinline__ void emit_item(const KArgs& a, float (&acc)[M][RPL], int t, int s, int lane, int h) {
+// The wave whose range holds step s (ranges are [floor(g*ts/gwa), floor((g+1)*ts/gwa))).
+__device__ __forceinline__ int wave_of_step(const KArgs& a, int64_t s) {
+  return __builtin_amdgcn_readfirstlane((int)(((s + 1) * a.gwa - 1) / a.ts));
+}
+
+// Finish the part [ca, cb) of tile t computed by wave g: reduce across lanes, then store y
+// (whole tile), hand the part over through slots (ca > 0), or, as the part holding chunk 0 of a
+// split tile (only possible when MAY_WAIT), add the other parts in chunk order and store y. The waits are bounded by a
+// deadline on the constant 100 MHz real-time counter (about 50 ms, thousands of times a whole
+// launch); a wait that runs out (not expected) stores NaN rather than hanging.
+template <int M, int RPL, bool MAY_WAIT>
+__device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[M][RPL], int t, int ca, int cb, int g,
+                                          int lane, int h) {
   constexpr int H = 16 / RPL;
   constexpr int NVAL = M * RPL, N4 = NVAL / 4;
   float vals[NVAL];
@@ -333,105 +343,163 @@ __device__ __forceinline__ void emit_item(const KArgs& a, float (&acc)[M][RPL], 
       acc[b][r] = 0.0f;
     }
   wave_reduce<NVAL, H>(vals, lane);
+  const bool writer = (lane & 15) < H;       // one writer lane per h in each 16-lane row
   const int base = ((lane >> 5) & 1) * (NVAL / 2) + ((lane >> 4) & 1) * N4;
-  if ((lane & 15) >= H) return;              // one writer lane per h in each 16-lane row
-  if (a.S == 1) {
+  int idx[N4];                               // slot index b*16 + row of value i
 #pragma unroll
-    for (int i = 0; i < N4; ++i) {
-      const int f = base + i, b = f / RPL, row = h * RPL + f % RPL;
-      const int grow = t * 16 + row;
-      if (b < a.m && grow < a.n) store_y(a, b, grow, vals[i]);
-    }
-  } else {
-    uint64_t* slot = a.ws_slot + ((int64_t)t * a.S + s) * (M * 16);
-#pragma unroll
-    for (int i = 0; i < N4; ++i) {
-      const int f = base + i, b = f / RPL, row = h * RPL + f % RPL;
-      slot_store(slot + b * 16 + row, vals[i]);
-    }
+  for (int i = 0; i < N4; ++i) {
+    const int f = base + i;
+    idx[i] = (f / RPL) * 16 + h * RPL + f % RPL;
   }
-}
-
-// Reducer of tile t: wait for every segment's slot to be valid (the segments are written by
-// waves that never wait before finishing their own items), add the segments in order, clear the
-// slots for the next call, write y. The wait is bounded by a deadline on the constant 100 MHz
-// real-time counter (about 50 ms, thousands of times a whole launch); a wait that runs out (not
-// expected) writes NaN rather than hanging.
-template <int M>
-__device__ __forceinline__ void reduce_tile(const KArgs& a, int t, int lane) {
-  uint64_t* slots = a.ws_slot + (int64_t)t * a.S * (M * 16);
-  const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + 5000000ull;
-  for (int j = lane; j < M * 16; j += 64) {
-    float sum = 0.0f;
-    bool ok = true;
-    for (int sg = 0; sg < a.S; ++sg) {
-      uint64_t* p = slots + sg * (M * 16) + j;
-      uint64_t w = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      while ((w >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline) {
-        __builtin_amdgcn_s_sleep(2);
-        w = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (ca > 0) {
+    if (!writer) return;
+    const int part = g - wave_of_step(a, (int64_t)t * a.nc);
+    uint64_t* slot = a.ws_slot + ((int64_t)t * a.pmax + part) * (M * 16);
+#pragma unroll
+    for (int i = 0; i < N4; ++i) slot_store(slot + idx[i], vals[i]);
+    return;
+  }
+  bool ok = true;
+  if (MAY_WAIT && cb < a.nc) {
+    // All 64 lanes fetch the other parts at once: lane l reads slot index l % NIDX of parts
+    // 1 + l / NIDX + PPI * j. Each lane adds its parts in increasing j, the lanes holding one slot
+    // index are then added by a fixed exchange tree, and the writer lanes add the result to their
+    // own part: a fixed order, independent of timing.
+    constexpr int NIDX = M * 16;
+    constexpr int PPI = NIDX >= 64 ? 1 : 64 / NIDX;   // parts per load instruction
+    constexpr int IPP = NIDX <= 64 ? 1 : NIDX / 64;   // load instructions per part
+    constexpr int JB = 8 / IPP;                       // parts per lane loaded together
+    const int np = wave_of_step(a, (int64_t)t * a.nc + a.nc - 1) - g + 1;
+    uint64_t* slots = a.ws_slot + (int64_t)t * a.pmax * NIDX;
+    const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + 5000000ull;
+    float ps[IPP];
+#pragma unroll
+    for (int k = 0; k < IPP; ++k) ps[k] = 0.0f;
+    const int loff = (NIDX >= 64) ? 0 : lane / NIDX;
+    for (int j0 = 0; 1 + loff + PPI * j0 < np; j0 += JB) {
+      uint64_t w[JB][IPP];
+#pragma unroll
+      for (int j = 0; j < JB; ++j) {
+        const int p = min(1 + loff + PPI * (j0 + j), np - 1);
+#pragma unroll
+        for (int k = 0; k < IPP; ++k)
+          w[j][k] = __hip_atomic_load(slots + (int64_t)p * NIDX + (lane % NIDX) + 64 * k, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
       }
-      ok = ok && (w >> 32) != 0;
-      sum += __builtin_bit_cast(float, (uint32_t)w);
-      __hip_atomic_store(p, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+      for (int j = 0; j < JB; ++j) {
+        const int p = 1 + loff + PPI * (j0 + j);
+        if (p < np) {
+#pragma unroll
+          for (int k = 0; k < IPP; ++k) {
+            uint64_t* q = slots + (int64_t)p * NIDX + (lane % NIDX) + 64 * k;
+            while ((w[j][k] >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline) {
+              __builtin_amdgcn_s_sleep(2);
+              w[j][k] = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            ok = ok && (w[j][k] >> 32) != 0;
+            ps[k] += __builtin_bit_cast(float, (uint32_t)w[j][k]);
+            __hip_atomic_store(q, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+        }
+      }
     }
-    const int b = j / 16, grow = t * 16 + (j % 16);
-    if (b < a.m && grow < a.n) store_y(a, b, grow, ok ? sum : __builtin_nanf(""));
+    // lanes l and l ^ NIDX, ... hold the same slot index: add them, larger distances first
+    if constexpr (NIDX <= 16) ps[0] += __shfl_xor(ps[0], 32);
+    if constexpr (NIDX <= 16) ps[0] += __shfl_xor(ps[0], 16);
+    if constexpr (NIDX == 32) ps[0] += __shfl_xor(ps[0], 32);
+    const bool all_ok = __all(ok);
+#pragma unroll
+    for (int i = 0; i < N4; ++i) {
+      const int src = idx[i] % 64, k = idx[i] / 64;
+      float other = 0.0f;
+#pragma unroll
+      for (int kk = 0; kk < IPP; ++kk) {
+        const float v = __shfl(ps[kk], src);
+        if (kk == k) other = v;
+      }
+      vals[i] += other;
+    }
+    ok = all_ok;
+  }
+  if (!writer) return;
+#pragma unroll
+  for (int i = 0; i < N4; ++i) {
+    const int b = idx[i] / 16, grow = t * 16 + idx[i] % 16;
+    if (b < a.m && grow < a.n) store_y(a, b, grow, ok ? vals[i] : __builtin_nanf(""));
   }
 }
 
-// A wave's position in its sequence of (item, chunk) steps; wave-uniform.
-struct Pos {
-  int item, t, s, c, cend;
-  bool live;
+// Lookup tables staged in two halves around the first record's loads: the table words are
+// fetched first, the record loads are issued behind them, and the LDS stores wait only for the
+// table words, so the first record's memory round trip overlaps the staging.
+template <int KIND, int D>
+struct TableWords {
+  static constexpr int N16 = (int)((Tables<KIND, D>::bytes - (KIND == SPH_KIND_CB13 ? 128u : 0u)) / 16u);
+  static constexpr int PER = (N16 + 1023) / 1024;
+  uint4 w[PER];
 };
 
-__device__ __forceinline__ Pos first_pos(const KArgs& a, int item) {
-  Pos p;
-  item = __builtin_amdgcn_readfirstlane(item);
-  p.item = item;
-  p.live = item < a.items;
-  p.t = item / a.S;
-  p.s = item % a.S;
-  p.c = p.s * a.cps;
-  p.cend = min(a.nc, p.c + a.cps);
-  return p;
-}
-
-__device__ __forceinline__ Pos next_pos(const KArgs& a, const Pos& p) {
-  if (p.c + 1 < p.cend) {
-    Pos q = p;
-    q.c = p.c + 1;
-    return q;
+template <int KIND, int D>
+__device__ __forceinline__ void fetch_tables(TableWords<KIND, D>& tw, const KArgs& a) {
+  constexpr int N16 = TableWords<KIND, D>::N16;
+#pragma unroll
+  for (int i = 0; i < TableWords<KIND, D>::PER; ++i) {
+    const int j = (int)threadIdx.x + 1024 * i;
+    tw.w[i] = a.T[j < N16 ? j : N16 - 1];
   }
-  return first_pos(a, p.item + a.gw);
 }
 
-// Persistent waves walk balanced items (a tile and a run of chunks) in steps of one record.
-// Two record buffers in ping-pong: the loads of step i+1 are in flight while step i is computed,
-// and no register copy ever waits on loads still in flight; the step after the last one
-// re-reads a valid record so that the loads stay unconditional. Emitting an item never waits
-// on memory, so the pipeline runs through item boundaries; split tiles are reduced at the end.
+template <int KIND, int D>
+__device__ __forceinline__ void store_tables(unsigned char* lds, const TableWords<KIND, D>& tw, const KArgs& a) {
+  constexpr int N16 = TableWords<KIND, D>::N16;
+#pragma unroll
+  for (int i = 0; i < TableWords<KIND, D>::PER; ++i) {
+    const int j = (int)threadIdx.x + 1024 * i;
+    if (j < N16) ((uint4*)lds)[j] = tw.w[i];
+  }
+  if constexpr (KIND == SPH_KIND_CB13) {
+    // mask[s] flips the fp16 sign bit of element j (of 4) where bit j of the nibble s is set.
+    if (threadIdx.x < 16) {
+      const uint32_t s = threadIdx.x;
+      uint2 m;
+      m.x = ((s & 1u) << 15) | ((s & 2u) << 30);
+      m.y = ((s & 4u) << 13) | ((s & 8u) << 28);
+      *(uint2*)(lds + a.t_bytes + s * 8u) = m;
+    }
+  }
+}
+
+// Two record buffers in ping-pong: the loads of step i+1 are in flight while step i is computed;
+// past the end of the range the loads re-read the range's first record so that they stay
+// unconditional. Finishing a tile part never waits on memory except in the part holding chunk 0
+// of a split tile, which is the last thing its wave does.
 template <int KIND, int D, int M, int RPL>
 __global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
   __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes];
   __shared__ __align__(16) uint32_t pstage_all[16 * 64];
-  __shared__ int red_list[16 * 32];
   constexpr int H = 16 / RPL;
-  stage_tables<KIND>(lds, a);
+  const int lane = threadIdx.x & 63;
+  // wave-uniform by construction; readfirstlane keeps the schedule in SGPRs
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = (int)blockIdx.x * a.wpb + wave;
+  const bool active = g < a.gwa;
+  // The range bounds are wave-uniform; readfirstlane keeps them (and every branch on them) scalar.
+  const int s_begin = __builtin_amdgcn_readfirstlane(active ? (int)((int64_t)g * a.ts / a.gwa) : 0);
+  const int s_end = __builtin_amdgcn_readfirstlane(active ? (int)((int64_t)(g + 1) * a.ts / a.gwa) : 1);
+  const int t0 = __builtin_amdgcn_readfirstlane(s_begin / a.nc);
+  const int c0 = s_begin - t0 * a.nc;
+  const int h = lane % H, vloc = lane / H;
+
+  Rec<KIND, M, RPL> r0, r1;
+  TableWords<KIND, D> tw;
+  fetch_tables<KIND, D>(tw, a);
+  load_rec<KIND, M, RPL>(r0, a, t0, c0, h, vloc, lane);
+  store_tables<KIND, D>(lds, tw, a);
   const uint32_t mask_off = a.t_bytes;
   __syncthreads();
-
-  const int lane = threadIdx.x & 63;
-  // wave-uniform by construction; readfirstlane keeps the schedule in SGPRs. Items are striped
-  // over workgroups first so that every CU gets a share.
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  Pos p0 = first_pos(a, wave * (int)gridDim.x + blockIdx.x);
-  if (!p0.live) return;                        // no barrier follows
+  if (!active) return;                       // no barrier follows
   uint32_t* pstage = pstage_all + wave * 64;
-  int* reds = red_list + wave * 32;
-  int nred = 0;
-  const int h = lane % H, vloc = lane / H;
 
   float acc[M][RPL];
 #pragma unroll
@@ -439,35 +507,44 @@ __global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
 #pragma unroll
     for (int r = 0; r < RPL; ++r) acc[b][r] = 0.0f;
 
-  Rec<KIND, M, RPL> r0, r1;
-  load_rec<KIND, M, RPL>(r0, a, p0.t, p0.c, h, vloc, lane);
-  while (true) {
-    const Pos p1 = next_pos(a, p0);
-    load_rec<KIND, M, RPL>(r1, a, p1.live ? p1.t : p0.t, p1.live ? p1.c : p0.c, h, vloc, lane);
-    compute_rec<KIND, D, M, RPL>(r0, acc, lds, mask_off, pstage, lane, h, vloc, a.m);
-    if (p0.c + 1 >= p0.cend) {
-      emit_item<M, RPL>(a, acc, p0.t, p0.s, lane, h);
-      if (a.S > 1 && p0.s == 0) {
-        if (lane == 0) reds[nred] = p0.t;
-        ++nred;
-      }
+  // Steps go in pairs, one per buffer, so that the loop has a single exit at the bottom (an
+  // early exit would give the compiler a path back to the loop head with loads still pending,
+  // and it would wait for them). Tile parts that end inside the range are whole tiles or later
+  // parts of split tiles, which only store; the range's last part, which may be the waiting
+  // part holding chunk 0, is finished after the loop.
+  const int nsteps = s_end - s_begin;
+  const int npairs = nsteps >> 1;
+  int t = t0, c = c0;                        // position of step 2i
+  int tl = t0, cl = c0;                      // position of the last step computed
+  for (int i = 0; i < npairs; ++i) {
+    int t1 = t, c1 = c + 1;
+    if (c1 == a.nc) {
+      ++t1;
+      c1 = 0;
     }
-    if (!p1.live) break;
-    const Pos p2 = next_pos(a, p1);
-    load_rec<KIND, M, RPL>(r0, a, p2.live ? p2.t : p1.t, p2.live ? p2.c : p1.c, h, vloc, lane);
-    compute_rec<KIND, D, M, RPL>(r1, acc, lds, mask_off, pstage, lane, h, vloc, a.m);
-    if (p1.c + 1 >= p1.cend) {
-      emit_item<M, RPL>(a, acc, p1.t, p1.s, lane, h);
-      if (a.S > 1 && p1.s == 0) {
-        if (lane == 0) reds[nred] = p1.t;
-        ++nred;
-      }
+    load_rec<KIND, M, RPL>(r1, a, t1, c1, h, vloc, lane);
+    compute_rec<KIND, D, M, RPL>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
+    if (c1 == 0) emit_part<M, RPL, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h);
+    int t2 = t1, c2 = c1 + 1;
+    if (c2 == a.nc) {
+      ++t2;
+      c2 = 0;
     }
-    if (!p2.live) break;
-    p0 = p2;
+    const bool has2 = 2 * i + 2 < nsteps;
+    load_rec<KIND, M, RPL>(r0, a, has2 ? t2 : t0, has2 ? c2 : c0, h, vloc, lane);
+    compute_rec<KIND, D, M, RPL>(r1, acc, lds, mask_off, pstage, lane, h, vloc);
+    if (has2 && c2 == 0) emit_part<M, RPL, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, h);
+    tl = t1;
+    cl = c1;
+    t = t2;
+    c = c2;
   }
-  // The reducer role comes last, after this wave has produced all of its own partial sums.
-  for (int i = 0; i < nred; ++i) reduce_tile<M>(a, __builtin_amdgcn_readfirstlane(reds[i]), lane);
+  if (nsteps & 1) {
+    compute_rec<KIND, D, M, RPL>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
+    tl = t;
+    cl = c;
+  }
+  emit_part<M, RPL, true>(a, acc, tl, tl == t0 ? c0 : 0, cl + 1, g, lane, h);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -599,7 +676,7 @@ struct Launch {
   int block;          // threads per workgroup
   int grid;
   int wpt;            // matrix-core kernel: waves per tile
-  int nc, cps, S, items;
+  int nc, gwa, pmax, ts;
   size_t ws_bytes;    // workspace the launch needs
 };
 
@@ -679,10 +756,8 @@ int num_cus() {
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
-// Work plan. Vector-ALU path: persistent waves filling every CU to the occupancy the kernel
-// allows.
-// The chunks-per-item count minimises the rounds of items times their length plus a fixed
-// cost per item for its reduction.
+// Work plan. Vector-ALU path: one 16-wave workgroup per CU, every wave a contiguous range of
+// steps (at least one). Matrix-core path: a workgroup per tile, its waves splitting K.
 Launch plan(const sph_weights* w, int m) {
   Launch L{};
   const int64_t nv = w->k / 8, nt = (w->n + 15) / 16;
@@ -693,35 +768,19 @@ Launch plan(const sph_weights* w, int m) {
     const int H = M <= 2 ? 1 : M == 4 ? 2 : 4;
     const int vpc = 64 / H;
     const int wpb = 16;                         // one 16-wave workgroup per CU
-    const int grid = cus;
-    const int64_t gw = (int64_t)grid * wpb;
     const int64_t nc = (nv + vpc - 1) / vpc;
-    // Cost of a plan: rounds of items times (record batches per item + a fixed cost per batch
-    // and per item). Split plans (S > 1) pay an extra reduction at the end of the waves' work.
-    int64_t best_cps = 1;
-    double best = 1e300;
-    for (int64_t cps = 1; cps <= nc; ++cps) {
-      const int64_t S = (nc + cps - 1) / cps;
-      const int64_t items = nt * S;
-      const int64_t rounds = (items + gw - 1) / gw;
-      if (S > 1 && rounds > 32) continue;       // reducer list bound per wave
-      // steps of the busiest wave, plus a small cost per item (its reduction) and one for the
-      // split reduction at the end of the waves' work
-      const double cost = (double)rounds * ((double)cps + 0.5) + (S > 1 ? 2.0 : 0.0);
-      if (cost < best - 1e-9) {
-        best = cost;
-        best_cps = cps;
-      }
-    }
+    const int64_t ts = nt * nc;
+    const int64_t gw = (int64_t)cus * wpb;
+    const int64_t gwa = ts < gw ? ts : gw;
     L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, false, M);
     L.block = 64 * wpb;
+    L.grid = (int)((gwa + wpb - 1) / wpb);
     L.nc = (int)nc;
-    L.cps = (int)best_cps;
-    L.S = (int)((nc + best_cps - 1) / best_cps);
-    L.items = (int)(nt * L.S);
-    const int64_t need = (L.items + wpb - 1) / wpb;
-    L.grid = (int)(need < grid ? need : grid);
-    L.ws_bytes = L.S > 1 ? (size_t)nt * L.S * M * 16 * 8 : 0;
+    L.ts = (int)ts;
+    L.gwa = (int)gwa;
+    // a range holds at least ts/gwa steps, so a tile meets at most nc/(ts/gwa) + 2 ranges
+    L.pmax = (int)(nc / (ts / gwa) + 2);
+    L.ws_bytes = (nt % gwa != 0) ? (size_t)nt * L.pmax * M * 16 * 8 : 0;
   } else {
     const int NB = m <= 16 ? 1 : 2;
     const int64_t per_wave = 4 * 8;             // 8 MFMA steps per wave
@@ -846,10 +905,9 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
   KArgs a = make_args(w);
   a.nc = L.nc;
   a.wpb = L.block / 64;
-  a.gw = L.grid * (L.block / 64);
-  a.cps = L.cps;
-  a.S = L.S;
-  a.items = L.items;
+  a.gwa = L.gwa;
+  a.pmax = L.pmax;
+  a.ts = L.ts;
   if (L.ws_bytes > 0) a.ws_slot = (uint64_t*)d_ws;
   a.x = (const uint16_t*)d_x;
   a.ldx = ldx;

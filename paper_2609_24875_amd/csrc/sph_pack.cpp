@@ -1,3 +1,4 @@
+#include <stdint.h>
 // Host side of the library: argument validation and packing of logical SPHQuant codes
 // (Sec. 3.1, Eq. 3-7) into the device layout described in sph_layout.h. Pure C++: no HIP
 // headers, so it also builds and runs with g++ on a machine without a GPU.
@@ -23,6 +24,8 @@ int sph_host_check_format(const sph_format* fmt) {
 int sph_host_check_shape(int64_t n, int64_t k) {
   if (n < 1 || n > (int64_t(1) << 24)) return SPH_ERR_SHAPE;
   if (k < SPH_GROUP || k % SPH_GROUP != 0 || k > (int64_t(1) << 20)) return SPH_ERR_SHAPE;
+  // records (16-row tiles x vector positions) are counted in 32 bits by the kernels' work plans
+  if ((n + SPH_TILE_ROWS - 1) / SPH_TILE_ROWS * (k / SPH_VEC) > INT32_MAX) return SPH_ERR_SHAPE;
   return SPH_OK;
 }
 

@@ -1,16 +1,18 @@
 """Benchmark of the SPHQuant decode path on one MI355X.
 
-A step is one decode forward through every linear layer of a backbone: for each of the L layers
-the seven projections (q, k, v, o, gate, up, down) run as sph_gemv (batch 1) or
-sph_gemm_small (batch > 1) on their own packed copy in HBM, so the weight stream is never served
-from the 256 MB Infinity Cache. The step is captured once in a HIP graph and replayed.
+A step is one decode forward through every linear layer of a backbone. The projections that
+read the same activations are packed as one matrix, as decode engines do (q, k and v stacked
+into one qkv matrix, gate and up into one gate_up matrix): per layer the launches are qkv, o,
+gate_up and down, each as sph_gemv (batch 1) or sph_gemm_small (batch > 1) on its own packed
+copy in HBM, so the weight stream is never served from the 256 MB Infinity Cache. The step is
+captured once in a HIP graph and replayed. --unfused runs the seven projections separately.
 
 Default workload: W2 (8 sign + 6 direction + 4 radius bits per 8-vector), 32B-class shapes
 (q/o 5120x5120, k/v 1024x5120, gate/up 25600x5120, down 5120x25600), 64 layers, batch 1:
-9.12 GB of packed weights per step.
+9.13 GB of packed weights per step.
 
 Prints one JSON line: whole-step packed-weight GB/s (`value`), linear-layer tokens/s, the
-roofline of the dominant kernel (the batch-1 GEMV on the 25600x5120 / 5120x25600 shapes), and
+roofline of the dominant kernel (the decode of the largest matrices: gate_up and down), and
 the fp64 CPU oracle timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -30,6 +32,23 @@ if ROOT not in sys.path:
 import synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.hip")
+
+# HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE + WRITE_SIZE runs, each
+# scaled by the reading of a plain device copy of known size (see profiles/). Keyed by the
+# SHA-256 of the kernel source the counters were taken with: any change to the kernels makes
+# the entry stale and `traffic` is reported as null.
+TRAFFIC = {
+    "52292062d28dec49ea6b1387ed92a7d4dfae49209c12e217437b279045db9ef2": {
+        "7168x5120-m1": 14986716, "5120x5120-m1": 10989776,
+        "51200x5120-m1": 85416048, "5120x25600-m1": 45083731},
+}
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
 
 
 def parse():
@@ -42,14 +61,35 @@ def parse():
     ap.add_argument("--layers", type=int, default=0, help="override layer count (0: workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
+    ap.add_argument("--unfused", action="store_true", help="launch q, k, v, gate, up separately")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (HBM counter calibration)")
     return ap.parse_args()
 
 
-def make_layer0(wl, fmt, m):
+FUSED = (("qkv", ("q", "k", "v")), ("o", ("o",)), ("gate_up", ("gate", "up")), ("down", ("down",)))
+
+
+def layer_shapes(wl, fused: bool):
+    """((label, n, k), ...) of the launches of one layer."""
+    if not fused:
+        return tuple(wl.shapes)
+    by = {label: (n, k) for label, n, k in wl.shapes}
+    if not all(m in by for _, members in FUSED for m in members):
+        return tuple(wl.shapes)
+    out = []
+    for label, members in FUSED:
+        ks = {by[m][1] for m in members}
+        assert len(ks) == 1
+        out.append((label, sum(by[m][0] for m in members), ks.pop()))
+    return tuple(out)
+
+
+def make_layer0(wl, fmt, m, shapes):
     """Codes, codebooks and activations of layer 0's matrices (seeded, uniform codes)."""
     D, V = synth.FORMATS[fmt]
     mats = []
-    for mi, (label, n, k) in enumerate(wl.shapes):
+    for mi, (label, n, k) in enumerate(shapes):
         g = synth.rng(wl_id(wl), 0, mi, synth.STREAM_CODES)
         codes = synth.uniform_codes(n, k, D, V, g)
         codes["gmin"], codes["gstep"] = synth.row_scale_group_params(n, k, V, g)
@@ -67,8 +107,9 @@ def wl_id(wl):
 
 
 def cpu_baseline(mats, budget_s, step_bytes_total, per_mat_bytes, layers):
-    """Time the fp64 oracle (decode + dot) on whole matrices of layer 0 until the budget is
-    used; report packed-weight GB/s over the matrices it finished."""
+    """Time the fp64 oracle (decode + dot) on whole matrices of the workload's layer shapes,
+    cycling through the layer's matrices until the time budget is used; report packed-weight
+    GB/s over the matrices it finished (each finished matrix counts its packed bytes)."""
     from oracle import sph as O
     try:
         from threadpoolctl import threadpool_info
@@ -76,14 +117,13 @@ def cpu_baseline(mats, budget_s, step_bytes_total, per_mat_bytes, layers):
     except Exception:
         threads = int(os.environ.get("OMP_NUM_THREADS") or os.cpu_count())
     done_bytes = 0
-    names = []
+    done = 0
     t0 = time.perf_counter()
-    for (label, n, k, codes, cb, x), nbytes in zip(mats, per_mat_bytes):
+    while time.perf_counter() - t0 < budget_s:
+        (label, n, k, codes, cb, x), nbytes = mats[done % len(mats)], per_mat_bytes[done % len(mats)]
         O.gemm(codes, cb, x)
         done_bytes += nbytes
-        names.append(f"{label} {n}x{k}")
-        if time.perf_counter() - t0 > budget_s:
-            break
+        done += 1
     dt = time.perf_counter() - t0
     gbs = done_bytes / dt / 1e9
     return {
@@ -91,8 +131,10 @@ def cpu_baseline(mats, budget_s, step_bytes_total, per_mat_bytes, layers):
         "unit": "GB/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": f"layer 0 matrices [{', '.join(names)}] of {layers} layers, {dt:.1f} s; "
-                  f"step-equivalent {step_bytes_total / gbs / 1e9 * 1e3:.0f} ms",
+        "sample": f"{done} matrix decodes cycling over one layer's shapes "
+                  f"[{', '.join(f'{m[0]} {m[1]}x{m[2]}' for m in mats)}] of the {layers}-layer step, "
+                  f"{done_bytes / 1e9:.2f} GB of packed weights in {dt:.1f} s; "
+                  f"step-equivalent {step_bytes_total / gbs / 1e9:.1f} s",
     }
 
 
@@ -114,11 +156,20 @@ def main():
     D, V = synth.FORMATS[fmt]
     m = args.batch
     layers = args.layers or wl.layers
+    shapes = layer_shapes(wl, not args.unfused)
     pkg.load_library()
+    if args.copy_calib_mib:
+        # one plain copy of known size, so that HBM byte counters can be scaled
+        nb = args.copy_calib_mib << 20
+        src = torch.ones(nb // 4, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---- inputs: layer 0 generated and packed, then replicated per layer (distinct buffers)
     t_setup = time.perf_counter()
-    mats = make_layer0(wl, fmt, m)
+    mats = make_layer0(wl, fmt, m, shapes)
     packed = []
     for label, n, k, codes, cb, x in mats:
         w0 = pkg.pack(D, V, codes, cb, device=dev)
@@ -215,6 +266,7 @@ def main():
             "batch": m,
             "packed_bytes_per_step": step_bytes,
             "launches_per_step": layers * len(packed),
+            "fused": "none" if args.unfused or shapes == tuple(wl.shapes) else "qkv, gate_up",
             "graph": True,
         },
         "tokens_per_s": round(m / (ms / 1e3), 2),
@@ -227,7 +279,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": TRAFFIC.get(kernel_source_hash(), {}).get(f"{big[0][1]}x{big[0][2]}-m{m}"),
             "avg_launch_us": round(dom_us, 3),
             "bytes_per_launch": int(dom_bytes),
         },

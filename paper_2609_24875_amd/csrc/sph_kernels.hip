@@ -471,8 +471,8 @@ __device__ __forceinline__ void store_tables(unsigned char* lds, const TableWord
 }
 
 // Two record buffers in ping-pong: the loads of step i+1 are in flight while step i is computed;
-// past the end of the range the loads re-read the range's first record so that they stay
-// unconditional. Finishing a tile part never waits on memory except in the part holding chunk 0
+// past the end of the range the loads re-read the record loaded just before (still in cache,
+// so it costs no HBM traffic) so that they stay unconditional. Finishing a tile part never waits on memory except in the part holding chunk 0
 // of a split tile, which is the last thing its wave does.
 template <int KIND, int D, int M, int RPL>
 __global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
@@ -531,7 +531,7 @@ __global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
       c2 = 0;
     }
     const bool has2 = 2 * i + 2 < nsteps;
-    load_rec<KIND, M, RPL>(r0, a, has2 ? t2 : t0, has2 ? c2 : c0, h, vloc, lane);
+    load_rec<KIND, M, RPL>(r0, a, has2 ? t2 : t1, has2 ? c2 : c1, h, vloc, lane);
     compute_rec<KIND, D, M, RPL>(r1, acc, lds, mask_off, pstage, lane, h, vloc);
     if (has2 && c2 == 0) emit_part<M, RPL, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, h);
     tl = t1;

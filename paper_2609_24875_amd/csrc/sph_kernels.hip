@@ -16,6 +16,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cstring>
 #include <vector>
@@ -41,10 +42,13 @@ struct KArgs {
   int y_f16;
   int n, nt, nv, ng, m;
   int wpt;            // waves per tile (matrix-core kernel)
-  // vector-ALU work plan: ts = nt * nc steps in tile-major order, cut into gwa contiguous and
-  // balanced wave ranges
+  // vector-ALU work plan: ts = nt * nc steps in tile-major order, cut into one contiguous range
+  // per workgroup (whole tiles when wg_tiles > 0, else balanced to one step), each cut evenly
+  // among the workgroup's waves
   int nc;             // steps (chunks of vector positions) per tile
-  int gwa;            // waves with work
+  int nwg;            // workgroups
+  int wg_tiles;       // tiles per workgroup, or 0 for balanced ranges
+  int wq, wr;         // balanced ranges: ts = (nwg * VALU_WPB) * wq + wr
   int wpb;            // waves per workgroup
   int pmax;           // slot parts per tile
   int ts;
@@ -177,6 +181,14 @@ __device__ __forceinline__ void store_y(const KArgs& a, int b, int row, float v)
 // long before that wave reaches its end; the order of the sum is fixed, so results do not depend
 // on scheduling.
 // ------------------------------------------------------------------------------------------
+// Waves per workgroup of the vector-ALU kernel, and workgroups resident per CU.
+constexpr int VALU_WPB = 16;
+constexpr int VALU_WG_PER_CU = 1;
+constexpr int VALU_THREADS = 64 * VALU_WPB;
+// Rows per batch of table lookups, and whether lookup batches are pinned in pipelined order.
+constexpr int VALU_RB = 4;
+constexpr bool VALU_PIPE_BARRIERS = true;
+
 template <int KIND, int D>
 struct Tables {
   static constexpr uint32_t bytes = (KIND == SPH_KIND_CB13) ? ((16u << D) + 128u) : (256u << D);
@@ -222,13 +234,39 @@ __device__ __forceinline__ void load_rec(Rec<KIND, M, RPL>& R, const KArgs& a, i
   }
 }
 
-// Rows of the record in batches of RB: all table lookups of a batch are issued before any
-// of its arithmetic, so one LDS round trip serves RB rows.
+// Table lookups of the rows [r0, r0 + RB) of a record: field extraction and the LDS reads.
+template <int KIND, int D, int M, int RPL, int RB>
+__device__ __forceinline__ void lookup_rows(const Rec<KIND, M, RPL>& R, int r0, uint32_t qodd, const unsigned char* lds,
+                                            uint32_t mask_off, uint4 (&tt)[RB], float (&qf)[RB]) {
+#pragma unroll
+  for (int i = 0; i < RB; ++i) {
+    const int r = r0 + i;
+    uint32_t q;
+    if constexpr (KIND == SPH_KIND_CB13) {
+      uint32_t s, z;
+      decode_cb13(R.ra[r / 4], r % 4, R.rb[r / 2], r & 1, s, z, q);
+      tt[i] = signed_dir_cb13(lds, mask_off, s, z);
+    } else {
+      uint32_t lo, hi, qx = 0;
+      if constexpr (KIND == SPH_KIND_W2) qx = (qodd >> (4 * (r / 2))) & 15u;
+      if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (R.rb[r / 4] >> (8 * (r % 4))) & 0xFFu;
+      decode_nib<KIND, D>(R.ra[r / 2], r & 1, qx, lo, hi, q);
+      tt[i] = signed_dir_nib<KIND, D>(lds, lo, hi);
+    }
+    qf[i] = (float)q;
+  }
+}
+
+// The rows of a record in batches of RB, software-pipelined: the lookups of batch j+1 are issued
+// before the arithmetic of batch j, and scheduling barriers keep the compiler from interleaving
+// them back (left alone, it keeps only a few LDS reads in flight per wave, far fewer than the
+// LDS latency under bank conflicts needs).
 template <int KIND, int D, int M, int RPL>
 __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL>& R, float (&acc)[M][RPL],
                                             const unsigned char* lds, uint32_t mask_off, uint32_t* pstage,
                                             int lane, int h, int vloc) {
-  constexpr int RB = RPL < 4 ? RPL : 4;
+  constexpr int RB = RPL < VALU_RB ? RPL : VALU_RB;
+  constexpr int NB = RPL / RB;
   // group parameters: stage the chunk's words in this wave's LDS slot, read back this lane's rows
   pstage[lane] = R.pok ? R.pw : 0u;
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -243,47 +281,39 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL>& R, float (&
   }
   uint32_t qodd = 0;
   if constexpr (KIND == SPH_KIND_W2) qodd = R.rb[0] >> (4 * (h * RPL / 2));
+  uint4 tt[2][RB];
+  float qf[2][RB];
+  lookup_rows<KIND, D, M, RPL, RB>(R, 0, qodd, lds, mask_off, tt[0], qf[0]);
 #pragma unroll
-  for (int r0 = 0; r0 < RPL; r0 += RB) {
-    uint4 tt[RB];
-    float qf[RB];
-#pragma unroll
-    for (int i = 0; i < RB; ++i) {
-      const int r = r0 + i;
-      uint32_t q;
-      if constexpr (KIND == SPH_KIND_CB13) {
-        uint32_t s, z;
-        decode_cb13(R.ra[r / 4], r % 4, R.rb[r / 2], r & 1, s, z, q);
-        tt[i] = signed_dir_cb13(lds, mask_off, s, z);
-      } else {
-        uint32_t lo, hi, qx = 0;
-        if constexpr (KIND == SPH_KIND_W2) qx = (qodd >> (4 * (r / 2))) & 15u;
-        if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (R.rb[r / 4] >> (8 * (r % 4))) & 0xFFu;
-        decode_nib<KIND, D>(R.ra[r / 2], r & 1, qx, lo, hi, q);
-        tt[i] = signed_dir_nib<KIND, D>(lds, lo, hi);
-      }
-      qf[i] = (float)q;
-    }
+  for (int j = 0; j < NB; ++j) {
+    if (j + 1 < NB) lookup_rows<KIND, D, M, RPL, RB>(R, (j + 1) * RB, qodd, lds, mask_off, tt[(j + 1) & 1], qf[(j + 1) & 1]);
+    if constexpr (VALU_PIPE_BARRIERS) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < RB; ++i) {
-      const int r = r0 + i;
-      const float rh = fmaf(qf[i], f16hi(pp[r]), f16lo(pp[r]));
+      const int r = j * RB + i;
+      const float rh = fmaf(qf[j & 1][i], f16hi(pp[r]), f16lo(pp[r]));
 #pragma unroll
-      for (int b = 0; b < M; ++b) acc[b][r] = fmaf(rh, dot8(tt[i], R.xv[b]), acc[b][r]);
+      for (int b = 0; b < M; ++b) acc[b][r] = fmaf(rh, dot8(tt[j & 1][i], R.xv[b]), acc[b][r]);
     }
+    if constexpr (VALU_PIPE_BARRIERS) __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// Exchange-and-add across lanes l and l^DIST: lanes with bit DIST clear end with
-// lo_keep[l] + lo_keep[l^DIST], the others with hi_keep[l] + hi_keep[l^DIST]. (The gfx950
-// permlane-swap builtins would do this in one instruction, but this compiler version folds the
-// sum of their two results into twice one of them, so they are not used.)
+// Exchange-and-add across lanes l and l^DIST (DIST = 32 or 16): lanes with bit DIST clear end
+// with lo_keep[l] + lo_keep[l^DIST], the others with hi_keep[l] + hi_keep[l^DIST]. This is one
+// gfx950 half-swap (v_permlane32_swap / v_permlane16_swap exchange the upper half of the first
+// register with the lower half of the second, at 32- or 16-lane granularity) and an add, all on
+// the vector ALU. The swap is written in assembly because this compiler version returns the
+// first register twice from the builtin's result pair; the leading s_nop gives the two wait
+// states the instruction needs after a vector write of its operands, which the compiler cannot
+// see through the assembly, and the trailing one is conservative.
 template <int DIST>
 __device__ __forceinline__ float xchg_add(float lo_keep, float hi_keep, int lane) {
-  const bool bit = (lane & DIST) != 0;
-  const float send = bit ? lo_keep : hi_keep;
-  const float keep = bit ? hi_keep : lo_keep;
-  return keep + __shfl_xor(send, DIST);
+  (void)lane;
+  float a = lo_keep, b = hi_keep;
+  if constexpr (DIST == 32) asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+  else asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+  return a + b;
 }
 
 template <int CTRL>
@@ -319,19 +349,87 @@ __device__ __forceinline__ void slot_store(uint64_t* p, float v) {
                      __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// The wave whose range holds step s (ranges are [floor(g*ts/gwa), floor((g+1)*ts/gwa))).
-__device__ __forceinline__ int wave_of_step(const KArgs& a, int64_t s) {
-  return __builtin_amdgcn_readfirstlane((int)(((s + 1) * a.gwa - 1) / a.ts));
+// n steps cut into `parts` contiguous pieces, the first n % parts of them one step longer: the
+// start of piece i, and the piece holding step x. 32-bit arithmetic only (the kernel computes
+// these in its prologue, before its first loads).
+__device__ __forceinline__ int piece_start(int n, int parts, int i) {
+  const int q = n / parts, r = n - q * parts;
+  return i * q + min(i, r);
+}
+__device__ __forceinline__ int piece_of(int n, int parts, int x) {
+  const int q = n / parts, r = n - q * parts;
+  return x < r * (q + 1) ? x / (q + 1) : r + (x - r * (q + 1)) / q;
+}
+
+// Step ranges. With wg_tiles > 0 workgroup b owns tiles [b*wg_tiles, (b+1)*wg_tiles) and cuts
+// their steps into nw = min(VALU_WPB, n) pieces, one per wave. Otherwise the ts steps are spread
+// over all gw = nwg * VALU_WPB waves of the grid: wave g starts at floor(g * ts / gw), written as
+// g * wq + floor(g * wr / gw) so that it stays in 32 bits (g * wr < gw^2).
+__device__ __forceinline__ void wg_range(const KArgs& a, int b, int& s0, int& s1) {
+  s0 = min(b * a.wg_tiles, a.nt) * a.nc;
+  s1 = min((b + 1) * a.wg_tiles, a.nt) * a.nc;
+}
+
+__device__ __forceinline__ int spread_start(const KArgs& a, int g) {
+  const int gw = a.nwg * VALU_WPB;
+  return g * a.wq + (g * a.wr) / gw;
+}
+
+// The wave (id = workgroup * VALU_WPB + wave in workgroup) whose range holds step s.
+__device__ __forceinline__ int wave_of_step(const KArgs& a, int s) {
+  if (a.wg_tiles == 0) {
+    const int64_t gw = (int64_t)a.nwg * VALU_WPB;
+    return __builtin_amdgcn_readfirstlane((int)(((int64_t)(s + 1) * gw - 1) / a.ts));
+  }
+  const int b = s / (a.wg_tiles * a.nc);
+  int s0, s1;
+  wg_range(a, b, s0, s1);
+  const int n = s1 - s0;
+  return __builtin_amdgcn_readfirstlane(b * VALU_WPB + piece_of(n, min(VALU_WPB, n), s - s0));
+}
+
+// Slot words of the other parts of a split tile, fetched by the wave holding chunk 0 before it
+// computes its last step, so that their round trip overlaps that computation: lane l reads slot
+// index l % NIDX of parts 1 + l / NIDX + PPI * j, j < JB.
+template <int M>
+struct SlotPre {
+  static constexpr int NIDX = M * 16;
+  static constexpr int PPI = NIDX >= 64 ? 1 : 64 / NIDX;   // parts per load instruction
+  static constexpr int IPP = NIDX <= 64 ? 1 : NIDX / 64;   // load instructions per part
+  static constexpr int JB = 4 / IPP;                       // parts per lane loaded together
+  uint64_t w[JB][IPP];
+};
+
+// Parts held by waves of the same workgroup are handed over through LDS instead (see emit_part);
+// only the parts of other workgroups are fetched here.
+template <int M>
+__device__ __forceinline__ void fetch_parts(SlotPre<M>& P, const KArgs& a, int t, int np, int j0, int g, int lane) {
+  using S = SlotPre<M>;
+  const uint64_t* slots = a.ws_slot + (int64_t)t * a.pmax * S::NIDX;
+  const int loff = (S::NIDX >= 64) ? 0 : lane / S::NIDX;
+#pragma unroll
+  for (int j = 0; j < S::JB; ++j) {
+    const int p = min(1 + loff + S::PPI * (j0 + j), np - 1);
+    const bool same_wg = (g + p) / VALU_WPB == g / VALU_WPB;
+#pragma unroll
+    for (int k = 0; k < S::IPP; ++k)
+      P.w[j][k] = same_wg ? 0ull
+                          : __hip_atomic_load(slots + (int64_t)p * S::NIDX + (lane % S::NIDX) + 64 * k,
+                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 // Finish the part [ca, cb) of tile t computed by wave g: reduce across lanes, then store y
-// (whole tile), hand the part over through slots (ca > 0), or, as the part holding chunk 0 of a
-// split tile (only possible when MAY_WAIT), add the other parts in chunk order and store y. The waits are bounded by a
+// (whole tile), hand the part over (ca > 0; only the first part of a range can be one), or, as
+// the part holding chunk 0 of a split tile (only possible when MAY_WAIT; np parts in all), add the
+// other parts in chunk order and store y. The waits are bounded by a
 // deadline on the constant 100 MHz real-time counter (about 50 ms, thousands of times a whole
 // launch); a wait that runs out (not expected) stores NaN rather than hanging.
 template <int M, int RPL, bool MAY_WAIT>
 __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[M][RPL], int t, int ca, int cb, int g,
-                                          int lane, int h) {
+                                          int lane, int h, const SlotPre<M>& pre, bool have_pre,
+                                          uint64_t* wg_slots, int np) {
+  int gr;
   constexpr int H = 16 / RPL;
   constexpr int NVAL = M * RPL, N4 = NVAL / 4;
   float vals[NVAL];
@@ -352,24 +450,30 @@ __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[M][RPL], 
     idx[i] = (f / RPL) * 16 + h * RPL + f % RPL;
   }
   if (ca > 0) {
+    gr = wave_of_step(a, t * a.nc);            // the wave holding chunk 0 of this tile
     if (!writer) return;
-    const int part = g - wave_of_step(a, (int64_t)t * a.nc);
-    uint64_t* slot = a.ws_slot + ((int64_t)t * a.pmax + part) * (M * 16);
+    if (gr / VALU_WPB == g / VALU_WPB) {
+      // same workgroup: this wave's LDS slot (a wave hands over at most one part per launch)
+      uint64_t* slot = wg_slots + (g % VALU_WPB) * (M * 16);
 #pragma unroll
-    for (int i = 0; i < N4; ++i) slot_store(slot + idx[i], vals[i]);
+      for (int i = 0; i < N4; ++i)
+        __hip_atomic_store(slot + idx[i], (uint64_t)__builtin_bit_cast(uint32_t, vals[i]) | (1ull << 32),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    } else {
+      uint64_t* slot = a.ws_slot + ((int64_t)t * a.pmax + (g - gr)) * (M * 16);
+#pragma unroll
+      for (int i = 0; i < N4; ++i) slot_store(slot + idx[i], vals[i]);
+    }
     return;
   }
   bool ok = true;
   if (MAY_WAIT && cb < a.nc) {
-    // All 64 lanes fetch the other parts at once: lane l reads slot index l % NIDX of parts
-    // 1 + l / NIDX + PPI * j. Each lane adds its parts in increasing j, the lanes holding one slot
-    // index are then added by a fixed exchange tree, and the writer lanes add the result to their
-    // own part: a fixed order, independent of timing.
-    constexpr int NIDX = M * 16;
-    constexpr int PPI = NIDX >= 64 ? 1 : 64 / NIDX;   // parts per load instruction
-    constexpr int IPP = NIDX <= 64 ? 1 : NIDX / 64;   // load instructions per part
-    constexpr int JB = 8 / IPP;                       // parts per lane loaded together
-    const int np = wave_of_step(a, (int64_t)t * a.nc + a.nc - 1) - g + 1;
+    // All 64 lanes fetch the other parts (the first batch normally prefetched, see SlotPre). Each
+    // lane adds its parts in increasing j, the lanes holding one slot index are then added by a
+    // fixed exchange tree, and the writer lanes add the result to their own part: a fixed order,
+    // independent of timing.
+    using S = SlotPre<M>;
+    constexpr int NIDX = S::NIDX, PPI = S::PPI, IPP = S::IPP, JB = S::JB;
     uint64_t* slots = a.ws_slot + (int64_t)t * a.pmax * NIDX;
     const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + 5000000ull;
     float ps[IPP];
@@ -377,29 +481,34 @@ __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[M][RPL], 
     for (int k = 0; k < IPP; ++k) ps[k] = 0.0f;
     const int loff = (NIDX >= 64) ? 0 : lane / NIDX;
     for (int j0 = 0; 1 + loff + PPI * j0 < np; j0 += JB) {
-      uint64_t w[JB][IPP];
-#pragma unroll
-      for (int j = 0; j < JB; ++j) {
-        const int p = min(1 + loff + PPI * (j0 + j), np - 1);
-#pragma unroll
-        for (int k = 0; k < IPP; ++k)
-          w[j][k] = __hip_atomic_load(slots + (int64_t)p * NIDX + (lane % NIDX) + 64 * k, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
-      }
+      S P = pre;
+      if (j0 > 0 || !have_pre) fetch_parts<M>(P, a, t, np, j0, g, lane);
 #pragma unroll
       for (int j = 0; j < JB; ++j) {
         const int p = 1 + loff + PPI * (j0 + j);
         if (p < np) {
+          const bool same_wg = (g + p) / VALU_WPB == g / VALU_WPB;
 #pragma unroll
           for (int k = 0; k < IPP; ++k) {
-            uint64_t* q = slots + (int64_t)p * NIDX + (lane % NIDX) + 64 * k;
-            while ((w[j][k] >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline) {
-              __builtin_amdgcn_s_sleep(2);
-              w[j][k] = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const int si = (lane % NIDX) + 64 * k;
+            uint64_t w = P.w[j][k];
+            if (same_wg) {
+              uint64_t* q = wg_slots + ((g + p) % VALU_WPB) * NIDX + si;
+              w = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+              while ((w >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline) {
+                __builtin_amdgcn_s_sleep(1);
+                w = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+              }
+            } else {
+              uint64_t* q = slots + (int64_t)p * NIDX + si;
+              while ((w >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline) {
+                __builtin_amdgcn_s_sleep(2);
+                w = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              }
+              __hip_atomic_store(q, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
-            ok = ok && (w[j][k] >> 32) != 0;
-            ps[k] += __builtin_bit_cast(float, (uint32_t)w[j][k]);
-            __hip_atomic_store(q, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            ok = ok && (w >> 32) != 0;
+            ps[k] += __builtin_bit_cast(float, (uint32_t)w);
           }
         }
       }
@@ -433,10 +542,11 @@ __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[M][RPL], 
 // Lookup tables staged in two halves around the first record's loads: the table words are
 // fetched first, the record loads are issued behind them, and the LDS stores wait only for the
 // table words, so the first record's memory round trip overlaps the staging.
+
 template <int KIND, int D>
 struct TableWords {
   static constexpr int N16 = (int)((Tables<KIND, D>::bytes - (KIND == SPH_KIND_CB13 ? 128u : 0u)) / 16u);
-  static constexpr int PER = (N16 + 1023) / 1024;
+  static constexpr int PER = (N16 + VALU_THREADS - 1) / VALU_THREADS;
   uint4 w[PER];
 };
 
@@ -445,7 +555,7 @@ __device__ __forceinline__ void fetch_tables(TableWords<KIND, D>& tw, const KArg
   constexpr int N16 = TableWords<KIND, D>::N16;
 #pragma unroll
   for (int i = 0; i < TableWords<KIND, D>::PER; ++i) {
-    const int j = (int)threadIdx.x + 1024 * i;
+    const int j = (int)threadIdx.x + VALU_THREADS * i;
     tw.w[i] = a.T[j < N16 ? j : N16 - 1];
   }
 }
@@ -455,7 +565,7 @@ __device__ __forceinline__ void store_tables(unsigned char* lds, const TableWord
   constexpr int N16 = TableWords<KIND, D>::N16;
 #pragma unroll
   for (int i = 0; i < TableWords<KIND, D>::PER; ++i) {
-    const int j = (int)threadIdx.x + 1024 * i;
+    const int j = (int)threadIdx.x + VALU_THREADS * i;
     if (j < N16) ((uint4*)lds)[j] = tw.w[i];
   }
   if constexpr (KIND == SPH_KIND_CB13) {
@@ -470,23 +580,38 @@ __device__ __forceinline__ void store_tables(unsigned char* lds, const TableWord
   }
 }
 
-// Two record buffers in ping-pong: the loads of step i+1 are in flight while step i is computed;
-// past the end of the range the loads re-read the record loaded just before (still in cache,
-// so it costs no HBM traffic) so that they stay unconditional. Finishing a tile part never waits on memory except in the part holding chunk 0
-// of a split tile, which is the last thing its wave does.
+// The kernel: tables and the first record are fetched together, then each wave walks its range
+// of steps through a ring of record buffers (see below). Finishing a tile part never waits on
+// memory except in the part holding chunk 0 of a split tile, which is the last thing its wave
+// does.
 template <int KIND, int D, int M, int RPL>
-__global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
+__global__ void __launch_bounds__(VALU_THREADS)
+__attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(KArgs a) {
   __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes];
-  __shared__ __align__(16) uint32_t pstage_all[16 * 64];
+  __shared__ __align__(16) uint32_t pstage_all[VALU_WPB * 64];
+  __shared__ uint64_t wg_slots[VALU_WPB * M * 16];   // split-tile parts handed over inside the workgroup
   constexpr int H = 16 / RPL;
   const int lane = threadIdx.x & 63;
   // wave-uniform by construction; readfirstlane keeps the schedule in SGPRs
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = (int)blockIdx.x * a.wpb + wave;
-  const bool active = g < a.gwa;
   // The range bounds are wave-uniform; readfirstlane keeps them (and every branch on them) scalar.
-  const int s_begin = __builtin_amdgcn_readfirstlane(active ? (int)((int64_t)g * a.ts / a.gwa) : 0);
-  const int s_end = __builtin_amdgcn_readfirstlane(active ? (int)((int64_t)(g + 1) * a.ts / a.gwa) : 1);
+  bool active;
+  int s_begin, s_end;
+  if (a.wg_tiles > 0) {
+    int wg_s0, wg_s1;
+    wg_range(a, blockIdx.x, wg_s0, wg_s1);
+    const int wg_n = wg_s1 - wg_s0, wg_nw = min(VALU_WPB, wg_n);
+    active = wave < wg_nw;
+    s_begin = active ? wg_s0 + piece_start(wg_n, wg_nw, wave) : 0;
+    s_end = active ? wg_s0 + piece_start(wg_n, wg_nw, wave + 1) : 1;
+  } else {
+    active = true;                           // every wave has at least one step
+    s_begin = spread_start(a, g);
+    s_end = spread_start(a, g + 1);
+  }
+  s_begin = __builtin_amdgcn_readfirstlane(s_begin);
+  s_end = __builtin_amdgcn_readfirstlane(s_end);
   const int t0 = __builtin_amdgcn_readfirstlane(s_begin / a.nc);
   const int c0 = s_begin - t0 * a.nc;
   const int h = lane % H, vloc = lane / H;
@@ -496,6 +621,7 @@ __global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
   fetch_tables<KIND, D>(tw, a);
   load_rec<KIND, M, RPL>(r0, a, t0, c0, h, vloc, lane);
   store_tables<KIND, D>(lds, tw, a);
+  for (int i = threadIdx.x; i < VALU_WPB * M * 16; i += VALU_THREADS) wg_slots[i] = 0;
   const uint32_t mask_off = a.t_bytes;
   __syncthreads();
   if (!active) return;                       // no barrier follows
@@ -505,17 +631,19 @@ __global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
 #pragma unroll
   for (int b = 0; b < M; ++b)
 #pragma unroll
-    for (int r = 0; r < RPL; ++r) acc[b][r] = 0.0f;
+    for (int rr = 0; rr < RPL; ++rr) acc[b][rr] = 0.0f;
 
-  // Steps go in pairs, one per buffer, so that the loop has a single exit at the bottom (an
-  // early exit would give the compiler a path back to the loop head with loads still pending,
-  // and it would wait for them). Tile parts that end inside the range are whole tiles or later
-  // parts of split tiles, which only store; the range's last part, which may be the waiting
-  // part holding chunk 0, is finished after the loop.
+  // Two record buffers in ping-pong: the loads of step i+1 are in flight while step i is
+  // computed. The loop runs over pairs of steps, one per buffer, with a single exit at the
+  // bottom (an early exit would give the compiler a path back to the loop head with loads still
+  // pending, and it would wait for them). The range's last step is peeled off: the tile parts
+  // that end inside the loop are whole tiles or later parts of split tiles, which only store,
+  // and the last part, which may be the part holding chunk 0 of a split tile, is finished after
+  // it, with the slots of the other parts fetched before the last step is computed.
   const int nsteps = s_end - s_begin;
-  const int npairs = nsteps >> 1;
+  const int npairs = (nsteps - 1) >> 1;
+  SlotPre<M> pre;                            // filled only before the last step (see below)
   int t = t0, c = c0;                        // position of step 2i
-  int tl = t0, cl = c0;                      // position of the last step computed
   for (int i = 0; i < npairs; ++i) {
     int t1 = t, c1 = c + 1;
     if (c1 == a.nc) {
@@ -524,27 +652,38 @@ __global__ void __launch_bounds__(1024) k_gemm_valu(KArgs a) {
     }
     load_rec<KIND, M, RPL>(r1, a, t1, c1, h, vloc, lane);
     compute_rec<KIND, D, M, RPL>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c1 == 0) emit_part<M, RPL, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h);
+    if (c1 == 0) emit_part<M, RPL, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
     int t2 = t1, c2 = c1 + 1;
     if (c2 == a.nc) {
       ++t2;
       c2 = 0;
     }
-    const bool has2 = 2 * i + 2 < nsteps;
-    load_rec<KIND, M, RPL>(r0, a, has2 ? t2 : t1, has2 ? c2 : c1, h, vloc, lane);
+    load_rec<KIND, M, RPL>(r0, a, t2, c2, h, vloc, lane);   // step 2i + 2 <= nsteps - 1 exists
     compute_rec<KIND, D, M, RPL>(r1, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (has2 && c2 == 0) emit_part<M, RPL, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, h);
-    tl = t1;
-    cl = c1;
+    if (c2 == 0) emit_part<M, RPL, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
     t = t2;
     c = c2;
   }
-  if (nsteps & 1) {
+  // r0 holds step 2 * npairs; one or two steps remain, the last one being the range's last.
+  int tf = t, cf = c;                        // position of the last step
+  if (nsteps - 2 * npairs == 2) {
+    cf = c + 1;
+    if (cf == a.nc) {
+      ++tf;
+      cf = 0;
+    }
+    load_rec<KIND, M, RPL>(r1, a, tf, cf, h, vloc, lane);
     compute_rec<KIND, D, M, RPL>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    tl = t;
-    cl = c;
+    if (cf == 0) emit_part<M, RPL, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
   }
-  emit_part<M, RPL, true>(a, acc, tl, tl == t0 ? c0 : 0, cl + 1, g, lane, h);
+  const int caf = tf == t0 ? c0 : 0;
+  const bool waits = caf == 0 && cf + 1 < a.nc;
+  const int np_final = waits ? wave_of_step(a, tf * a.nc + a.nc - 1) - g + 1 : 0;
+  if (waits) fetch_parts<M>(pre, a, tf, np_final, 0, g, lane);
+  // one instance of the step code for the last step, whichever buffer holds it
+  const Rec<KIND, M, RPL>& rf = (nsteps - 2 * npairs == 2) ? r1 : r0;
+  compute_rec<KIND, D, M, RPL>(rf, acc, lds, mask_off, pstage, lane, h, vloc);
+  emit_part<M, RPL, true>(a, acc, tf, caf, cf + 1, g, lane, h, pre, waits, wg_slots, np_final);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -676,7 +815,7 @@ struct Launch {
   int block;          // threads per workgroup
   int grid;
   int wpt;            // matrix-core kernel: waves per tile
-  int nc, gwa, pmax, ts;
+  int nc, wg_tiles, wq, wr, pmax, ts;
   size_t ws_bytes;    // workspace the launch needs
 };
 
@@ -767,20 +906,39 @@ Launch plan(const sph_weights* w, int m) {
     const int M = m <= 1 ? 1 : m <= 2 ? 2 : m <= 4 ? 4 : 8;
     const int H = M <= 2 ? 1 : M == 4 ? 2 : 4;
     const int vpc = 64 / H;
-    const int wpb = 16;                         // one 16-wave workgroup per CU
+    const int wpb = VALU_WPB;
     const int64_t nc = (nv + vpc - 1) / vpc;
     const int64_t ts = nt * nc;
-    const int64_t gw = (int64_t)cus * wpb;
-    const int64_t gwa = ts < gw ? ts : gw;
+    const int64_t slots = (int64_t)cus * VALU_WG_PER_CU;
+    // whole tiles per workgroup (no tile split across workgroups, parts meet in LDS) ...
+    const int64_t T = (nt + slots - 1) / slots;
+    const int64_t gA = (nt + T - 1) / T;
+    const int64_t lA = (T * nc + wpb - 1) / wpb;
+    // ... or balanced ranges spread over all waves of the grid (tiles split across workgroups
+    // meet in global slots); at most ts / wpb workgroups, so that every wave gets a step
+    const int64_t gB = std::max<int64_t>(1, std::min<int64_t>(slots, ts / wpb));
+    const int64_t lB = (ts + gB * wpb - 1) / (gB * wpb);
+    const bool aligned = lA <= lB;
     L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, false, M);
     L.block = 64 * wpb;
-    L.grid = (int)((gwa + wpb - 1) / wpb);
     L.nc = (int)nc;
     L.ts = (int)ts;
-    L.gwa = (int)gwa;
-    // a range holds at least ts/gwa steps, so a tile meets at most nc/(ts/gwa) + 2 ranges
-    L.pmax = (int)(nc / (ts / gwa) + 2);
-    L.ws_bytes = (nt % gwa != 0) ? (size_t)nt * L.pmax * M * 16 * 8 : 0;
+    if (aligned) {
+      L.grid = (int)gA;
+      L.wg_tiles = (int)T;
+      L.pmax = 0;
+      L.ws_bytes = 0;
+    } else {
+      L.grid = (int)gB;
+      L.wg_tiles = 0;
+      L.wq = (int)(ts / (gB * wpb));
+      L.wr = (int)(ts % (gB * wpb));
+      // a wave range holds at least floor(ts / (gB * wpb)) >= 1 steps, so a tile meets at most
+      // nc / that + 2 ranges
+      const int64_t lmin = std::max<int64_t>(1, ts / (gB * wpb));
+      L.pmax = (int)(nc / lmin + 2);
+      L.ws_bytes = (size_t)nt * L.pmax * M * 16 * 8;
+    }
   } else {
     const int NB = m <= 16 ? 1 : 2;
     const int64_t per_wave = 4 * 8;             // 8 MFMA steps per wave
@@ -905,7 +1063,10 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
   KArgs a = make_args(w);
   a.nc = L.nc;
   a.wpb = L.block / 64;
-  a.gwa = L.gwa;
+  a.nwg = L.grid;
+  a.wg_tiles = L.wg_tiles;
+  a.wq = L.wq;
+  a.wr = L.wr;
   a.pmax = L.pmax;
   a.ts = L.ts;
   if (L.ws_bytes > 0) a.ws_slot = (uint64_t*)d_ws;

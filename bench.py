@@ -39,9 +39,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source the counters were taken with: any change to the kernels makes
 # the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "52292062d28dec49ea6b1387ed92a7d4dfae49209c12e217437b279045db9ef2": {
-        "7168x5120-m1": 14986716, "5120x5120-m1": 10989776,
-        "51200x5120-m1": 85416048, "5120x25600-m1": 45083731},
+    "cd94ca3712c51d9a33f144b6e34f838f13f1473c6677129e56559251149b6147": {
+        "7168x5120-m1": 11945869, "5120x5120-m1": 9358232,
+        "51200x5120-m1": 82773938, "5120x25600-m1": 42907589},
 }
 
 

@@ -26,6 +26,7 @@
 
 typedef _Float16 f16;
 typedef f16 f16x2 __attribute__((ext_vector_type(2)));
+typedef f16 f16x4 __attribute__((ext_vector_type(4)));
 typedef f16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -194,15 +195,19 @@ struct Tables {
   static constexpr uint32_t bytes = (KIND == SPH_KIND_CB13) ? ((16u << D) + 128u) : (256u << D);
 };
 
-template <int KIND, int M, int RPL>
+// MX selects the matrix-core variant (batch 2..16): the lane's rows are rebuilt as in the vector
+// variant, scaled to fp16 and multiplied by 4x4x4 MFMA blocks, one block per vector position.
+template <int KIND, int M, int RPL, bool MX = false>
 struct Rec {
   static constexpr int ADW = (KIND == SPH_KIND_CB13) ? RPL / 4 : RPL / 2;
   static constexpr int BDW = (KIND == SPH_KIND_NIB16Q8) ? RPL / 4 : (KIND == SPH_KIND_CB13) ? RPL / 2 : 1;
+  static constexpr int NX = MX ? M / 4 : M;
   uint32_t ra[ADW];
   uint32_t rb[BDW];
-  uint32_t pw;        // one group-parameter word of the chunk, staged through LDS at compute time
-  uint32_t xv[M][4];  // the activation vector(s) of this lane's position
-  bool pok;           // pw belongs to a group inside the row; else the group's radii are taken as 0
+  uint32_t pw;         // one group-parameter word of the chunk, staged through LDS at compute time
+  uint32_t xv[NX][4];  // vector variant: x[b] at this lane's position for every batch row b;
+                       // MX: x[4g + lane % 4] at this lane's position for each group g of 4 rows
+  bool pok;            // pw belongs to a group inside the row; else the group's radii are taken as 0
 };
 
 // Loads of one step. Branch-free, and no loaded value is ever selected or copied before use, so
@@ -210,13 +215,13 @@ struct Rec {
 // past the end of the row (whole groups, since k is a multiple of 128) read a valid record and
 // contribute nothing because their group parameters are taken as zero. The chunk's group
 // parameters (VPC/16 groups x 16 rows = VPC words, contiguous) are spread one word per lane.
-template <int KIND, int M, int RPL>
-__device__ __forceinline__ void load_rec(Rec<KIND, M, RPL>& R, const KArgs& a, int t, int c, int h, int vloc,
+template <int KIND, int M, int RPL, bool MX = false>
+__device__ __forceinline__ void load_rec(Rec<KIND, M, RPL, MX>& R, const KArgs& a, int t, int c, int h, int vloc,
                                          int lane) {
   constexpr int H = 16 / RPL, VPC = 64 / H;
   constexpr int ADW_REC = (KIND == SPH_KIND_CB13) ? 4 : 8;
   constexpr int BDW_REC = (KIND == SPH_KIND_W2) ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
-  constexpr int ADW = Rec<KIND, M, RPL>::ADW, BDW = Rec<KIND, M, RPL>::BDW;
+  constexpr int ADW = Rec<KIND, M, RPL, MX>::ADW, BDW = Rec<KIND, M, RPL, MX>::BDW;
   const int v = min(c * VPC + vloc, a.nv - 1);
   const int64_t rec = (int64_t)t * a.nv + v;
   load_dw<ADW>(R.ra, a.A + rec * ADW_REC + h * ADW);
@@ -227,16 +232,25 @@ __device__ __forceinline__ void load_rec(Rec<KIND, M, RPL>& R, const KArgs& a, i
   const int pg = min(pg0, a.ng - 1);
   R.pw = a.P[((int64_t)t * a.ng + pg) * 16 + (lane & 15)];
   R.pok = pg0 < a.ng;
+  if constexpr (MX) {
+    // batch rows past m feed MFMA columns that are never stored; they read row m - 1
 #pragma unroll
-  for (int b = 0; b < M; ++b) {
-    const int bb = (M == 1 || b < a.m) ? b : 0;
-    load_dw<4>(R.xv[b], (const uint32_t*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v));
+    for (int g = 0; g < Rec<KIND, M, RPL, MX>::NX; ++g) {
+      const int bb = min(4 * g + (lane & 3), a.m - 1);
+      load_dw<4>(R.xv[g], (const uint32_t*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v));
+    }
+  } else {
+#pragma unroll
+    for (int b = 0; b < M; ++b) {
+      const int bb = (M == 1 || b < a.m) ? b : 0;
+      load_dw<4>(R.xv[b], (const uint32_t*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v));
+    }
   }
 }
 
 // Table lookups of the rows [r0, r0 + RB) of a record: field extraction and the LDS reads.
-template <int KIND, int D, int M, int RPL, int RB>
-__device__ __forceinline__ void lookup_rows(const Rec<KIND, M, RPL>& R, int r0, uint32_t qodd, const unsigned char* lds,
+template <int KIND, int D, int M, int RPL, int RB, bool MX = false>
+__device__ __forceinline__ void lookup_rows(const Rec<KIND, M, RPL, MX>& R, int r0, uint32_t qodd, const unsigned char* lds,
                                             uint32_t mask_off, uint4 (&tt)[RB], float (&qf)[RB]) {
 #pragma unroll
   for (int i = 0; i < RB; ++i) {
@@ -261,8 +275,8 @@ __device__ __forceinline__ void lookup_rows(const Rec<KIND, M, RPL>& R, int r0, 
 // before the arithmetic of batch j, and scheduling barriers keep the compiler from interleaving
 // them back (left alone, it keeps only a few LDS reads in flight per wave, far fewer than the
 // LDS latency under bank conflicts needs).
-template <int KIND, int D, int M, int RPL>
-__device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL>& R, float (&acc)[M][RPL],
+template <int KIND, int D, int M, int RPL, bool MX = false>
+__device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL, MX>& R, float (&acc)[M][RPL],
                                             const unsigned char* lds, uint32_t mask_off, uint32_t* pstage,
                                             int lane, int h, int vloc) {
   constexpr int RB = RPL < VALU_RB ? RPL : VALU_RB;
@@ -283,17 +297,41 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL>& R, float (&
   if constexpr (KIND == SPH_KIND_W2) qodd = R.rb[0] >> (4 * (h * RPL / 2));
   uint4 tt[2][RB];
   float qf[2][RB];
-  lookup_rows<KIND, D, M, RPL, RB>(R, 0, qodd, lds, mask_off, tt[0], qf[0]);
+  lookup_rows<KIND, D, M, RPL, RB, MX>(R, 0, qodd, lds, mask_off, tt[0], qf[0]);
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
-    if (j + 1 < NB) lookup_rows<KIND, D, M, RPL, RB>(R, (j + 1) * RB, qodd, lds, mask_off, tt[(j + 1) & 1], qf[(j + 1) & 1]);
+    if (j + 1 < NB) lookup_rows<KIND, D, M, RPL, RB, MX>(R, (j + 1) * RB, qodd, lds, mask_off, tt[(j + 1) & 1], qf[(j + 1) & 1]);
     if constexpr (VALU_PIPE_BARRIERS) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < RB; ++i) {
       const int r = j * RB + i;
       const float rh = fmaf(qf[j & 1][i], f16hi(pp[r]), f16lo(pp[r]));
+      if constexpr (MX) {
+        // w = fp16(fp16(r) * t): rounded once to fp16 for the radius, once for each product.
+        // Block v of the MFMA is this lane's vector position; its row lane % 4 is the lane's row
+        // 4 * (lane % 4) + r, and its column lane % 4 is batch row 4g + lane % 4, so lane
+        // (v, j) accumulates rows 4e + r (e = 0..3, in acc[4g + r][e]) of batch row 4g + j.
+        const f16 rs = (f16)rh;
+        const f16x2 r2 = {rs, rs};
+        const uint4 tv = tt[j & 1][i];
+        const uint2 wlo = make_uint2(__builtin_bit_cast(uint32_t, as_h2(tv.x) * r2),
+                                     __builtin_bit_cast(uint32_t, as_h2(tv.y) * r2));
+        const uint2 whi = make_uint2(__builtin_bit_cast(uint32_t, as_h2(tv.z) * r2),
+                                     __builtin_bit_cast(uint32_t, as_h2(tv.w) * r2));
 #pragma unroll
-      for (int b = 0; b < M; ++b) acc[b][r] = fmaf(rh, dot8(tt[j & 1][i], R.xv[b]), acc[b][r]);
+        for (int g = 0; g < M / 4; ++g) {
+          f32x4 d = {acc[4 * g + r][0], acc[4 * g + r][1], acc[4 * g + r][2], acc[4 * g + r][3]};
+          d = __builtin_amdgcn_mfma_f32_4x4x4f16(__builtin_bit_cast(f16x4, wlo),
+                                                  __builtin_bit_cast(f16x4, make_uint2(R.xv[g][0], R.xv[g][1])), d, 0, 0, 0);
+          d = __builtin_amdgcn_mfma_f32_4x4x4f16(__builtin_bit_cast(f16x4, whi),
+                                                  __builtin_bit_cast(f16x4, make_uint2(R.xv[g][2], R.xv[g][3])), d, 0, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[4 * g + r][e] = d[e];
+        }
+      } else {
+#pragma unroll
+        for (int b = 0; b < M; ++b) acc[b][r] = fmaf(rh, dot8(tt[j & 1][i], R.xv[b]), acc[b][r]);
+      }
     }
     if constexpr (VALU_PIPE_BARRIERS) __builtin_amdgcn_sched_barrier(0);
   }
@@ -425,7 +463,7 @@ __device__ __forceinline__ void fetch_parts(SlotPre<M>& P, const KArgs& a, int t
 // other parts in chunk order and store y. The waits are bounded by a
 // deadline on the constant 100 MHz real-time counter (about 50 ms, thousands of times a whole
 // launch); a wait that runs out (not expected) stores NaN rather than hanging.
-template <int M, int RPL, bool MAY_WAIT>
+template <int M, int RPL, bool MAY_WAIT, bool MX = false>
 __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[M][RPL], int t, int ca, int cb, int g,
                                           int lane, int h, const SlotPre<M>& pre, bool have_pre,
                                           uint64_t* wg_slots, int np) {
@@ -447,7 +485,9 @@ __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[M][RPL], 
 #pragma unroll
   for (int i = 0; i < N4; ++i) {
     const int f = base + i;
-    idx[i] = (f / RPL) * 16 + h * RPL + f % RPL;
+    // vector variant: value b * RPL + r is batch row b, tile row h * RPL + r; MX: value
+    // 16g + 4r + e is batch row 4g + h, tile row 4e + r (see compute_rec)
+    idx[i] = MX ? ((f / 16) * 4 + h) * 16 + 4 * (f % 4) + (f / 4) % 4 : (f / RPL) * 16 + h * RPL + f % RPL;
   }
   if (ca > 0) {
     gr = wave_of_step(a, t * a.nc);            // the wave holding chunk 0 of this tile
@@ -584,7 +624,7 @@ __device__ __forceinline__ void store_tables(unsigned char* lds, const TableWord
 // of steps through a ring of record buffers (see below). Finishing a tile part never waits on
 // memory except in the part holding chunk 0 of a split tile, which is the last thing its wave
 // does.
-template <int KIND, int D, int M, int RPL>
+template <int KIND, int D, int M, int RPL, bool MX = false>
 __global__ void __launch_bounds__(VALU_THREADS)
 __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(KArgs a) {
   __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes];
@@ -616,10 +656,10 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   const int c0 = s_begin - t0 * a.nc;
   const int h = lane % H, vloc = lane / H;
 
-  Rec<KIND, M, RPL> r0, r1;
+  Rec<KIND, M, RPL, MX> r0, r1;
   TableWords<KIND, D> tw;
   fetch_tables<KIND, D>(tw, a);
-  load_rec<KIND, M, RPL>(r0, a, t0, c0, h, vloc, lane);
+  load_rec<KIND, M, RPL, MX>(r0, a, t0, c0, h, vloc, lane);
   store_tables<KIND, D>(lds, tw, a);
   for (int i = threadIdx.x; i < VALU_WPB * M * 16; i += VALU_THREADS) wg_slots[i] = 0;
   const uint32_t mask_off = a.t_bytes;
@@ -650,17 +690,17 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
       ++t1;
       c1 = 0;
     }
-    load_rec<KIND, M, RPL>(r1, a, t1, c1, h, vloc, lane);
-    compute_rec<KIND, D, M, RPL>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c1 == 0) emit_part<M, RPL, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
+    load_rec<KIND, M, RPL, MX>(r1, a, t1, c1, h, vloc, lane);
+    compute_rec<KIND, D, M, RPL, MX>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
+    if (c1 == 0) emit_part<M, RPL, false, MX>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
     int t2 = t1, c2 = c1 + 1;
     if (c2 == a.nc) {
       ++t2;
       c2 = 0;
     }
-    load_rec<KIND, M, RPL>(r0, a, t2, c2, h, vloc, lane);   // step 2i + 2 <= nsteps - 1 exists
-    compute_rec<KIND, D, M, RPL>(r1, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c2 == 0) emit_part<M, RPL, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
+    load_rec<KIND, M, RPL, MX>(r0, a, t2, c2, h, vloc, lane);   // step 2i + 2 <= nsteps - 1 exists
+    compute_rec<KIND, D, M, RPL, MX>(r1, acc, lds, mask_off, pstage, lane, h, vloc);
+    if (c2 == 0) emit_part<M, RPL, false, MX>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
     t = t2;
     c = c2;
   }
@@ -672,18 +712,18 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
       ++tf;
       cf = 0;
     }
-    load_rec<KIND, M, RPL>(r1, a, tf, cf, h, vloc, lane);
-    compute_rec<KIND, D, M, RPL>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (cf == 0) emit_part<M, RPL, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
+    load_rec<KIND, M, RPL, MX>(r1, a, tf, cf, h, vloc, lane);
+    compute_rec<KIND, D, M, RPL, MX>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
+    if (cf == 0) emit_part<M, RPL, false, MX>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
   }
   const int caf = tf == t0 ? c0 : 0;
   const bool waits = caf == 0 && cf + 1 < a.nc;
   const int np_final = waits ? wave_of_step(a, tf * a.nc + a.nc - 1) - g + 1 : 0;
   if (waits) fetch_parts<M>(pre, a, tf, np_final, 0, g, lane);
   // one instance of the step code for the last step, whichever buffer holds it
-  const Rec<KIND, M, RPL>& rf = (nsteps - 2 * npairs == 2) ? r1 : r0;
-  compute_rec<KIND, D, M, RPL>(rf, acc, lds, mask_off, pstage, lane, h, vloc);
-  emit_part<M, RPL, true>(a, acc, tf, caf, cf + 1, g, lane, h, pre, waits, wg_slots, np_final);
+  const Rec<KIND, M, RPL, MX>& rf = (nsteps - 2 * npairs == 2) ? r1 : r0;
+  compute_rec<KIND, D, M, RPL, MX>(rf, acc, lds, mask_off, pstage, lane, h, vloc);
+  emit_part<M, RPL, true, MX>(a, acc, tf, caf, cf + 1, g, lane, h, pre, waits, wg_slots, np_final);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -839,9 +879,8 @@ template <int KIND, int D>
 const void* valu_fn(int M) {
   switch (M) {
     case 1: return (const void*)k_gemm_valu<KIND, D, 1, 16>;
-    case 2: return (const void*)k_gemm_valu<KIND, D, 2, 16>;
-    case 4: return (const void*)k_gemm_valu<KIND, D, 4, 8>;
-    default: return (const void*)k_gemm_valu<KIND, D, 8, 4>;
+    case 4: return (const void*)k_gemm_valu<KIND, D, 4, 4, true>;
+    default: return (const void*)k_gemm_valu<KIND, D, 8, 4, true>;
   }
 }
 
@@ -895,6 +934,7 @@ int num_cus() {
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
+
 // Work plan. Vector-ALU path: one 16-wave workgroup per CU, every wave a contiguous range of
 // steps (at least one). Matrix-core path: a workgroup per tile, its waves splitting K.
 Launch plan(const sph_weights* w, int m) {
@@ -902,9 +942,11 @@ Launch plan(const sph_weights* w, int m) {
   const int64_t nv = w->k / 8, nt = (w->n + 15) / 16;
   const int kind = sph_kind_of(w->fmt.dir_bits, w->fmt.radius_bits);
   const int cus = num_cus();
+  // batch 1: vector ALU; 2..8: 4x4x4 MFMA blocks on the same records (4 lanes per vector
+  // position, rebuilt weights rounded to fp16); 9..32: the tile-per-workgroup MFMA kernel
   if (m <= 8) {
-    const int M = m <= 1 ? 1 : m <= 2 ? 2 : m <= 4 ? 4 : 8;
-    const int H = M <= 2 ? 1 : M == 4 ? 2 : 4;
+    const int M = m <= 1 ? 1 : m <= 4 ? 4 : 8;
+    const int H = M == 1 ? 1 : 4;
     const int vpc = 64 / H;
     const int wpb = VALU_WPB;
     const int64_t nc = (nv + vpc - 1) / vpc;

@@ -18,6 +18,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <type_traits>
 #include <cstring>
 #include <vector>
 
@@ -111,6 +112,16 @@ __device__ __forceinline__ uint4 signed_dir_cb13(const unsigned char* lds, uint3
 __device__ __forceinline__ float f16lo(uint32_t u) { return (float)__builtin_bit_cast(f16, (uint16_t)(u & 0xFFFFu)); }
 __device__ __forceinline__ float f16hi(uint32_t u) { return (float)__builtin_bit_cast(f16, (uint16_t)(u >> 16)); }
 __device__ __forceinline__ f16x2 as_h2(uint32_t u) { return __builtin_bit_cast(f16x2, u); }
+
+// r * t for the 8 fp16 values of t, each rounded once to fp16 (v_fma_mix writes one half each).
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t scale_h2(uint32_t t, float r) {
+  const f32x2 p = {fmaf(f16lo(t), r, 0.0f), fmaf(f16hi(t), r, 0.0f)};   // products rounded to fp32
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(p, f16x2));
+}
+__device__ __forceinline__ uint4 scale_dir(uint4 t, float r) {
+  return make_uint4(scale_h2(t.x, r), scale_h2(t.y, r), scale_h2(t.z, r), scale_h2(t.w, r));
+}
 
 __device__ __forceinline__ float dot8(uint4 t, const uint32_t (&x)[4]) {
   float p = __builtin_amdgcn_fdot2(as_h2(t.x), as_h2(x[0]), 0.0f, false);
@@ -307,17 +318,12 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL, MX>& R, floa
       const int r = j * RB + i;
       const float rh = fmaf(qf[j & 1][i], f16hi(pp[r]), f16lo(pp[r]));
       if constexpr (MX) {
-        // w = fp16(fp16(r) * t): rounded once to fp16 for the radius, once for each product.
-        // Block v of the MFMA is this lane's vector position; its row lane % 4 is the lane's row
-        // 4 * (lane % 4) + r, and its column lane % 4 is batch row 4g + lane % 4, so lane
-        // (v, j) accumulates rows 4e + r (e = 0..3, in acc[4g + r][e]) of batch row 4g + j.
-        const f16 rs = (f16)rh;
-        const f16x2 r2 = {rs, rs};
-        const uint4 tv = tt[j & 1][i];
-        const uint2 wlo = make_uint2(__builtin_bit_cast(uint32_t, as_h2(tv.x) * r2),
-                                     __builtin_bit_cast(uint32_t, as_h2(tv.y) * r2));
-        const uint2 whi = make_uint2(__builtin_bit_cast(uint32_t, as_h2(tv.z) * r2),
-                                     __builtin_bit_cast(uint32_t, as_h2(tv.w) * r2));
+        // w = fp16(r * t), one rounding per weight. Block v of the MFMA is this lane's vector
+        // position; its row lane % 4 is the lane's row 4 * (lane % 4) + r, and its column
+        // lane % 4 is batch row 4g + lane % 4, so lane (v, j) accumulates rows 4e + r (e = 0..3,
+        // in acc[4g + r][e]) of batch row 4g + j.
+        const uint4 w = scale_dir(tt[j & 1][i], rh);
+        const uint2 wlo = make_uint2(w.x, w.y), whi = make_uint2(w.z, w.w);
 #pragma unroll
         for (int g = 0; g < M / 4; ++g) {
           f32x4 d = {acc[4 * g + r][0], acc[4 * g + r][1], acc[4 * g + r][2], acc[4 * g + r][3]};
@@ -336,6 +342,106 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL, MX>& R, floa
     if constexpr (VALU_PIPE_BARRIERS) __builtin_amdgcn_sched_barrier(0);
   }
 }
+
+// Tile variant (batch 9..32): lane (r, j) = (lane % 16, lane / 16) rebuilds row r of the vector
+// positions 4i + j (i = 0..3) of a 16-position chunk, which is exactly the A operand of
+// v_mfma_f32_16x16x32_f16 (16 rows x 4 positions); the B operand is x for batch rows
+// 16nb + lane % 16 at the same positions. The MFMA sums over the chunk, so each lane ends a step
+// with finished sums for (batch 16nb + lane % 16, rows 4 * (lane / 16) + e) and no lane reduction
+// is needed. One record dword (and one aux dword) per position and lane: 128 contiguous bytes
+// per load over the wave.
+template <int KIND, int NB>
+struct RecT {
+  uint32_t ra[4];
+  uint32_t rb[4];
+  uint32_t pw;            // (min, step) of this lane's row in the chunk's group
+  uint32_t xv[NB * 4][4]; // x[16nb + lane % 16] at position 4i + j, index nb * 4 + i
+  bool pok;
+};
+
+template <int KIND, int NB>
+__device__ __forceinline__ void load_rec_t(RecT<KIND, NB>& R, const KArgs& a, int t, int c, int lane) {
+  constexpr int ADW_REC = (KIND == SPH_KIND_CB13) ? 4 : 8;
+  constexpr int BDW_REC = (KIND == SPH_KIND_W2) ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
+  const int r = lane & 15, j = lane >> 4;
+  // the dword holding row r in each stream
+  const int adw = (KIND == SPH_KIND_CB13) ? r / 4 : r / 2;
+  const int bdw = (KIND == SPH_KIND_W2) ? 0 : (KIND == SPH_KIND_NIB16Q8) ? r / 4 : r / 2;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int v = min(c * 16 + 4 * i + j, a.nv - 1);
+    const int64_t rec = (int64_t)t * a.nv + v;
+    R.ra[i] = a.A[rec * ADW_REC + adw];
+    if constexpr (KIND != SPH_KIND_NIB16) R.rb[i] = a.B[rec * BDW_REC + bdw];
+    else R.rb[i] = 0;
+  }
+  // one 128-weight group per chunk: (min, step) of row r
+  const int pg = min(c, a.ng - 1);
+  R.pw = a.P[((int64_t)t * a.ng + pg) * 16 + r];
+  R.pok = c < a.ng;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int bb = min(16 * nb + r, a.m - 1);   // columns past the batch are never stored
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int v = min(c * 16 + 4 * i + j, a.nv - 1);
+      load_dw<4>(R.xv[nb * 4 + i], (const uint32_t*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v));
+    }
+  }
+}
+
+template <int KIND, int D, int NB>
+__device__ __forceinline__ void compute_rec_t(const RecT<KIND, NB>& R, float (&acc)[NB][4], const unsigned char* lds,
+                                              uint32_t mask_off, int lane) {
+  const int r = lane & 15;
+  const uint32_t pw = R.pok ? R.pw : 0u;
+  const float lo = f16lo(pw), st = f16hi(pw);
+  uint4 tt[4];
+  uint32_t q[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if constexpr (KIND == SPH_KIND_CB13) {
+      uint32_t sg, z;
+      decode_cb13(R.ra[i], r % 4, R.rb[i], r & 1, sg, z, q[i]);
+      tt[i] = signed_dir_cb13(lds, mask_off, sg, z);
+    } else {
+      uint32_t l, hh, qx = 0;
+      if constexpr (KIND == SPH_KIND_W2) qx = (R.rb[i] >> (4 * (r / 2))) & 15u;
+      if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (R.rb[i] >> (8 * (r % 4))) & 0xFFu;
+      decode_nib<KIND, D>(R.ra[i], r & 1, qx, l, hh, q[i]);
+      tt[i] = signed_dir_nib<KIND, D>(lds, l, hh);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint4 w = scale_dir(tt[i], fmaf((float)q[i], st, lo));   // fp16(r * t), one rounding
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const uint32_t* xq = R.xv[nb * 4 + i];
+      f32x4 d = {acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3]};
+      d = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, w),
+                                                 __builtin_bit_cast(f16x8, make_uint4(xq[0], xq[1], xq[2], xq[3])), d, 0, 0, 0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[nb][e] = d[e];
+    }
+  }
+}
+
+// Step dispatch over the three variants (MODE 0: vector ALU, 1: 4x4x4 blocks, 2: 16x16x32 tiles).
+template <int KIND, int D, int M, int RPL, int MODE>
+struct Step {
+  static constexpr int AR = MODE == 2 ? M / 16 : M;       // accumulator rows per lane
+  using R = typename std::conditional<MODE == 2, RecT<KIND, M / 16>, Rec<KIND, M, RPL, MODE == 1>>::type;
+  static __device__ __forceinline__ void load(R& rec, const KArgs& a, int t, int c, int h, int vloc, int lane) {
+    if constexpr (MODE == 2) load_rec_t<KIND, M / 16>(rec, a, t, c, lane);
+    else load_rec<KIND, M, RPL, MODE == 1>(rec, a, t, c, h, vloc, lane);
+  }
+  static __device__ __forceinline__ void compute(const R& rec, float (&acc)[AR][RPL], const unsigned char* lds,
+                                                 uint32_t mask_off, uint32_t* pstage, int lane, int h, int vloc) {
+    if constexpr (MODE == 2) compute_rec_t<KIND, D, M / 16>(rec, acc, lds, mask_off, lane);
+    else compute_rec<KIND, D, M, RPL, MODE == 1>(rec, acc, lds, mask_off, pstage, lane, h, vloc);
+  }
+};
 
 // Exchange-and-add across lanes l and l^DIST (DIST = 32 or 16): lanes with bit DIST clear end
 // with lo_keep[l] + lo_keep[l^DIST], the others with hi_keep[l] + hi_keep[l^DIST]. This is one
@@ -434,13 +540,13 @@ struct SlotPre {
   static constexpr int NIDX = M * 16;
   static constexpr int PPI = NIDX >= 64 ? 1 : 64 / NIDX;   // parts per load instruction
   static constexpr int IPP = NIDX <= 64 ? 1 : NIDX / 64;   // load instructions per part
-  static constexpr int JB = 4 / IPP;                       // parts per lane loaded together
+  static constexpr int JB = IPP >= 4 ? 1 : 4 / IPP;        // parts per lane loaded together
   uint64_t w[JB][IPP];
 };
 
 // Parts held by waves of the same workgroup are handed over through LDS instead (see emit_part);
 // only the parts of other workgroups are fetched here.
-template <int M>
+template <int M, bool LDS_HO = true>
 __device__ __forceinline__ void fetch_parts(SlotPre<M>& P, const KArgs& a, int t, int np, int j0, int g, int lane) {
   using S = SlotPre<M>;
   const uint64_t* slots = a.ws_slot + (int64_t)t * a.pmax * S::NIDX;
@@ -448,7 +554,7 @@ __device__ __forceinline__ void fetch_parts(SlotPre<M>& P, const KArgs& a, int t
 #pragma unroll
   for (int j = 0; j < S::JB; ++j) {
     const int p = min(1 + loff + S::PPI * (j0 + j), np - 1);
-    const bool same_wg = (g + p) / VALU_WPB == g / VALU_WPB;
+    const bool same_wg = LDS_HO && (g + p) / VALU_WPB == g / VALU_WPB;
 #pragma unroll
     for (int k = 0; k < S::IPP; ++k)
       P.w[j][k] = same_wg ? 0ull
@@ -463,36 +569,41 @@ __device__ __forceinline__ void fetch_parts(SlotPre<M>& P, const KArgs& a, int t
 // other parts in chunk order and store y. The waits are bounded by a
 // deadline on the constant 100 MHz real-time counter (about 50 ms, thousands of times a whole
 // launch); a wait that runs out (not expected) stores NaN rather than hanging.
-template <int M, int RPL, bool MAY_WAIT, bool MX = false>
-__device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[M][RPL], int t, int ca, int cb, int g,
-                                          int lane, int h, const SlotPre<M>& pre, bool have_pre,
+template <int M, int RPL, bool MAY_WAIT, int MODE = 0, bool LDS_HO = true>
+__device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[MODE == 2 ? M / 16 : M][RPL], int t, int ca,
+                                          int cb, int g, int lane, int h, const SlotPre<M>& pre, bool have_pre,
                                           uint64_t* wg_slots, int np) {
   int gr;
   constexpr int H = 16 / RPL;
-  constexpr int NVAL = M * RPL, N4 = NVAL / 4;
+  constexpr int AR = MODE == 2 ? M / 16 : M;
+  constexpr int NVAL = AR * RPL, N4 = MODE == 2 ? NVAL : NVAL / 4;
   float vals[NVAL];
 #pragma unroll
-  for (int b = 0; b < M; ++b)
+  for (int b = 0; b < AR; ++b)
 #pragma unroll
     for (int r = 0; r < RPL; ++r) {
       vals[b * RPL + r] = acc[b][r];
       acc[b][r] = 0.0f;
     }
-  wave_reduce<NVAL, H>(vals, lane);
-  const bool writer = (lane & 15) < H;       // one writer lane per h in each 16-lane row
-  const int base = ((lane >> 5) & 1) * (NVAL / 2) + ((lane >> 4) & 1) * N4;
+  if constexpr (MODE != 2) wave_reduce<NVAL, H>(vals, lane);
+  // one writer lane per h in each 16-lane row; the tile variant's sums are already per lane
+  const bool writer = MODE == 2 || (lane & 15) < H;
+  const int base = MODE == 2 ? 0 : ((lane >> 5) & 1) * (NVAL / 2) + ((lane >> 4) & 1) * N4;
   int idx[N4];                               // slot index b*16 + row of value i
 #pragma unroll
   for (int i = 0; i < N4; ++i) {
     const int f = base + i;
-    // vector variant: value b * RPL + r is batch row b, tile row h * RPL + r; MX: value
-    // 16g + 4r + e is batch row 4g + h, tile row 4e + r (see compute_rec)
-    idx[i] = MX ? ((f / 16) * 4 + h) * 16 + 4 * (f % 4) + (f / 4) % 4 : (f / RPL) * 16 + h * RPL + f % RPL;
+    // vector variant: value b * RPL + r is batch row b, tile row h * RPL + r; 4x4x4 blocks: value
+    // 16g + 4r + e is batch row 4g + h, tile row 4e + r (see compute_rec); tiles: value 4nb + e
+    // is batch row 16nb + lane % 16, tile row 4 * (lane / 16) + e (see compute_rec_t)
+    if constexpr (MODE == 2) idx[i] = (16 * (f / 4) + (lane & 15)) * 16 + 4 * (lane >> 4) + f % 4;
+    else if constexpr (MODE == 1) idx[i] = ((f / 16) * 4 + h) * 16 + 4 * (f % 4) + (f / 4) % 4;
+    else idx[i] = (f / RPL) * 16 + h * RPL + f % RPL;
   }
   if (ca > 0) {
     gr = wave_of_step(a, t * a.nc);            // the wave holding chunk 0 of this tile
     if (!writer) return;
-    if (gr / VALU_WPB == g / VALU_WPB) {
+    if (LDS_HO && gr / VALU_WPB == g / VALU_WPB) {
       // same workgroup: this wave's LDS slot (a wave hands over at most one part per launch)
       uint64_t* slot = wg_slots + (g % VALU_WPB) * (M * 16);
 #pragma unroll
@@ -522,12 +633,12 @@ __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[M][RPL], 
     const int loff = (NIDX >= 64) ? 0 : lane / NIDX;
     for (int j0 = 0; 1 + loff + PPI * j0 < np; j0 += JB) {
       S P = pre;
-      if (j0 > 0 || !have_pre) fetch_parts<M>(P, a, t, np, j0, g, lane);
+      if (j0 > 0 || !have_pre) fetch_parts<M, LDS_HO>(P, a, t, np, j0, g, lane);
 #pragma unroll
       for (int j = 0; j < JB; ++j) {
         const int p = 1 + loff + PPI * (j0 + j);
         if (p < np) {
-          const bool same_wg = (g + p) / VALU_WPB == g / VALU_WPB;
+          const bool same_wg = LDS_HO && (g + p) / VALU_WPB == g / VALU_WPB;
 #pragma unroll
           for (int k = 0; k < IPP; ++k) {
             const int si = (lane % NIDX) + 64 * k;
@@ -624,12 +735,17 @@ __device__ __forceinline__ void store_tables(unsigned char* lds, const TableWord
 // of steps through a ring of record buffers (see below). Finishing a tile part never waits on
 // memory except in the part holding chunk 0 of a split tile, which is the last thing its wave
 // does.
-template <int KIND, int D, int M, int RPL, bool MX = false>
+template <int KIND, int D, int M, int RPL, int MODE = 0>
 __global__ void __launch_bounds__(VALU_THREADS)
 __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(KArgs a) {
+  using S = Step<KIND, D, M, RPL, MODE>;
+  // split-tile parts of waves of the same workgroup meet in LDS
+  constexpr bool LDS_HO = true;
+  static_assert(Tables<KIND, D>::bytes + VALU_WPB * M * 16 * 8 + (MODE == 2 ? 0 : VALU_WPB * 256) <= 160 * 1024,
+                "lookup table and hand-over slots exceed LDS");
   __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes];
-  __shared__ __align__(16) uint32_t pstage_all[VALU_WPB * 64];
-  __shared__ uint64_t wg_slots[VALU_WPB * M * 16];   // split-tile parts handed over inside the workgroup
+  __shared__ __align__(16) uint32_t pstage_all[MODE == 2 ? 1 : VALU_WPB * 64];
+  __shared__ uint64_t wg_slots[VALU_WPB * M * 16];
   constexpr int H = 16 / RPL;
   const int lane = threadIdx.x & 63;
   // wave-uniform by construction; readfirstlane keeps the schedule in SGPRs
@@ -656,10 +772,10 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   const int c0 = s_begin - t0 * a.nc;
   const int h = lane % H, vloc = lane / H;
 
-  Rec<KIND, M, RPL, MX> r0, r1;
+  typename S::R r0, r1;
   TableWords<KIND, D> tw;
   fetch_tables<KIND, D>(tw, a);
-  load_rec<KIND, M, RPL, MX>(r0, a, t0, c0, h, vloc, lane);
+  S::load(r0, a, t0, c0, h, vloc, lane);
   store_tables<KIND, D>(lds, tw, a);
   for (int i = threadIdx.x; i < VALU_WPB * M * 16; i += VALU_THREADS) wg_slots[i] = 0;
   const uint32_t mask_off = a.t_bytes;
@@ -667,9 +783,9 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   if (!active) return;                       // no barrier follows
   uint32_t* pstage = pstage_all + wave * 64;
 
-  float acc[M][RPL];
+  float acc[S::AR][RPL];
 #pragma unroll
-  for (int b = 0; b < M; ++b)
+  for (int b = 0; b < S::AR; ++b)
 #pragma unroll
     for (int rr = 0; rr < RPL; ++rr) acc[b][rr] = 0.0f;
 
@@ -690,17 +806,17 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
       ++t1;
       c1 = 0;
     }
-    load_rec<KIND, M, RPL, MX>(r1, a, t1, c1, h, vloc, lane);
-    compute_rec<KIND, D, M, RPL, MX>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c1 == 0) emit_part<M, RPL, false, MX>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
+    S::load(r1, a, t1, c1, h, vloc, lane);
+    S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
+    if (c1 == 0) emit_part<M, RPL, false, MODE, LDS_HO>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
     int t2 = t1, c2 = c1 + 1;
     if (c2 == a.nc) {
       ++t2;
       c2 = 0;
     }
-    load_rec<KIND, M, RPL, MX>(r0, a, t2, c2, h, vloc, lane);   // step 2i + 2 <= nsteps - 1 exists
-    compute_rec<KIND, D, M, RPL, MX>(r1, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c2 == 0) emit_part<M, RPL, false, MX>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
+    S::load(r0, a, t2, c2, h, vloc, lane);   // step 2i + 2 <= nsteps - 1 exists
+    S::compute(r1, acc, lds, mask_off, pstage, lane, h, vloc);
+    if (c2 == 0) emit_part<M, RPL, false, MODE, LDS_HO>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
     t = t2;
     c = c2;
   }
@@ -712,18 +828,18 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
       ++tf;
       cf = 0;
     }
-    load_rec<KIND, M, RPL, MX>(r1, a, tf, cf, h, vloc, lane);
-    compute_rec<KIND, D, M, RPL, MX>(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (cf == 0) emit_part<M, RPL, false, MX>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
+    S::load(r1, a, tf, cf, h, vloc, lane);
+    S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
+    if (cf == 0) emit_part<M, RPL, false, MODE, LDS_HO>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
   }
   const int caf = tf == t0 ? c0 : 0;
   const bool waits = caf == 0 && cf + 1 < a.nc;
   const int np_final = waits ? wave_of_step(a, tf * a.nc + a.nc - 1) - g + 1 : 0;
-  if (waits) fetch_parts<M>(pre, a, tf, np_final, 0, g, lane);
+  if (waits) fetch_parts<M, LDS_HO>(pre, a, tf, np_final, 0, g, lane);
   // one instance of the step code for the last step, whichever buffer holds it
-  const Rec<KIND, M, RPL, MX>& rf = (nsteps - 2 * npairs == 2) ? r1 : r0;
-  compute_rec<KIND, D, M, RPL, MX>(rf, acc, lds, mask_off, pstage, lane, h, vloc);
-  emit_part<M, RPL, true, MX>(a, acc, tf, caf, cf + 1, g, lane, h, pre, waits, wg_slots, np_final);
+  const typename S::R& rf = (nsteps - 2 * npairs == 2) ? r1 : r0;
+  S::compute(rf, acc, lds, mask_off, pstage, lane, h, vloc);
+  emit_part<M, RPL, true, MODE, LDS_HO>(a, acc, tf, caf, cf + 1, g, lane, h, pre, waits, wg_slots, np_final);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -878,10 +994,15 @@ KArgs make_args(const sph_weights* w) {
 template <int KIND, int D>
 const void* valu_fn(int M) {
   switch (M) {
-    case 1: return (const void*)k_gemm_valu<KIND, D, 1, 16>;
-    case 4: return (const void*)k_gemm_valu<KIND, D, 4, 4, true>;
-    default: return (const void*)k_gemm_valu<KIND, D, 8, 4, true>;
+    case 1: return (const void*)k_gemm_valu<KIND, D, 1, 16, 0>;
+    case 4: return (const void*)k_gemm_valu<KIND, D, 4, 4, 1>;
+    case 8: return (const void*)k_gemm_valu<KIND, D, 8, 4, 1>;
   }
+  if constexpr (KIND != SPH_KIND_CB13) {   // the 128 KiB codebook leaves no LDS for 16+ batch slots
+    if (M == 16) return (const void*)k_gemm_valu<KIND, D, 16, 4, 2>;
+    return (const void*)k_gemm_valu<KIND, D, 32, 4, 2>;
+  }
+  return nullptr;
 }
 
 template <int KIND, int D>
@@ -943,9 +1064,11 @@ Launch plan(const sph_weights* w, int m) {
   const int kind = sph_kind_of(w->fmt.dir_bits, w->fmt.radius_bits);
   const int cus = num_cus();
   // batch 1: vector ALU; 2..8: 4x4x4 MFMA blocks on the same records (4 lanes per vector
-  // position, rebuilt weights rounded to fp16); 9..32: the tile-per-workgroup MFMA kernel
-  if (m <= 8) {
-    const int M = m <= 1 ? 1 : m <= 4 ? 4 : 8;
+  // position); 9..32: 16x16x32 MFMA tiles (lane = row x position group). The batched variants
+  // round each rebuilt weight to fp16. All share the step plan below (16 positions per step for
+  // the batched variants, 64 for batch 1).
+  if (m <= (kind == SPH_KIND_CB13 ? 8 : 32)) {
+    const int M = m <= 1 ? 1 : m <= 4 ? 4 : m <= 8 ? 8 : m <= 16 ? 16 : 32;
     const int H = M == 1 ? 1 : 4;
     const int vpc = 64 / H;
     const int wpb = VALU_WPB;

@@ -58,6 +58,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3, help="workload id in synth.WORKLOADS")
     ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--fmt", default="", help="override the workload's format (e.g. W3)")
     ap.add_argument("--layers", type=int, default=0, help="override layer count (0: workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
@@ -152,7 +153,7 @@ def main():
         raise RuntimeError("bench.py needs a GPU")
     dev = torch.device("cuda:0")
     wl = synth.WORKLOADS[args.workload]
-    fmt = wl.fmt
+    fmt = args.fmt or wl.fmt
     D, V = synth.FORMATS[fmt]
     m = args.batch
     layers = args.layers or wl.layers
@@ -259,7 +260,7 @@ def main():
         "data": "synthetic: seeded uniform codes and per-row radius scales, random positive "
                 "unit codebook, fp16 N(0,1) activations",
         "config": {
-            "workload": f"{wl.name}-m{m}",
+            "workload": f"{wl.name}-{fmt}-m{m}" if args.fmt else f"{wl.name}-m{m}",
             "format": f"{fmt} (8 sign + {D} direction + {V} radius bits per 8-vector)",
             "layers": layers,
             "shapes": [f"{label} {n}x{k}" for label, n, k, *_ in packed],
@@ -272,8 +273,7 @@ def main():
         "tokens_per_s": round(m / (ms / 1e3), 2),
         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "roofline": {
-            "kernel": f"k_gemm_valu<W2,M={m}> on {', '.join(f'{p[1]}x{p[2]}' for p in big)}"
-            if m <= 8 else f"k_gemm_mfma<W2> on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
+            "kernel": f"{kernel_label(fmt, m)} on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
             "bound": "hbm",
             "achieved": round(dom_gbs, 2),
             "peak": HBM_PEAK_GBS,
@@ -290,6 +290,15 @@ def main():
         out["cpu_baseline"] = cpu_baseline(mats_cpu, args.cpu_sample_seconds, step_bytes,
                                            per_mat_bytes, layers)
     print(json.dumps(out), flush=True)
+
+
+def kernel_label(fmt, m):
+    """The decode kernel variant the library picks for this format and batch."""
+    if m == 1:
+        return f"k_gemm_valu<{fmt},M=1> (vector ALU)"
+    if m <= 8:
+        return f"k_gemm_valu<{fmt},M={4 if m <= 4 else 8}> (4x4x4 MFMA blocks)"
+    return f"k_gemm_valu<{fmt},M={16 if m <= 16 else 32}> (16x16x32 MFMA tiles)"
 
 
 def clone_weights(pkg, w):

@@ -43,7 +43,6 @@ struct KArgs {
   int64_t ldy;
   int y_f16;
   int n, nt, nv, ng, m;
-  int wpt;            // waves per tile (matrix-core kernel)
   // vector-ALU work plan: ts = nt * nc steps in tile-major order, cut into one contiguous range
   // per workgroup (whole tiles when wg_tiles > 0, else balanced to one step), each cut evenly
   // among the workgroup's waves
@@ -130,29 +129,6 @@ __device__ __forceinline__ float dot8(uint4 t, const uint32_t (&x)[4]) {
   return __builtin_amdgcn_fdot2(as_h2(t.w), as_h2(x[3]), p, false);
 }
 
-// Stage the lookup tables (and for the codebook kind the 16-entry sign-mask table, placed right
-// after the codebook at LDS offset a.t_bytes) into LDS. Returns the first free LDS offset,
-// rounded up to 16 bytes.
-template <int KIND>
-__device__ __forceinline__ uint32_t stage_tables(unsigned char* lds, const KArgs& a) {
-  uint4* dst = (uint4*)lds;
-  const uint32_t n16 = a.t_bytes / 16u;
-  for (uint32_t i = threadIdx.x; i < n16; i += blockDim.x) dst[i] = a.T[i];
-  uint32_t end = a.t_bytes;
-  if constexpr (KIND == SPH_KIND_CB13) {
-    // mask[s] flips the fp16 sign bit of element j (of 4) where bit j of the nibble s is set.
-    if (threadIdx.x < 16) {
-      const uint32_t s = threadIdx.x;
-      uint2 m;
-      m.x = ((s & 1u) << 15) | ((s & 2u) << 30);
-      m.y = ((s & 4u) << 13) | ((s & 8u) << 28);
-      *(uint2*)(lds + end + s * 8u) = m;
-    }
-    end += 128;
-  }
-  return (end + 15u) & ~15u;
-}
-
 template <int N>
 __device__ __forceinline__ void load_dw(uint32_t (&d)[N], const uint32_t* p) {
   if constexpr (N == 16) {
@@ -205,6 +181,13 @@ template <int KIND, int D>
 struct Tables {
   static constexpr uint32_t bytes = (KIND == SPH_KIND_CB13) ? ((16u << D) + 128u) : (256u << D);
 };
+
+// Whether the split-tile parts of one workgroup's waves fit in LDS next to the lookup table (else
+// they go through the global workspace, and the plan keeps to balanced ranges). Host and device.
+__host__ __device__ constexpr bool lds_handover_fits(int kind, int D, int M, int mode) {
+  return ((kind == SPH_KIND_CB13) ? ((16u << D) + 128u) : (256u << D)) + 16u * M * 16u * 8u +
+             (mode == 2 ? 0u : 16u * 256u) <= 160u * 1024u;
+}
 
 // MX selects the matrix-core variant (batch 2..16): the lane's rows are rebuilt as in the vector
 // variant, scaled to fp16 and multiplied by 4x4x4 MFMA blocks, one block per vector position.
@@ -739,13 +722,13 @@ template <int KIND, int D, int M, int RPL, int MODE = 0>
 __global__ void __launch_bounds__(VALU_THREADS)
 __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(KArgs a) {
   using S = Step<KIND, D, M, RPL, MODE>;
-  // split-tile parts of waves of the same workgroup meet in LDS
-  constexpr bool LDS_HO = true;
-  static_assert(Tables<KIND, D>::bytes + VALU_WPB * M * 16 * 8 + (MODE == 2 ? 0 : VALU_WPB * 256) <= 160 * 1024,
-                "lookup table and hand-over slots exceed LDS");
+  // split-tile parts of waves of the same workgroup meet in LDS when it has room
+  constexpr bool LDS_HO = lds_handover_fits(KIND, D, M, MODE);
+  static_assert(VALU_WPB == 16, "lds_handover_fits assumes 16 waves per workgroup");
+  static_assert(LDS_HO || MODE == 2, "only the tile variant may hand over through the workspace alone");
   __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes];
   __shared__ __align__(16) uint32_t pstage_all[MODE == 2 ? 1 : VALU_WPB * 64];
-  __shared__ uint64_t wg_slots[VALU_WPB * M * 16];
+  __shared__ uint64_t wg_slots[LDS_HO ? VALU_WPB * M * 16 : 1];
   constexpr int H = 16 / RPL;
   const int lane = threadIdx.x & 63;
   // wave-uniform by construction; readfirstlane keeps the schedule in SGPRs
@@ -777,7 +760,8 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   fetch_tables<KIND, D>(tw, a);
   S::load(r0, a, t0, c0, h, vloc, lane);
   store_tables<KIND, D>(lds, tw, a);
-  for (int i = threadIdx.x; i < VALU_WPB * M * 16; i += VALU_THREADS) wg_slots[i] = 0;
+  if constexpr (LDS_HO)
+    for (int i = threadIdx.x; i < VALU_WPB * M * 16; i += VALU_THREADS) wg_slots[i] = 0;
   const uint32_t mask_off = a.t_bytes;
   __syncthreads();
   if (!active) return;                       // no barrier follows
@@ -843,92 +827,6 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
 }
 
 // ------------------------------------------------------------------------------------------
-// Matrix-core kernel: batch up to 16*NB; weights rounded once to fp16, fp32 accumulation.
-// ------------------------------------------------------------------------------------------
-
-// Decode row r of record `rec` and return its signed direction (4 half2) and radius level.
-template <int KIND, int D>
-__device__ __forceinline__ uint4 decode_row(const unsigned char* lds, uint32_t mask_off, const KArgs& a,
-                                            int64_t rec, int r, uint32_t& q) {
-  if constexpr (KIND == SPH_KIND_CB13) {
-    const uint32_t sdw = a.A[rec * 4 + (r >> 2)];
-    const uint32_t zdw = a.B[rec * 8 + (r >> 1)];
-    uint32_t s, z;
-    decode_cb13(sdw, r & 3, zdw, r & 1, s, z, q);
-    return signed_dir_cb13(lds, mask_off, s, z);
-  } else {
-    const uint32_t d = a.A[rec * 8 + (r >> 1)];
-    uint32_t qx = 0;
-    if constexpr (KIND == SPH_KIND_W2) qx = (a.B[rec] >> (4 * (r >> 1))) & 15u;
-    if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (a.B[rec * 4 + (r >> 2)] >> (8 * (r & 3))) & 0xFFu;
-    uint32_t lo, hi;
-    decode_nib<KIND, D>(d, r & 1, qx, lo, hi, q);
-    return signed_dir_nib<KIND, D>(lds, lo, hi);
-  }
-}
-
-__device__ __forceinline__ uint32_t scale_pack(uint32_t t, float rh) {
-  const f16 lo = (f16)(rh * f16lo(t));
-  const f16 hi = (f16)(rh * f16hi(t));
-  return (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
-}
-
-template <int KIND, int D, int NB>
-__global__ void __launch_bounds__(1024) k_gemm_mfma(KArgs a) {
-  constexpr int WMAX = (KIND == SPH_KIND_CB13) ? 8 : 16;
-  __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes + WMAX * NB * 1024];
-  const uint32_t mask_off = a.t_bytes;
-  const uint32_t red_off = stage_tables<KIND>(lds, a);
-  float* red = (float*)(lds + red_off);
-  __syncthreads();
-
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, W = a.wpt;
-  const int r = lane & 15, j = lane >> 4;
-
-  for (int t = blockIdx.x; t < a.nt; t += gridDim.x) {
-    f32x4 acc[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    for (int vb = 4 * wave; vb < a.nv; vb += 4 * W) {
-      const int v = vb + j;
-      const int64_t rec = (int64_t)t * a.nv + v;
-      uint32_t q;
-      const uint4 tt = decode_row<KIND, D>(lds, mask_off, a, rec, r, q);
-      const uint32_t pr = a.P[((int64_t)t * a.ng + (v >> 4)) * 16 + r];
-      const float rh = fmaf((float)q, f16hi(pr), f16lo(pr));
-      uint4 wq;
-      wq.x = scale_pack(tt.x, rh);
-      wq.y = scale_pack(tt.y, rh);
-      wq.z = scale_pack(tt.z, rh);
-      wq.w = scale_pack(tt.w, rh);
-      const f16x8 wa = __builtin_bit_cast(f16x8, wq);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const int b = nb * 16 + r;
-        uint4 xq = make_uint4(0, 0, 0, 0);
-        if (b < a.m) xq = *(const uint4*)(a.x + (int64_t)b * a.ldx + 8 * (int64_t)v);
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa, __builtin_bit_cast(f16x8, xq), acc[nb], 0, 0, 0);
-      }
-    }
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) red[((wave * NB + nb) * 64 + lane) * 4 + e] = acc[nb][e];
-    __syncthreads();
-    for (int i = threadIdx.x; i < NB * 256; i += blockDim.x) {
-      const int nb = i / 256, l = (i / 4) % 64, e = i % 4;
-      float s = 0.0f;
-      for (int w = 0; w < W; ++w) s += red[((w * NB + nb) * 64 + l) * 4 + e];
-      const int row = 4 * (l >> 4) + e, b = nb * 16 + (l & 15);
-      const int grow = t * 16 + row;
-      if (b < a.m && grow < a.n) store_y(a, b, grow, s);
-    }
-    __syncthreads();
-  }
-}
-
-// ------------------------------------------------------------------------------------------
 // Unpack: logical codes through the compute kernels' field extraction.
 // ------------------------------------------------------------------------------------------
 template <int KIND, int D>
@@ -970,7 +868,6 @@ struct Launch {
   const void* fn;
   int block;          // threads per workgroup
   int grid;
-  int wpt;            // matrix-core kernel: waves per tile
   int nc, wg_tiles, wq, wr, pmax, ts;
   size_t ws_bytes;    // workspace the launch needs
 };
@@ -998,28 +895,19 @@ const void* valu_fn(int M) {
     case 4: return (const void*)k_gemm_valu<KIND, D, 4, 4, 1>;
     case 8: return (const void*)k_gemm_valu<KIND, D, 8, 4, 1>;
   }
-  if constexpr (KIND != SPH_KIND_CB13) {   // the 128 KiB codebook leaves no LDS for 16+ batch slots
-    if (M == 16) return (const void*)k_gemm_valu<KIND, D, 16, 4, 2>;
-    return (const void*)k_gemm_valu<KIND, D, 32, 4, 2>;
-  }
-  return nullptr;
+  if (M == 16) return (const void*)k_gemm_valu<KIND, D, 16, 4, 2>;
+  return (const void*)k_gemm_valu<KIND, D, 32, 4, 2>;
 }
 
-template <int KIND, int D>
-const void* mfma_fn(int NB) {
-  return NB == 1 ? (const void*)k_gemm_mfma<KIND, D, 1> : (const void*)k_gemm_mfma<KIND, D, 2>;
-}
-
-const void* pick(int D, int V, bool mfma, int sel) {
-  const int kind = sph_kind_of(D, V);
-  switch (kind) {
-    case SPH_KIND_W2: return mfma ? mfma_fn<SPH_KIND_W2, 6>(sel) : valu_fn<SPH_KIND_W2, 6>(sel);
+const void* pick(int D, int V, int M) {
+  switch (sph_kind_of(D, V)) {
+    case SPH_KIND_W2: return valu_fn<SPH_KIND_W2, 6>(M);
     case SPH_KIND_NIB16:
-      if (D == 4) return mfma ? mfma_fn<SPH_KIND_NIB16, 4>(sel) : valu_fn<SPH_KIND_NIB16, 4>(sel);
-      if (D == 5) return mfma ? mfma_fn<SPH_KIND_NIB16, 5>(sel) : valu_fn<SPH_KIND_NIB16, 5>(sel);
-      return mfma ? mfma_fn<SPH_KIND_NIB16, 6>(sel) : valu_fn<SPH_KIND_NIB16, 6>(sel);
-    case SPH_KIND_NIB16Q8: return mfma ? mfma_fn<SPH_KIND_NIB16Q8, 8>(sel) : valu_fn<SPH_KIND_NIB16Q8, 8>(sel);
-    case SPH_KIND_CB13: return mfma ? mfma_fn<SPH_KIND_CB13, 13>(sel) : valu_fn<SPH_KIND_CB13, 13>(sel);
+      if (D == 4) return valu_fn<SPH_KIND_NIB16, 4>(M);
+      if (D == 5) return valu_fn<SPH_KIND_NIB16, 5>(M);
+      return valu_fn<SPH_KIND_NIB16, 6>(M);
+    case SPH_KIND_NIB16Q8: return valu_fn<SPH_KIND_NIB16Q8, 8>(M);
+    case SPH_KIND_CB13: return valu_fn<SPH_KIND_CB13, 13>(M);
   }
   return nullptr;
 }
@@ -1067,7 +955,7 @@ Launch plan(const sph_weights* w, int m) {
   // position); 9..32: 16x16x32 MFMA tiles (lane = row x position group). The batched variants
   // round each rebuilt weight to fp16. All share the step plan below (16 positions per step for
   // the batched variants, 64 for batch 1).
-  if (m <= (kind == SPH_KIND_CB13 ? 8 : 32)) {
+  if (m <= 32) {
     const int M = m <= 1 ? 1 : m <= 4 ? 4 : m <= 8 ? 8 : m <= 16 ? 16 : 32;
     const int H = M == 1 ? 1 : 4;
     const int vpc = 64 / H;
@@ -1083,8 +971,9 @@ Launch plan(const sph_weights* w, int m) {
     // meet in global slots); at most ts / wpb workgroups, so that every wave gets a step
     const int64_t gB = std::max<int64_t>(1, std::min<int64_t>(slots, ts / wpb));
     const int64_t lB = (ts + gB * wpb - 1) / (gB * wpb);
-    const bool aligned = lA <= lB;
-    L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, false, M);
+    // whole tiles per workgroup need the parts inside a workgroup to meet in LDS
+    const bool aligned = lA <= lB && lds_handover_fits(kind, w->fmt.dir_bits, M, M == 1 ? 0 : M <= 8 ? 1 : 2);
+    L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, M);
     L.block = 64 * wpb;
     L.nc = (int)nc;
     L.ts = (int)ts;
@@ -1104,18 +993,6 @@ Launch plan(const sph_weights* w, int m) {
       L.pmax = (int)(nc / lmin + 2);
       L.ws_bytes = (size_t)nt * L.pmax * M * 16 * 8;
     }
-  } else {
-    const int NB = m <= 16 ? 1 : 2;
-    const int64_t per_wave = 4 * 8;             // 8 MFMA steps per wave
-    int wpt = (int)((nv + per_wave - 1) / per_wave);
-    const int wmax = (kind == SPH_KIND_CB13) ? 8 : 16;
-    wpt = wpt < 1 ? 1 : wpt > wmax ? wmax : wpt;
-    L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, true, NB);
-    L.wpt = wpt;
-    L.block = 64 * wpt;
-    const int64_t cap = (int64_t)cus * 4;
-    L.grid = (int)(nt < cap ? nt : cap);
-    L.ws_bytes = 0;
   }
   return L;
 }
@@ -1241,7 +1118,6 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
   a.ldy = ldy;
   a.y_f16 = (y_dtype == SPH_F16);
   a.m = (int)m;
-  a.wpt = L.wpt;
   return launch(L, a, (hipStream_t)stream);
 }
 

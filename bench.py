@@ -36,19 +36,24 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 
 # HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE + WRITE_SIZE runs, each
 # scaled by the reading of a plain device copy of known size (see profiles/). Keyed by the
-# SHA-256 of the kernel source the counters were taken with: any change to the kernels makes
-# the entry stale and `traffic` is reported as null.
+# SHA-256 of the kernel source and compile flags the counters were taken with: any change to
+# the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "cd94ca3712c51d9a33f144b6e34f838f13f1473c6677129e56559251149b6147": {
-        "7168x5120-m1": 11945869, "5120x5120-m1": 9358232,
-        "51200x5120-m1": 82773938, "5120x25600-m1": 42907589},
+    "b3f9d293118efa124a69f58f85369bd75c1b84e6d54510059e8bf329389ce343": {
+        "7168x5120-m1": 11943949, "5120x5120-m1": 9339802,
+        "51200x5120-m1": 82789648, "5120x25600-m1": 42926722},
 }
 
 
 def kernel_source_hash() -> str:
+    """SHA-256 of the kernel source followed by the compile flags (both decide the code)."""
     import hashlib
+    from paper_2609_24875_amd import build as B
+    h = hashlib.sha256()
     with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+        h.update(f.read())
+    h.update(" ".join(B.HIPCC_FLAGS).encode())
+    return h.hexdigest()
 
 
 def parse():

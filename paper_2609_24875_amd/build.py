@@ -15,6 +15,10 @@ HIPCC_FLAGS = [
     "-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC", "-shared",
     # Packed fp32 instructions stay off: the compiler must not emit v_pk_{add,mul,fma}_f32.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # The fp16 dot builtin is emitted as the three-operand v_dot2_f32_f16: the two-operand
+    # v_dot2c_f32_f16 ties its accumulator to the destination and costs a copy of the zero seed
+    # per rebuilt vector.
+    "-Xclang", "-target-feature", "-Xclang", "-dot5-insts",
     "-Wall", "-Wno-unused-command-line-argument",
 ]
 

@@ -58,7 +58,10 @@ typedef enum { SPH_F16 = 0, SPH_F32 = 1 } sph_dtype;
  *   (13, 3) W3: K_dir = 7*3 - 8 = 13 with 3 radius bits (3.00 bits/weight payload, App. B)
  *   (4, 4)  16-bit vectors: 8 sign + 4 direction + 4 radius bits
  *   (6, 2)  16-bit vectors: 8 sign + 6 direction + 2 radius bits (2.00 bits/weight payload)
- *   (8, 8)  24-bit vectors: 8 sign + 8 direction + 8 radius bits                              */
+ *   (8, 8)  24-bit vectors: 8 sign + 8 direction + 8 radius bits
+ *   (13, 4) W3 with 4 radius bits (3.125 bits/weight payload, the W3 row of Tab. 1)
+ *   (6, 3), (7, 2), (8, 2)  further splits of the W2 budget from the bit-allocation study of
+ *           Tab. 4 (8 sign bits + D direction + V radius bits)                                 */
 typedef struct {
   int32_t vec_dim;      /* must be 8   */
   int32_t dir_bits;     /* D           */

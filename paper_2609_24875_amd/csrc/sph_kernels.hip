@@ -35,6 +35,7 @@ struct KArgs {
   const uint32_t* A;
   const uint32_t* B;
   const uint32_t* P;
+  const uint16_t* C;  // codebook kind with 4 radius bits: bit 3 of q, one 16-bit word per record
   const uint4* T;
   uint32_t t_bytes;   // bytes of lookup tables staged into LDS
   const uint16_t* x;
@@ -68,10 +69,12 @@ __device__ __forceinline__ void decode_nib(uint32_t d, bool odd, uint32_t qx, ui
                                            uint32_t& hi, uint32_t& q) {
   constexpr uint32_t IM = (1u << (D + 4)) - 1;
   if constexpr (KIND == SPH_KIND_W2) {
-    const uint32_t f = odd ? ((d >> 14) & 0x3FFFu) : (d & 0x3FFFu);
+    constexpr int W = 8 + D;                   // field width
+    constexpr uint32_t FM = (1u << W) - 1u;
+    const uint32_t f = odd ? ((d >> W) & FM) : (d & FM);
     lo = f & IM;
     hi = f >> 4;
-    q = odd ? qx : (d >> 28);
+    q = odd ? qx : (d >> (2 * W));
   } else {
     const uint32_t f = odd ? (d >> 16) : (d & 0xFFFFu);
     lo = f & IM;
@@ -177,15 +180,18 @@ constexpr int VALU_THREADS = 64 * VALU_WPB;
 constexpr int VALU_RB = 4;
 constexpr bool VALU_PIPE_BARRIERS = true;
 
+template <int KIND>
+constexpr bool IS_CB = KIND == SPH_KIND_CB13 || KIND == SPH_KIND_CB13Q4;
+
 template <int KIND, int D>
 struct Tables {
-  static constexpr uint32_t bytes = (KIND == SPH_KIND_CB13) ? ((16u << D) + 128u) : (256u << D);
+  static constexpr uint32_t bytes = IS_CB<KIND> ? ((16u << D) + 128u) : (256u << D);
 };
 
 // Whether the split-tile parts of one workgroup's waves fit in LDS next to the lookup table (else
 // they go through the global workspace, and the plan keeps to balanced ranges). Host and device.
 __host__ __device__ constexpr bool lds_handover_fits(int kind, int D, int M, int mode) {
-  return ((kind == SPH_KIND_CB13) ? ((16u << D) + 128u) : (256u << D)) + 16u * M * 16u * 8u +
+  return ((kind == SPH_KIND_CB13 || kind == SPH_KIND_CB13Q4) ? ((16u << D) + 128u) : (256u << D)) + 16u * M * 16u * 8u +
              (mode == 2 ? 0u : 16u * 256u) <= 160u * 1024u;
 }
 
@@ -193,11 +199,12 @@ __host__ __device__ constexpr bool lds_handover_fits(int kind, int D, int M, int
 // variant, scaled to fp16 and multiplied by 4x4x4 MFMA blocks, one block per vector position.
 template <int KIND, int M, int RPL, bool MX = false>
 struct Rec {
-  static constexpr int ADW = (KIND == SPH_KIND_CB13) ? RPL / 4 : RPL / 2;
-  static constexpr int BDW = (KIND == SPH_KIND_NIB16Q8) ? RPL / 4 : (KIND == SPH_KIND_CB13) ? RPL / 2 : 1;
+  static constexpr int ADW = IS_CB<KIND> ? RPL / 4 : RPL / 2;
+  static constexpr int BDW = (KIND == SPH_KIND_NIB16Q8) ? RPL / 4 : IS_CB<KIND> ? RPL / 2 : 1;
   static constexpr int NX = MX ? M / 4 : M;
   uint32_t ra[ADW];
   uint32_t rb[BDW];
+  uint32_t rc;         // stream C word of the record (codebook kind with 4 radius bits)
   uint32_t pw;         // one group-parameter word of the chunk, staged through LDS at compute time
   uint32_t xv[NX][4];  // vector variant: x[b] at this lane's position for every batch row b;
                        // MX: x[4g + lane % 4] at this lane's position for each group g of 4 rows
@@ -213,14 +220,16 @@ template <int KIND, int M, int RPL, bool MX = false>
 __device__ __forceinline__ void load_rec(Rec<KIND, M, RPL, MX>& R, const KArgs& a, int t, int c, int h, int vloc,
                                          int lane) {
   constexpr int H = 16 / RPL, VPC = 64 / H;
-  constexpr int ADW_REC = (KIND == SPH_KIND_CB13) ? 4 : 8;
-  constexpr int BDW_REC = (KIND == SPH_KIND_W2) ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
+  constexpr int ADW_REC = IS_CB<KIND> ? 4 : 8;
+  constexpr int BDW_REC = (KIND == SPH_KIND_W2 || KIND == SPH_KIND_NIB16Q2) ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
   constexpr int ADW = Rec<KIND, M, RPL, MX>::ADW, BDW = Rec<KIND, M, RPL, MX>::BDW;
   const int v = min(c * VPC + vloc, a.nv - 1);
   const int64_t rec = (int64_t)t * a.nv + v;
   load_dw<ADW>(R.ra, a.A + rec * ADW_REC + h * ADW);
-  if constexpr (KIND == SPH_KIND_W2) R.rb[0] = a.B[rec];
+  if constexpr (KIND == SPH_KIND_W2 || KIND == SPH_KIND_NIB16Q2) R.rb[0] = a.B[rec];
   else if constexpr (KIND != SPH_KIND_NIB16) load_dw<BDW>(R.rb, a.B + rec * BDW_REC + h * BDW);
+  if constexpr (KIND == SPH_KIND_CB13Q4) R.rc = a.C[rec];
+  else R.rc = 0;
   // parameter word `lane` of the chunk: group c*VPC/16 + lane/16, row lane%16 (clamped to the row)
   const int pg0 = c * (VPC / 16) + (lane & (VPC - 1)) / 16;
   const int pg = min(pg0, a.ng - 1);
@@ -250,13 +259,15 @@ __device__ __forceinline__ void lookup_rows(const Rec<KIND, M, RPL, MX>& R, int 
   for (int i = 0; i < RB; ++i) {
     const int r = r0 + i;
     uint32_t q;
-    if constexpr (KIND == SPH_KIND_CB13) {
+    if constexpr (IS_CB<KIND>) {
       uint32_t s, z;
       decode_cb13(R.ra[r / 4], r % 4, R.rb[r / 2], r & 1, s, z, q);
+      if constexpr (KIND == SPH_KIND_CB13Q4) q |= ((qodd >> r) & 1u) << 3;
       tt[i] = signed_dir_cb13(lds, mask_off, s, z);
     } else {
       uint32_t lo, hi, qx = 0;
       if constexpr (KIND == SPH_KIND_W2) qx = (qodd >> (4 * (r / 2))) & 15u;
+      if constexpr (KIND == SPH_KIND_NIB16Q2) qx = (qodd >> (2 * r)) & 3u;
       if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (R.rb[r / 4] >> (8 * (r % 4))) & 0xFFu;
       decode_nib<KIND, D>(R.ra[r / 2], r & 1, qx, lo, hi, q);
       tt[i] = signed_dir_nib<KIND, D>(lds, lo, hi);
@@ -287,8 +298,11 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL, MX>& R, floa
     const uint4 u = *(const uint4*)(src + i);
     pp[i] = u.x; pp[i + 1] = u.y; pp[i + 2] = u.z; pp[i + 3] = u.w;
   }
+  // radius bits kept outside the lane's A words, shifted to its first row
   uint32_t qodd = 0;
   if constexpr (KIND == SPH_KIND_W2) qodd = R.rb[0] >> (4 * (h * RPL / 2));
+  if constexpr (KIND == SPH_KIND_NIB16Q2) qodd = R.rb[0] >> (2 * h * RPL);
+  if constexpr (KIND == SPH_KIND_CB13Q4) qodd = R.rc >> (h * RPL);
   uint4 tt[2][RB];
   float qf[2][RB];
   lookup_rows<KIND, D, M, RPL, RB, MX>(R, 0, qodd, lds, mask_off, tt[0], qf[0]);
@@ -337,6 +351,7 @@ template <int KIND, int NB>
 struct RecT {
   uint32_t ra[4];
   uint32_t rb[4];
+  uint32_t rc[4];         // stream C words (codebook kind with 4 radius bits)
   uint32_t pw;            // (min, step) of this lane's row in the chunk's group
   uint32_t xv[NB * 4][4]; // x[16nb + lane % 16] at position 4i + j, index nb * 4 + i
   bool pok;
@@ -344,12 +359,13 @@ struct RecT {
 
 template <int KIND, int NB>
 __device__ __forceinline__ void load_rec_t(RecT<KIND, NB>& R, const KArgs& a, int t, int c, int lane) {
-  constexpr int ADW_REC = (KIND == SPH_KIND_CB13) ? 4 : 8;
-  constexpr int BDW_REC = (KIND == SPH_KIND_W2) ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
+  constexpr bool B1 = KIND == SPH_KIND_W2 || KIND == SPH_KIND_NIB16Q2;   // one B dword per record
+  constexpr int ADW_REC = IS_CB<KIND> ? 4 : 8;
+  constexpr int BDW_REC = B1 ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
   const int r = lane & 15, j = lane >> 4;
   // the dword holding row r in each stream
-  const int adw = (KIND == SPH_KIND_CB13) ? r / 4 : r / 2;
-  const int bdw = (KIND == SPH_KIND_W2) ? 0 : (KIND == SPH_KIND_NIB16Q8) ? r / 4 : r / 2;
+  const int adw = IS_CB<KIND> ? r / 4 : r / 2;
+  const int bdw = B1 ? 0 : (KIND == SPH_KIND_NIB16Q8) ? r / 4 : r / 2;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int v = min(c * 16 + 4 * i + j, a.nv - 1);
@@ -357,6 +373,8 @@ __device__ __forceinline__ void load_rec_t(RecT<KIND, NB>& R, const KArgs& a, in
     R.ra[i] = a.A[rec * ADW_REC + adw];
     if constexpr (KIND != SPH_KIND_NIB16) R.rb[i] = a.B[rec * BDW_REC + bdw];
     else R.rb[i] = 0;
+    if constexpr (KIND == SPH_KIND_CB13Q4) R.rc[i] = a.C[rec];
+    else R.rc[i] = 0;
   }
   // one 128-weight group per chunk: (min, step) of row r
   const int pg = min(c, a.ng - 1);
@@ -383,13 +401,15 @@ __device__ __forceinline__ void compute_rec_t(const RecT<KIND, NB>& R, float (&a
   uint32_t q[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    if constexpr (KIND == SPH_KIND_CB13) {
+    if constexpr (IS_CB<KIND>) {
       uint32_t sg, z;
       decode_cb13(R.ra[i], r % 4, R.rb[i], r & 1, sg, z, q[i]);
+      if constexpr (KIND == SPH_KIND_CB13Q4) q[i] |= ((R.rc[i] >> r) & 1u) << 3;
       tt[i] = signed_dir_cb13(lds, mask_off, sg, z);
     } else {
       uint32_t l, hh, qx = 0;
       if constexpr (KIND == SPH_KIND_W2) qx = (R.rb[i] >> (4 * (r / 2))) & 15u;
+      if constexpr (KIND == SPH_KIND_NIB16Q2) qx = (R.rb[i] >> (2 * r)) & 3u;
       if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (R.rb[i] >> (8 * (r % 4))) & 0xFFu;
       decode_nib<KIND, D>(R.ra[i], r & 1, qx, l, hh, q[i]);
       tt[i] = signed_dir_nib<KIND, D>(lds, l, hh);
@@ -679,7 +699,7 @@ __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[MODE == 2
 
 template <int KIND, int D>
 struct TableWords {
-  static constexpr int N16 = (int)((Tables<KIND, D>::bytes - (KIND == SPH_KIND_CB13 ? 128u : 0u)) / 16u);
+  static constexpr int N16 = (int)((Tables<KIND, D>::bytes - (IS_CB<KIND> ? 128u : 0u)) / 16u);
   static constexpr int PER = (N16 + VALU_THREADS - 1) / VALU_THREADS;
   uint4 w[PER];
 };
@@ -702,7 +722,7 @@ __device__ __forceinline__ void store_tables(unsigned char* lds, const TableWord
     const int j = (int)threadIdx.x + VALU_THREADS * i;
     if (j < N16) ((uint4*)lds)[j] = tw.w[i];
   }
-  if constexpr (KIND == SPH_KIND_CB13) {
+  if constexpr (IS_CB<KIND>) {
     // mask[s] flips the fp16 sign bit of element j (of 4) where bit j of the nibble s is set.
     if (threadIdx.x < 16) {
       const uint32_t s = threadIdx.x;
@@ -840,12 +860,14 @@ __global__ void __launch_bounds__(256) k_unpack(KArgs a, uint8_t* signs, uint16_
   const int64_t row = t * 16 + r;
   if (row >= a.n) return;
   uint32_t s, z, q;
-  if constexpr (KIND == SPH_KIND_CB13) {
+  if constexpr (IS_CB<KIND>) {
     decode_cb13(a.A[rec * 4 + (r >> 2)], r & 3, a.B[rec * 8 + (r >> 1)], r & 1, s, z, q);
+    if constexpr (KIND == SPH_KIND_CB13Q4) q |= ((uint32_t)(a.C[rec] >> r) & 1u) << 3;
   } else {
     const uint32_t d = a.A[rec * 8 + (r >> 1)];
     uint32_t qx = 0;
     if constexpr (KIND == SPH_KIND_W2) qx = (a.B[rec] >> (4 * (r >> 1))) & 15u;
+    if constexpr (KIND == SPH_KIND_NIB16Q2) qx = (a.B[rec] >> (2 * r)) & 3u;
     if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (a.B[rec * 4 + (r >> 2)] >> (8 * (r & 3))) & 0xFFu;
     uint32_t lo, hi;
     decode_nib<KIND, D>(d, r & 1, qx, lo, hi, q);
@@ -879,6 +901,7 @@ KArgs make_args(const sph_weights* w) {
   a.A = (const uint32_t*)(base + w->off[SPH_OFF_A]);
   a.B = (const uint32_t*)(base + w->off[SPH_OFF_B]);
   a.P = (const uint32_t*)(base + w->off[SPH_OFF_PARAMS]);
+  a.C = (const uint16_t*)(base + w->off[SPH_OFF_C]);
   a.T = (const uint4*)(base + w->off[SPH_OFF_TABLES]);
   a.t_bytes = (uint32_t)sph_table_bytes(kind, w->fmt.dir_bits);
   a.n = (int)w->n;
@@ -901,26 +924,30 @@ const void* valu_fn(int M) {
 
 const void* pick(int D, int V, int M) {
   switch (sph_kind_of(D, V)) {
-    case SPH_KIND_W2: return valu_fn<SPH_KIND_W2, 6>(M);
+    case SPH_KIND_W2: return D == 7 ? valu_fn<SPH_KIND_W2, 7>(M) : valu_fn<SPH_KIND_W2, 6>(M);
     case SPH_KIND_NIB16:
       if (D == 4) return valu_fn<SPH_KIND_NIB16, 4>(M);
       if (D == 5) return valu_fn<SPH_KIND_NIB16, 5>(M);
       return valu_fn<SPH_KIND_NIB16, 6>(M);
     case SPH_KIND_NIB16Q8: return valu_fn<SPH_KIND_NIB16Q8, 8>(M);
+    case SPH_KIND_NIB16Q2: return valu_fn<SPH_KIND_NIB16Q2, 8>(M);
     case SPH_KIND_CB13: return valu_fn<SPH_KIND_CB13, 13>(M);
+    case SPH_KIND_CB13Q4: return valu_fn<SPH_KIND_CB13Q4, 13>(M);
   }
   return nullptr;
 }
 
 const void* unpack_fn(int D, int V) {
   switch (sph_kind_of(D, V)) {
-    case SPH_KIND_W2: return (const void*)k_unpack<SPH_KIND_W2, 6>;
+    case SPH_KIND_W2: return D == 7 ? (const void*)k_unpack<SPH_KIND_W2, 7> : (const void*)k_unpack<SPH_KIND_W2, 6>;
     case SPH_KIND_NIB16:
       if (D == 4) return (const void*)k_unpack<SPH_KIND_NIB16, 4>;
       if (D == 5) return (const void*)k_unpack<SPH_KIND_NIB16, 5>;
       return (const void*)k_unpack<SPH_KIND_NIB16, 6>;
     case SPH_KIND_NIB16Q8: return (const void*)k_unpack<SPH_KIND_NIB16Q8, 8>;
+    case SPH_KIND_NIB16Q2: return (const void*)k_unpack<SPH_KIND_NIB16Q2, 8>;
     case SPH_KIND_CB13: return (const void*)k_unpack<SPH_KIND_CB13, 13>;
+    case SPH_KIND_CB13Q4: return (const void*)k_unpack<SPH_KIND_CB13Q4, 13>;
   }
   return nullptr;
 }

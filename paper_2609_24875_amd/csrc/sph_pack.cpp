@@ -49,6 +49,8 @@ int sph_host_layout(const sph_format* fmt, int64_t n, int64_t k, uint64_t off[8]
   p = align_up(p + sph_table_bytes(kind, fmt->dir_bits), SPH_ALIGN);
   off[SPH_OFF_CODEBOOK] = p;
   p = align_up(p + ((uint64_t)16 << fmt->dir_bits), SPH_ALIGN);
+  off[SPH_OFF_C] = p;
+  p = align_up(p + nt * nv * 2 * sph_c_halves(kind), SPH_ALIGN);
   *total = p;
   return SPH_OK;
 }
@@ -86,6 +88,8 @@ void sph_host_pack(const sph_format* fmt, int64_t n, int64_t k, const uint8_t* s
   uint32_t* A = (uint32_t*)(blob + off[SPH_OFF_A]);
   uint32_t* B = (uint32_t*)(blob + off[SPH_OFF_B]);
   uint32_t* P = (uint32_t*)(blob + off[SPH_OFF_PARAMS]);
+  uint16_t* Cs = (uint16_t*)(blob + off[SPH_OFF_C]);
+  const int W = 8 + D;                       // field width of kind W2
 
   for (int64_t t = 0; t < nt; ++t) {
     for (int64_t v = 0; v < nv; ++v) {
@@ -108,9 +112,9 @@ void sph_host_pack(const sph_format* fmt, int64_t n, int64_t k, const uint8_t* s
           for (int i = 0; i < 8; ++i) {
             const Code& e = c[2 * i];
             const Code& o = c[2 * i + 1];
-            const uint32_t fe = (e.s & 15) | (e.z << 4) | ((e.s >> 4) << 10);
-            const uint32_t fo = (o.s & 15) | (o.z << 4) | ((o.s >> 4) << 10);
-            a[i] = fe | (fo << 14) | (e.q << 28);
+            const uint32_t fe = (e.s & 15) | (e.z << 4) | ((e.s >> 4) << (4 + D));
+            const uint32_t fo = (o.s & 15) | (o.z << 4) | ((o.s >> 4) << (4 + D));
+            a[i] = fe | (fo << W) | (e.q << (2 * W));
             b[0] |= o.q << (4 * i);
           }
           break;
@@ -127,12 +131,24 @@ void sph_host_pack(const sph_format* fmt, int64_t n, int64_t k, const uint8_t* s
             b[r / 4] |= (c[r].q & 0xFF) << (8 * (r % 4));
           }
           break;
-        case SPH_KIND_CB13:
+        case SPH_KIND_NIB16Q2:
           for (int r = 0; r < 16; ++r) {
-            a[r / 4] |= (c[r].s & 0xFF) << (8 * (r % 4));
-            b[r / 2] |= ((c[r].z & 0x1FFF) | (c[r].q << 13)) << (16 * (r % 2));
+            const uint32_t f = (c[r].s & 15) | (c[r].z << 4) | ((c[r].s >> 4) << 12);
+            a[r / 2] |= (f & 0xFFFF) << (16 * (r % 2));
+            b[0] |= (c[r].q & 3) << (2 * r);
           }
           break;
+        case SPH_KIND_CB13:
+        case SPH_KIND_CB13Q4: {
+          uint32_t hi = 0;
+          for (int r = 0; r < 16; ++r) {
+            a[r / 4] |= (c[r].s & 0xFF) << (8 * (r % 4));
+            b[r / 2] |= ((c[r].z & 0x1FFF) | ((c[r].q & 7) << 13)) << (16 * (r % 2));
+            hi |= ((c[r].q >> 3) & 1) << r;
+          }
+          if (kind == SPH_KIND_CB13Q4) Cs[t * nv + v] = (uint16_t)hi;
+          break;
+        }
       }
     }
     for (int64_t g = 0; g < ng; ++g)
@@ -147,7 +163,7 @@ void sph_host_pack(const sph_format* fmt, int64_t n, int64_t k, const uint8_t* s
   // Lookup tables derived from the codebook.
   uint16_t* T = (uint16_t*)(blob + off[SPH_OFF_TABLES]);
   const uint32_t entries = 1u << D;
-  if (kind == SPH_KIND_CB13) {
+  if (sph_is_codebook_kind(kind)) {
     for (uint32_t z = 0; z < entries; ++z)
       for (int j = 0; j < 8; ++j) T[z * 8 + j] = codebook[z * 8 + j];
   } else {

@@ -39,6 +39,9 @@ FORMATS = {
     "W3_cfg": (8, 8),   # 8 sign + 8-bit direction + 8-bit radius (24 bits per vector)
     "W2_16": (6, 2),    # 8 sign + 6-bit direction + 2-bit radius (2.00 bpw payload)
     "W3_25": (13, 4),   # 8 sign + 13-bit direction + 4-bit radius (3.125 bpw payload)
+    "W2_63": (6, 3),    # bit-allocation splits of the W2 budget: 8 sign + 6 direction + 3 radius,
+    "W2_72": (7, 2),    # 8 + 7 + 2,
+    "W2_82": (8, 2),    # 8 + 8 + 2
 }
 
 

@@ -46,8 +46,9 @@ def test_status_strings():
 
 @needs_lib
 @pytest.mark.parametrize("d,v,ok", [(6, 4, True), (13, 3, True), (4, 4, True), (8, 8, True),
-                                    (6, 2, True), (5, 3, True), (6, 3, False), (13, 4, False),
-                                    (2, 4, False), (16, 4, False)])
+                                    (6, 2, True), (5, 3, True), (6, 3, True), (7, 2, True),
+                                    (8, 2, True), (13, 4, True), (7, 3, False), (8, 4, False),
+                                    (13, 5, False), (2, 4, False), (16, 4, False)])
 def test_format_supported(d, v, ok):
     assert pkg.format_supported(d, v) == ok
 
@@ -63,6 +64,18 @@ def test_packed_bytes_accounts_for_every_stream():
     assert codes + params + tables <= got <= codes + params + tables + 5 * 256
     # padding to 16-row tiles
     assert pkg.packed_bytes(6, 4, 17, 128) == pkg.packed_bytes(6, 4, 32, 128)
+
+
+@needs_lib
+def test_packed_bytes_w3_four_radius_bits():
+    # 8 sign + 13 direction + 4 radius bits: sign bytes and (z | low 3 bits of q) words as for 3
+    # radius bits, plus one 16-bit word of high radius bits per record.
+    n, k = 4096, 12288
+    got = pkg.packed_bytes(13, 4, n, k)
+    codes = (n // 16) * (k // 8) * (16 + 32 + 2)
+    params = n * (k // 128) * 4
+    tables = (16 << 13) * 2                     # codebook table + raw codebook
+    assert codes + params + tables <= got <= codes + params + tables + 6 * 256
 
 
 @needs_lib

@@ -24,7 +24,7 @@ import paper_2609_24875_amd as pkg  # noqa: E402
 
 DEV = torch.device("cuda:0")
 TOL = 2e-3
-FMTS = ["W2", "W3", "W2_cfg", "W3_cfg", "W2_16"]
+FMTS = ["W2", "W3", "W2_cfg", "W3_cfg", "W2_16", "W3_25", "W2_63", "W2_72", "W2_82"]
 
 
 def to_dev_f16(bits: np.ndarray):

@@ -177,6 +177,54 @@ def encode(w, codebook_bits, radius_bits: int, params=None) -> dict:
             "gmin": gmin, "gstep": gstep}
 
 
+# ------------------------------------------- codebook initialisation (Sec. 3.1, Sec. 4.1)
+
+def sample_by_squared_radius(r, u) -> np.ndarray:
+    """Sec. 3.1: vector indices drawn with probability proportional to r_i^2, by the inverse of
+    the cumulative distribution: sample j takes the first i whose running sum of r^2 exceeds
+    u_j * (total r^2). The uniforms u_j in [0, 1) are drawn by the caller. Readings: with
+    replacement; the running sum is in storage order of the vectors (row-major)."""
+    r2 = np.asarray(r, dtype=np.float64).reshape(-1) ** 2
+    cdf = np.cumsum(r2)
+    idx = np.searchsorted(cdf, np.asarray(u, dtype=np.float64) * cdf[-1], side="right")
+    return np.minimum(idx, r2.size - 1)
+
+
+def spherical_kmeans(d, init_bits, iters: int):
+    """Spherical k-means on unit directions d [N, 8] from the fp16 codebook ``init_bits``
+    (Sec. 3.1, App. A step 6). Each iteration assigns every direction to its nearest centre by
+    cosine (Eq. 5, ties to the lowest index) and moves each centre to the normalised sum of its
+    directions, the unit vector with the largest summed cosine to them; a centre with no
+    directions stays where it is (reading). Returns the centres (fp64) and the objective, the
+    summed cosine of each iteration's assignment and finally of the returned centres."""
+    c = f16_to_f64(init_bits)
+    d = np.asarray(d, dtype=np.float64).reshape(-1, VEC)
+    obj = []
+    for _ in range(iters):
+        z = assign_directions(d, c)
+        obj.append(float(np.sum(np.sum(d * c[z], axis=1))))
+        s = np.zeros_like(c)
+        np.add.at(s, z, d)
+        norm = np.linalg.norm(s, axis=1)
+        c = np.where(norm[:, None] > 0, s / np.where(norm > 0, norm, 1.0)[:, None], c)
+    z = assign_directions(d, c)
+    obj.append(float(np.sum(np.sum(d * c[z], axis=1))))
+    return c, obj
+
+
+def kmeans_codebook(w, init_bits, u, iters: int = 20):
+    """Radius-weighted spherical k-means codebook of a weight matrix W[n][k] (Sec. 3.1; Sec. 4.1
+    uses 65,536 samples and 20 iterations): Eq. 3 decomposition of the rows' 8-D vectors,
+    directions sampled by r^2 (one per uniform in ``u``), k-means from ``init_bits``. Returns the
+    fp16 codebook (reading: centres rounded to fp16 for storage) and the objective trace."""
+    w = np.asarray(w, dtype=np.float64)
+    n, k = w.shape
+    _neg, _wp, r, d = decompose(w.reshape(n, k // VEC, VEC))
+    idx = sample_by_squared_radius(r, u)
+    c, obj = spherical_kmeans(d.reshape(-1, VEC)[idx], init_bits, iters)
+    return f64_to_f16(c), obj
+
+
 # ---------------------------------------------------------------- decoder (Eq. 4 and 7)
 
 def sign_factors(signs) -> np.ndarray:

@@ -341,6 +341,79 @@ def pin_angular_codebook(o):
     assert np.allclose(o.angular_codebook(np.zeros(7)), np.eye(8)[0])
 
 
+def pin_sample_by_squared_radius(o):
+    """Sec. 3.1's r^2-proportional sampling: its definition on a tiny input (uniforms chosen away
+    from the cumulative boundaries), zero radii never drawn, equal radii give floor(u * N), and
+    drawn frequencies follow r^2 / sum r^2."""
+    r = np.array([0.0, 1.0, 2.0, 0.0, 3.0])                 # r^2 = 0, 1, 4, 0, 9; total 14
+    u = np.array([0.0, 0.5, 0.9, 1.5, 4.9, 5.1, 13.9]) / 14
+    assert np.array_equal(o.sample_by_squared_radius(r, u), [1, 1, 1, 2, 2, 4, 4])
+    one = np.zeros(50)
+    one[17] = 0.3
+    g = np.random.default_rng(53)
+    assert np.all(o.sample_by_squared_radius(one, g.random(200)) == 17)
+    n = 1000
+    uu = (np.arange(n) + 0.5) / n
+    assert np.array_equal(o.sample_by_squared_radius(np.full(n, 0.7), uu), np.arange(n))
+    rr = np.array([1.0, 2.0, 3.0, 4.0])
+    idx = o.sample_by_squared_radius(rr, g.random(200000))
+    freq = np.bincount(idx, minlength=4) / idx.size
+    p = rr**2 / np.sum(rr**2)
+    assert np.all(np.abs(freq - p) < 4 * np.sqrt(p * (1 - p) / idx.size))
+
+
+def pin_spherical_kmeans(o):
+    """Spherical k-means (Sec. 3.1): exact centres are a fixed point with the objective equal to
+    the sample count; one update moves a centre to the normalised sum of its two directions and
+    leaves centres without directions in place; on random data the centres stay on S^7_+, the
+    summed cosine never decreases, and no unit vector beats a centre on its own cluster."""
+    cb = exact_unit_codebook(16)
+    c0 = O.f16_to_f64(cb)
+    c, obj = o.spherical_kmeans(np.repeat(c0, 3, axis=0), cb, 3)
+    assert np.allclose(c, c0, atol=1e-15) and all(abs(v - 48) < 1e-12 for v in obj)
+    a = np.array([1.0, 0.2, 0, 0, 0, 0, 0, 0])
+    b = np.array([1.0, 0, 0.3, 0, 0, 0, 0, 0])
+    a, b = a / np.linalg.norm(a), b / np.linalg.norm(b)
+    c, _ = o.spherical_kmeans(np.stack([a, b]), cb, 1)
+    assert np.allclose(c[0], (a + b) / np.linalg.norm(a + b), atol=1e-15)
+    assert np.array_equal(c[1:], c0[1:])
+    g = np.random.default_rng(51)
+    d = np.abs(g.standard_normal((3000, 8)))
+    d /= np.linalg.norm(d, axis=1, keepdims=True)
+    cbr = synth.random_codebook(5, synth.rng(52))
+    c, obj = o.spherical_kmeans(d, cbr, 8)
+    assert np.all(c >= 0) and np.allclose(np.linalg.norm(c, axis=1), 1.0, atol=1e-12)
+    assert all(y >= x - 1e-9 for x, y in zip(obj, obj[1:]))
+    # one update from the fp16 start: each new centre beats random unit vectors on the
+    # directions that were assigned to it (the maximiser of the summed cosine)
+    c1, _ = o.spherical_kmeans(d, cbr, 1)
+    z0 = np.argmax(d @ O.f16_to_f64(cbr).T, axis=1)
+    v = np.abs(g.standard_normal((200, 8)))
+    v /= np.linalg.norm(v, axis=1, keepdims=True)
+    for kk in np.unique(z0)[:8]:
+        dk = d[z0 == kk]
+        best = np.sum(dk @ c1[kk])
+        assert np.all(np.sum(dk @ v.T, axis=0) <= best + 1e-9)
+
+
+def pin_kmeans_codebook(o):
+    """The codebook of a matrix whose vectors all point one way (any signs and radii): the centre
+    nearest that direction moves onto it (in fp16), every other centre stays, and the objective is
+    the sample count."""
+    g = np.random.default_rng(54)
+    dirn = np.abs(g.standard_normal(8))
+    dirn /= np.linalg.norm(dirn)
+    scale = g.uniform(0.5, 2.0, (32, 16, 1)) * np.where(g.random((32, 16, 8)) < 0.5, -1.0, 1.0)
+    w = (scale * dirn).reshape(32, 128)
+    cb = synth.random_codebook(6, synth.rng(55))
+    out, obj = o.kmeans_codebook(w, cb, g.random(500), iters=3)
+    k0 = int(np.argmax(O.f16_to_f64(cb) @ dirn))
+    assert np.array_equal(out[k0], O.f64_to_f16(dirn))
+    others = np.arange(64) != k0
+    assert np.array_equal(out[others], cb[others])
+    assert abs(obj[-1] - 500) < 1e-9
+
+
 def pin_rel_err(o):
     """The comparison metric: zero on equal inputs, scale invariant, floored by row RMS."""
     y = np.array([[1.0, -2.0, 0.0, 4.0]])
@@ -356,7 +429,8 @@ PINS = [pin_worked_radius, pin_spherical_roundtrip, pin_bit_budget, pin_decompos
         pin_assign, pin_ls_radius, pin_radius_quant, pin_decode_norm_and_sign,
         pin_decode_one_hot, pin_gemm_exact_rational, pin_gemm_special_cases,
         pin_encode_roundtrip_bruteforce, pin_encode_group_params_recovered, pin_w2_layout,
-        pin_angular_codebook, pin_rel_err]
+        pin_angular_codebook, pin_sample_by_squared_radius, pin_spherical_kmeans,
+        pin_kmeans_codebook, pin_rel_err]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
@@ -424,6 +498,42 @@ def _mut_gemm_x_transposed(codes, cb, x_bits, row_chunk=256):
     return xr @ w.T
 
 
+def _mut_sample_by_radius(r, u):
+    return O.sample_by_squared_radius(np.sqrt(np.abs(np.asarray(r, np.float64))), u)   # r, not r^2
+
+
+def _mut_kmeans_mean(d, init_bits, iters):
+    c = O.f16_to_f64(init_bits)
+    d = np.asarray(d, dtype=np.float64).reshape(-1, 8)
+    obj = []
+    for _ in range(iters):
+        z = O.assign_directions(d, c)
+        obj.append(float(np.sum(np.sum(d * c[z], axis=1))))
+        cnt = np.bincount(z, minlength=c.shape[0])
+        s = np.zeros_like(c)
+        np.add.at(s, z, d)
+        c = np.where(cnt[:, None] > 0, s / np.maximum(cnt, 1)[:, None], c)   # mean, not normalised
+    z = O.assign_directions(d, c)
+    obj.append(float(np.sum(np.sum(d * c[z], axis=1))))
+    return c, obj
+
+
+def _mut_kmeans_empty_zero(d, init_bits, iters):
+    c = O.f16_to_f64(init_bits)
+    d = np.asarray(d, dtype=np.float64).reshape(-1, 8)
+    obj = []
+    for _ in range(iters):
+        z = O.assign_directions(d, c)
+        obj.append(float(np.sum(np.sum(d * c[z], axis=1))))
+        s = np.zeros_like(c)
+        np.add.at(s, z, d)
+        norm = np.linalg.norm(s, axis=1)
+        c = s / np.where(norm > 0, norm, 1.0)[:, None]                       # empty -> zero centre
+    z = O.assign_directions(d, c)
+    obj.append(float(np.sum(np.sum(d * c[z], axis=1))))
+    return c, obj
+
+
 MUTANTS = {
     "sign_bit_order": dict(sign_factors=_mut_sign_order),
     "dropped_group_offset": dict(dequantize_radius=_mut_drop_min),
@@ -434,6 +544,9 @@ MUTANTS = {
     "aux_bits_swapped": dict(paper_pack_w2=_mut_aux_order),
     "assign_ties_last": dict(assign_directions=_mut_assign_last_tie),
     "gemm_activation_order": dict(gemm=_mut_gemm_x_transposed),
+    "sample_by_radius": dict(sample_by_squared_radius=_mut_sample_by_radius),
+    "kmeans_mean_not_normalised": dict(spherical_kmeans=_mut_kmeans_mean),
+    "kmeans_empty_centre_zero": dict(spherical_kmeans=_mut_kmeans_empty_zero),
 }
 
 
@@ -471,6 +584,16 @@ def _rebind(ns):
             x = x[None, :]
         return x @ ns.decode(codes, cb).T
 
+    def kmeans_codebook(w, init_bits, u, iters=20):
+        w = np.asarray(w, dtype=np.float64)
+        n, k = w.shape
+        _neg, _wp, r, d = ns.decompose(w.reshape(n, k // 8, 8))
+        idx = ns.sample_by_squared_radius(r, u)
+        c, obj = ns.spherical_kmeans(d.reshape(-1, 8)[idx], init_bits, iters)
+        return O.f64_to_f16(c), obj
+
+    if ns.kmeans_codebook is O.kmeans_codebook:
+        ns.kmeans_codebook = kmeans_codebook
     if ns.decode is O.decode:
         ns.decode = decode
     if ns.encode is O.encode:

@@ -132,6 +132,52 @@ sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes);
 sph_status sph_unpack(const sph_weights* w, uint8_t* d_signs, uint16_t* d_dir_idx,
                       uint8_t* d_radius_code, void* stream);
 
+/* Spherical quantisation of a dense matrix on the device (Sec. 3.1: Eq. 3 decomposition into signs,
+ * radius and unit direction, Eq. 5 nearest direction by cosine, Eq. 6 least-squares radius
+ * <|w|, c_z>, Eq. 7 per-group offset min_G, step (max_G - min_G)/(2^V - 1) and level
+ * q = clip(round((r~ - min_G)/step_G), 0, 2^V - 1) with the offset and step as stored in fp16).
+ * d_w: device fp32[n][ldw] (ldw >= k, ldw % 4 == 0, 16-byte aligned); d_codebook: device
+ * fp16 bits [2^D][8]. Outputs are caller-owned device arrays in the layout sph_pack_weights reads:
+ * d_signs uint8[n][k/8], d_dir_idx uint16[n][k/8], d_radius_code uint8[n][k/8],
+ * d_group_min / d_group_step fp16 bits [n][k/128]. Arithmetic is fp64. Decisions: a coordinate is
+ * negative when w < 0 (so -0 is positive); among equal cosines the lowest index wins; a radius of
+ * zero divides by 1e-12 instead; rounding is to nearest, ties to even, for the level and for the
+ * fp16 offset and step; a zero step gives level 0. The codebook is not validated here (a
+ * non-finite or negative entry gives unspecified codes; sph_pack_weights rejects it later), and
+ * non-finite weights give unspecified codes. Offsets or steps beyond the fp16 range become
+ * infinite, which sph_pack_weights rejects. Asynchronous on `stream`; the result does not depend
+ * on the launch or on earlier calls. */
+sph_status sph_encode(const sph_format* fmt, int64_t n, int64_t k, const float* d_w, int64_t ldw,
+                      const uint16_t* d_codebook, uint8_t* d_signs, uint16_t* d_dir_idx,
+                      uint8_t* d_radius_code, uint16_t* d_group_min, uint16_t* d_group_step,
+                      void* stream);
+
+/* Device workspace needed by sph_kmeans_codebook for an n x k matrix and n_samples samples
+ * (1 <= n_samples <= 2^24): 8 bytes per 8-D vector of the matrix for the running sum of squared
+ * radii, 68 bytes per sample, and 64 bytes per codebook entry times the number of sample chunks
+ * (about 64 K entry-chunk pairs), plus alignment. */
+sph_status sph_kmeans_workspace_bytes(const sph_format* fmt, int64_t n, int64_t k, int64_t n_samples,
+                                      size_t* bytes);
+
+/* Radius-weighted spherical k-means codebook of a matrix (Sec. 3.1; Sec. 4.1 uses 65,536 samples
+ * and 20 iterations). The matrix's 8-D vectors are decomposed as in sph_encode; sample j draws the
+ * first vector (in row-major order) whose running sum of r^2 exceeds d_u[j] * (total r^2), so
+ * vectors are drawn with replacement with probability r^2 / sum r^2; d_u is device fp64[n_samples]
+ * of uniforms in [0, 1), drawn by the caller. Starting from the centres d_init (device fp16 bits
+ * [2^D][8]), each of `iters` iterations assigns every sampled unit direction to its nearest centre
+ * by cosine (lowest index among equals) and moves each centre to the normalised sum of its
+ * directions; a centre without directions stays. d_codebook (device fp16 bits [2^D][8]) receives
+ * the final centres rounded to nearest fp16. d_objective (device fp64[iters + 1], or NULL) receives
+ * the summed cosine of each iteration's assignment and, last, of the final centres.
+ * d_sample_idx (device int64[n_samples], or NULL) receives the drawn vector indices (row * k/8 +
+ * vector). d_ws: workspace of sph_kmeans_workspace_bytes, 256-byte aligned, no initial contents;
+ * concurrent calls must not share one. iters is 0..10000. fp64 arithmetic; every sum runs in a
+ * fixed order, so repeated calls give bitwise identical results. Asynchronous on `stream`. */
+sph_status sph_kmeans_codebook(const sph_format* fmt, int64_t n, int64_t k, const float* d_w, int64_t ldw,
+                               const double* d_u, int64_t n_samples, int32_t iters,
+                               const uint16_t* d_init, uint16_t* d_codebook, double* d_objective,
+                               int64_t* d_sample_idx, void* d_ws, size_t ws_bytes, void* stream);
+
 /* Whether (dir_bits, radius_bits) is one of the built-in formats: 1 yes, 0 no. */
 int sph_format_supported(const sph_format* fmt);
 

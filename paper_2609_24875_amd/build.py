@@ -8,7 +8,8 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = [os.path.join(CSRC, "sph_kernels.hip"), os.path.join(CSRC, "sph_pack.cpp")]
+SOURCES = [os.path.join(CSRC, "sph_kernels.hip"), os.path.join(CSRC, "sph_encode.hip"),
+           os.path.join(CSRC, "sph_pack.cpp")]
 OUT = os.path.join(HERE, "libsph.so")
 
 HIPCC_FLAGS = [

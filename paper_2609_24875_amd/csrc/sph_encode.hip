@@ -1,0 +1,574 @@
+// Spherical encoder and codebook initialisation on the device (Sec. 3.1, Eq. 3 and 5-7;
+// Sec. 4.1 for the k-means settings).
+//
+// All arithmetic is fp64 on the vector ALUs, from fp32 weights, so that each integer decision (a
+// direction index, a radius level, a sampled vector) is taken in the same precision as in a plain
+// fp64 implementation of the equations. Sums whose order fixes the bits of a stored value (the
+// squared radius, the least-squares radius of Eq. 6, the norm of a k-means centre) use the
+// pairwise order ((p0+p1)+(p2+p3))+((p4+p5)+(p6+p7)) with the products rounded first, never
+// fused. Every reduction runs in a fixed order, so repeated calls give bitwise identical results.
+//
+// Work layout:
+//   encoder      one thread per 8-D vector (four per thread), 16 neighbouring lanes form one
+//                128-weight group; the codebook is staged in LDS as fp64 in 512-entry chunks and
+//                read by broadcast.
+//   k-means      squared radii and their running sum (three-pass scan), inverse-CDF sampling by
+//                binary search, then per iteration: assignment (as in the encoder), per-centre
+//                partial sums over fixed sample chunks in sample order, and one workgroup per
+//                centre summing those partials in a fixed order and renormalising.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "sph_host.h"
+#include "sph_layout.h"
+
+namespace {
+
+constexpr double kEps = 1e-12;  // Eq. 3's guard against a zero radius
+constexpr int kThreads = 256;
+constexpr int kVpt = 4;          // vectors (or samples) per thread in the assignment kernels
+constexpr int kChunk = 512;      // codebook entries per LDS pass: 32 KiB of fp64
+constexpr int kScanItems = 8;    // vectors per thread in the radius scan
+constexpr int kScanBlock = kThreads * kScanItems;
+constexpr int kPartialThreads = 64;
+constexpr int64_t kPartialTarget = 65536;  // centre x chunk pairs per partial-sum launch
+
+__device__ __forceinline__ double h2d(uint16_t b) { return (double)(float)__builtin_bit_cast(_Float16, b); }
+
+// fp64 -> fp16 bits, round to nearest with ties to even, from the two formats' definitions:
+// binary16 normals keep 11 significant bits, subnormals count units of 2^-24, and magnitudes
+// that round beyond 65504 become infinity.
+__device__ uint16_t d2h(double x) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, x);
+  const uint16_t sign = (uint16_t)((b >> 48) & 0x8000u);
+  const uint64_t a = b & 0x7FFFFFFFFFFFFFFFull;
+  if (a >= 0x7FF0000000000000ull) return sign | (a == 0x7FF0000000000000ull ? 0x7C00u : 0x7E00u);
+  const int e = (int)(a >> 52) - 1023;
+  if (e > 15) return sign | 0x7C00u;
+  if (e < -25) return sign;  // below half of the smallest subnormal (2^-24)
+  const uint64_t m = (a & 0xFFFFFFFFFFFFFull) | 0x10000000000000ull;
+  const int shift = e >= -14 ? 42 : 28 - e;
+  uint64_t q = m >> shift;
+  const uint64_t rem = m & ((1ull << shift) - 1), half = 1ull << (shift - 1);
+  if (rem > half || (rem == half && (q & 1))) ++q;
+  if (e < -14) return sign | (uint16_t)q;  // q == 1024 encodes the smallest normal
+  int ee = e;
+  if (q == 2048) {
+    q = 1024;
+    ++ee;
+  }
+  if (ee > 15) return sign | 0x7C00u;
+  return sign | (uint16_t)((ee + 15) << 10) | (uint16_t)(q - 1024);
+}
+
+// Pairwise sum of the eight rounded products a[j] * b[j].
+__device__ __forceinline__ double dot8_pairwise(const double* a, const double* b) {
+#pragma clang fp contract(off)
+  double p[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) p[j] = a[j] * b[j];
+  return ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+}
+
+// Eq. 3 on one fp32 vector: magnitudes |w_j| (w_+), sign bits (set where w_j < 0) and the
+// unit direction w_+ / max(||w||, eps). Returns the radius.
+__device__ __forceinline__ double decompose(const float* __restrict__ w, int64_t ldw, int64_t nv, int64_t i,
+                                            double a[8], double d[8], uint32_t& neg) {
+#pragma clang fp contract(off)
+  const int64_t row = i / nv, v = i - row * nv;
+  const float4* p = reinterpret_cast<const float4*>(w + row * ldw + v * 8);
+  const float4 x0 = p[0], x1 = p[1];
+  const float f[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+  neg = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    neg |= (f[j] < 0.0f ? 1u : 0u) << j;
+    a[j] = fabs((double)f[j]);
+  }
+  const double r = sqrt(dot8_pairwise(a, a));
+  const double rr = r < kEps ? kEps : r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) d[j] = a[j] / rr;
+  return r;
+}
+
+// Eq. 5 over entries [base, base + cnt) of a codebook held in LDS (fp64, 8 per entry): strict
+// comparison in ascending index order keeps the lowest index among equal cosines.
+__device__ __forceinline__ void argmax_chunk(const double* __restrict__ cl, int cnt, int base,
+                                             const double (&d)[kVpt][8], double (&best)[kVpt],
+                                             int (&bz)[kVpt]) {
+  for (int e = 0; e < cnt; ++e) {
+    const double2* ce2 = reinterpret_cast<const double2*>(cl + e * 8);
+    const double2 c01 = ce2[0], c23 = ce2[1], c45 = ce2[2], c67 = ce2[3];
+    const double c[8] = {c01.x, c01.y, c23.x, c23.y, c45.x, c45.y, c67.x, c67.y};
+#pragma unroll
+    for (int u = 0; u < kVpt; ++u) {
+      double s = d[u][0] * c[0];
+#pragma unroll
+      for (int j = 1; j < 8; ++j) s = fma(d[u][j], c[j], s);
+      if (s > best[u]) {
+        best[u] = s;
+        bz[u] = base + e;
+      }
+    }
+  }
+}
+
+// Stage the codebook chunk by chunk into LDS and run the argmax over it. The source is either the
+// fp16 codebook or fp64 centres. Every thread of the block must call this.
+template <typename T>
+__device__ __forceinline__ void argmax_codebook(const T* __restrict__ src, int ncb, double* cl,
+                                                const double (&d)[kVpt][8], double (&best)[kVpt],
+                                                int (&bz)[kVpt]) {
+  for (int base = 0; base < ncb; base += kChunk) {
+    const int cnt = min(kChunk, ncb - base);
+    __syncthreads();
+    for (int t = threadIdx.x; t < cnt * 8; t += kThreads) {
+      if constexpr (sizeof(T) == 2)
+        cl[t] = h2d(src[(int64_t)base * 8 + t]);
+      else
+        cl[t] = src[(int64_t)base * 8 + t];
+    }
+    __syncthreads();
+    argmax_chunk(cl, cnt, base, d, best, bz);
+  }
+}
+
+// ------------------------------------------------------------------------------------ encoder
+
+struct EncArgs {
+  const float* w;
+  int64_t ldw, nv, nvec;
+  const uint16_t* cb;
+  int ncb, vmax;
+  uint8_t* signs;
+  uint16_t* dir;
+  uint8_t* q;
+  uint16_t* gmin;
+  uint16_t* gstep;
+};
+
+// Eq. 3, 5, 6 and 7 for kVpt * 256 consecutive vectors. Groups of 16 vectors never straddle a
+// row (k is a multiple of 128) and start at multiples of 16 in the flat vector index, so each
+// group is 16 aligned lanes of one wave, all inside or all outside [0, nvec).
+__global__ __launch_bounds__(kThreads) void k_encode(EncArgs a) {
+  __shared__ double cl[kChunk * 8];
+  const int64_t blk = (int64_t)blockIdx.x * kThreads * kVpt;
+  double d[kVpt][8], best[kVpt];
+  int bz[kVpt];
+#pragma unroll
+  for (int u = 0; u < kVpt; ++u) {
+    const int64_t i = blk + u * kThreads + threadIdx.x;
+    best[u] = -INFINITY;
+    bz[u] = 0;
+    double av[8];
+    uint32_t neg;
+    if (i < a.nvec) {
+      decompose(a.w, a.ldw, a.nv, i, av, d[u], neg);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) d[u][j] = 0.0;
+    }
+  }
+  argmax_codebook(a.cb, a.ncb, cl, d, best, bz);
+#pragma unroll
+  for (int u = 0; u < kVpt; ++u) {
+    const int64_t i = blk + u * kThreads + threadIdx.x;
+    // the magnitudes and signs are read again rather than kept live across the argmax
+    double av[8] = {0, 0, 0, 0, 0, 0, 0, 0}, dd[8];
+    uint32_t neg = 0;
+    if (i < a.nvec) decompose(a.w, a.ldw, a.nv, i, av, dd, neg);
+    double c[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) c[j] = h2d(a.cb[(int64_t)bz[u] * 8 + j]);
+    const double rt = dot8_pairwise(av, c);  // Eq. 6
+    double lo = rt, hi = rt;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      lo = fmin(lo, __shfl_xor(lo, o, 16));
+      hi = fmax(hi, __shfl_xor(hi, o, 16));
+    }
+    const uint16_t lo16 = d2h(lo), st16 = d2h((hi - lo) / (double)a.vmax);
+    const double lod = h2d(lo16), std_ = h2d(st16);
+    int q = 0;
+    if (std_ > 0.0) {
+      const double t = rint((rt - lod) / std_);
+      q = (int)fmin(fmax(t, 0.0), (double)a.vmax);
+    }
+    if (i < a.nvec) {
+      a.signs[i] = (uint8_t)neg;
+      a.dir[i] = (uint16_t)bz[u];
+      a.q[i] = (uint8_t)q;
+      if ((threadIdx.x & 15) == 0) {
+        a.gmin[i >> 4] = lo16;
+        a.gstep[i >> 4] = st16;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------ k-means
+
+// Block-wide exclusive prefix of one value per thread, in a fixed order; also returns the block
+// total. `sh` holds kThreads doubles.
+__device__ __forceinline__ double block_exclusive(double v, double* sh, double& total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  double incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double t = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += t;
+  }
+  if (lane == 63) sh[wv] = incl;
+  __syncthreads();
+  double woff = 0.0;
+  for (int k = 0; k < wv; ++k) woff += sh[k];
+  double tot = 0.0;
+  for (int k = 0; k < kThreads / 64; ++k) tot += sh[k];
+  __syncthreads();
+  total = tot;
+  return woff + (incl - v);
+}
+
+// Squared radius r^2 of every vector (r from Eq. 3), stored in cdf[], and each block's total.
+__global__ __launch_bounds__(kThreads) void k_r2(const float* __restrict__ w, int64_t ldw, int64_t nv,
+                                                 int64_t nvec, double* __restrict__ cdf,
+                                                 double* __restrict__ bsum) {
+  __shared__ double sh[kThreads / 64];
+  const int64_t i0 = (int64_t)blockIdx.x * kScanBlock + (int64_t)threadIdx.x * kScanItems;
+  double s = 0.0;
+  for (int j = 0; j < kScanItems; ++j) {
+    const int64_t i = i0 + j;
+    if (i >= nvec) break;
+    double av[8], d[8];
+    uint32_t neg;
+    const double r = decompose(w, ldw, nv, i, av, d, neg);
+    const double r2 = r * r;
+    cdf[i] = r2;
+    s += r2;
+  }
+  double total;
+  block_exclusive(s, sh, total);
+  if (threadIdx.x == 0) bsum[blockIdx.x] = total;
+}
+
+// Exclusive running sum of the nb block totals, in place, by one block.
+__global__ __launch_bounds__(kThreads) void k_scan_blocks(double* __restrict__ bsum, int64_t nb) {
+  __shared__ double sh[kThreads / 64];
+  const int64_t per = (nb + kThreads - 1) / kThreads;
+  const int64_t b0 = (int64_t)threadIdx.x * per, b1 = min(nb, b0 + per);
+  double s = 0.0;
+  for (int64_t b = b0; b < b1; ++b) s += bsum[b];
+  double total;
+  double run = block_exclusive(s, sh, total);
+  for (int64_t b = b0; b < b1; ++b) {
+    const double v = bsum[b];
+    bsum[b] = run;
+    run += v;
+  }
+}
+
+// Running sum of r^2 in storage order: cdf[i] = sum of r^2 over vectors 0..i.
+__global__ __launch_bounds__(kThreads) void k_scan_apply(double* __restrict__ cdf, const double* __restrict__ boff,
+                                                         int64_t nvec) {
+  __shared__ double sh[kThreads / 64];
+  const int64_t i0 = (int64_t)blockIdx.x * kScanBlock + (int64_t)threadIdx.x * kScanItems;
+  double v[kScanItems];
+  double s = 0.0;
+  for (int j = 0; j < kScanItems; ++j) {
+    const int64_t i = i0 + j;
+    v[j] = i < nvec ? cdf[i] : 0.0;
+    s += v[j];
+  }
+  double total;
+  const double off = boff[blockIdx.x] + block_exclusive(s, sh, total);
+  double run = 0.0;
+  for (int j = 0; j < kScanItems; ++j) {
+    const int64_t i = i0 + j;
+    run += v[j];
+    if (i < nvec) cdf[i] = off + run;
+  }
+}
+
+// Inverse-CDF draw (Sec. 3.1): sample j takes the first vector whose running r^2 exceeds
+// u_j * total, clamped to the last vector; its unit direction goes to ds[j][0..8).
+__global__ __launch_bounds__(kThreads) void k_sample(const float* __restrict__ w, int64_t ldw, int64_t nv,
+                                                     int64_t nvec, const double* __restrict__ cdf,
+                                                     const double* __restrict__ u, int64_t ns,
+                                                     double* __restrict__ ds, int64_t* __restrict__ sidx) {
+  const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (j >= ns) return;
+  const double target = u[j] * cdf[nvec - 1];
+  int64_t lo = 0, hi = nvec;
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo) / 2;
+    if (cdf[mid] > target)
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  const int64_t idx = lo < nvec ? lo : nvec - 1;
+  if (sidx) sidx[j] = idx;
+  double av[8], d[8];
+  uint32_t neg;
+  decompose(w, ldw, nv, idx, av, d, neg);
+#pragma unroll
+  for (int c = 0; c < 8; ++c) ds[j * 8 + c] = d[c];
+}
+
+__global__ __launch_bounds__(kThreads) void k_init_centres(const uint16_t* __restrict__ init, int64_t count,
+                                                           double* __restrict__ cen) {
+  const int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (t < count) cen[t] = h2d(init[t]);
+}
+
+// Eq. 5 for every sample against the current centres; z[j] gets the nearest centre and each
+// block writes the sum of the samples' cosines to their centre (summed per sample in pairwise
+// order, then in a fixed order over the block).
+__global__ __launch_bounds__(kThreads) void k_assign(const double* __restrict__ ds, int64_t ns,
+                                                     const double* __restrict__ cen, int ncb,
+                                                     int32_t* __restrict__ z, double* __restrict__ opart) {
+  __shared__ double cl[kChunk * 8];
+  __shared__ double sh[kThreads / 64];
+  const int64_t blk = (int64_t)blockIdx.x * kThreads * kVpt;
+  double d[kVpt][8], best[kVpt];
+  int bz[kVpt];
+#pragma unroll
+  for (int u = 0; u < kVpt; ++u) {
+    const int64_t j = blk + u * kThreads + threadIdx.x;
+    best[u] = -INFINITY;
+    bz[u] = 0;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) d[u][c] = j < ns ? ds[j * 8 + c] : 0.0;
+  }
+  argmax_codebook(cen, ncb, cl, d, best, bz);
+  double s = 0.0;
+#pragma unroll
+  for (int u = 0; u < kVpt; ++u) {
+    const int64_t j = blk + u * kThreads + threadIdx.x;
+    if (j < ns) {
+      z[j] = bz[u];
+      s += dot8_pairwise(d[u], cen + (int64_t)bz[u] * 8);
+    }
+  }
+  double total;
+  block_exclusive(s, sh, total);
+  if (threadIdx.x == 0) opart[blockIdx.x] = total;
+}
+
+// Objective of one assignment: the blocks' sums added in block order.
+__global__ __launch_bounds__(64) void k_objective(const double* __restrict__ opart, int64_t nblk,
+                                                  double* __restrict__ out) {
+  if (threadIdx.x != 0) return;
+  double s = 0.0;
+  for (int64_t b = 0; b < nblk; ++b) s += opart[b];
+  *out = s;
+}
+
+// Sum of the directions assigned to centre c among samples [p*ch, (p+1)*ch), in sample order.
+__global__ __launch_bounds__(kPartialThreads) void k_partial(const double* __restrict__ ds, int64_t ns,
+                                                             const int32_t* __restrict__ z, int ncb,
+                                                             int64_t ch, int np, double* __restrict__ part) {
+  const int c = blockIdx.x * kPartialThreads + threadIdx.x;
+  const int p = blockIdx.y;
+  const int64_t j0 = (int64_t)p * ch, j1 = min(ns, j0 + ch);
+  double s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int64_t j = j0; j < j1; ++j) {
+    if (z[j] == c) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s[e] += ds[j * 8 + e];
+    }
+  }
+  if (c < ncb) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[((int64_t)c * np + p) * 8 + e] = s[e];
+  }
+}
+
+// New centre c: the chunk partials summed in a fixed order (lane-strided, then a fixed lane
+// tree), normalised to unit length; a centre without directions keeps its position.
+__global__ __launch_bounds__(64) void k_update(const double* __restrict__ part, int np,
+                                               double* __restrict__ cen) {
+#pragma clang fp contract(off)
+  const int c = blockIdx.x;
+  const int lane = threadIdx.x;
+  double s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int p = lane; p < np; p += 64) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] += part[((int64_t)c * np + p) * 8 + e];
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] += __shfl_xor(s[e], o, 64);
+  }
+  if (lane == 0) {
+    const double norm = sqrt(dot8_pairwise(s, s));
+    if (norm > 0.0) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) cen[(int64_t)c * 8 + e] = s[e] / norm;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_centres_to_f16(const double* __restrict__ cen, int64_t count,
+                                                             uint16_t* __restrict__ out) {
+  const int64_t t = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (t < count) out[t] = d2h(cen[t]);
+}
+
+// ------------------------------------------------------------------------------------ host side
+
+inline uint64_t align256(uint64_t x) { return (x + 255) / 256 * 256; }
+
+struct KmPlan {
+  int64_t nvec, nb, nab, ch;
+  int ncb, np;
+  uint64_t off_cdf, off_bsum, off_ds, off_z, off_opart, off_cen, off_part, total;
+};
+
+KmPlan km_plan(const sph_format* fmt, int64_t n, int64_t k, int64_t ns) {
+  KmPlan P{};
+  P.nvec = n * (k / SPH_VEC);
+  P.nb = (P.nvec + kScanBlock - 1) / kScanBlock;
+  P.nab = (ns + kThreads * kVpt - 1) / (kThreads * kVpt);
+  P.ncb = 1 << fmt->dir_bits;
+  int64_t np = kPartialTarget / P.ncb;
+  np = np < 1 ? 1 : np > ns ? ns : np;
+  P.ch = (ns + np - 1) / np;
+  P.np = (int)((ns + P.ch - 1) / P.ch);
+  uint64_t p = 0;
+  P.off_cdf = p;
+  p = align256(p + (uint64_t)P.nvec * 8);
+  P.off_bsum = p;
+  p = align256(p + (uint64_t)P.nb * 8);
+  P.off_ds = p;
+  p = align256(p + (uint64_t)ns * 64);
+  P.off_z = p;
+  p = align256(p + (uint64_t)ns * 4);
+  P.off_opart = p;
+  p = align256(p + (uint64_t)P.nab * 8);
+  P.off_cen = p;
+  p = align256(p + (uint64_t)P.ncb * 64);
+  P.off_part = p;
+  p = align256(p + (uint64_t)P.ncb * P.np * 64);
+  P.total = p;
+  return P;
+}
+
+constexpr int64_t kMaxSamples = int64_t(1) << 24;
+constexpr int32_t kMaxIters = 10000;
+
+int check_common(const sph_format* fmt, int64_t n, int64_t k, const float* d_w, int64_t ldw) {
+  int st = sph_host_check_format(fmt);
+  if (st) return st;
+  st = sph_host_check_shape(n, k);
+  if (st) return st;
+  if (!d_w) return SPH_ERR_NULL;
+  if (ldw < k || ldw % 4 != 0 || (uintptr_t)d_w % 16 != 0) return SPH_ERR_SHAPE;
+  return SPH_OK;
+}
+
+template <typename... A>
+bool launch_ok(const void* fn, dim3 grid, dim3 block, hipStream_t s, A... args) {
+  void* kargs[] = {(void*)&args...};
+  if (hipLaunchKernel(fn, grid, block, kargs, 0, s) != hipSuccess) return false;
+  return hipGetLastError() == hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+sph_status sph_encode(const sph_format* fmt, int64_t n, int64_t k, const float* d_w, int64_t ldw,
+                      const uint16_t* d_codebook, uint8_t* d_signs, uint16_t* d_dir_idx,
+                      uint8_t* d_radius_code, uint16_t* d_group_min, uint16_t* d_group_step,
+                      void* stream) {
+  if (!fmt || !d_codebook || !d_signs || !d_dir_idx || !d_radius_code || !d_group_min || !d_group_step)
+    return SPH_ERR_NULL;
+  const int st = check_common(fmt, n, k, d_w, ldw);
+  if (st) return (sph_status)st;
+  if ((uintptr_t)d_codebook % 2 || (uintptr_t)d_dir_idx % 2 || (uintptr_t)d_group_min % 2 ||
+      (uintptr_t)d_group_step % 2)
+    return SPH_ERR_SHAPE;
+  EncArgs a{};
+  a.w = d_w;
+  a.ldw = ldw;
+  a.nv = k / SPH_VEC;
+  a.nvec = n * a.nv;
+  a.cb = d_codebook;
+  a.ncb = 1 << fmt->dir_bits;
+  a.vmax = (1 << fmt->radius_bits) - 1;
+  a.signs = d_signs;
+  a.dir = d_dir_idx;
+  a.q = d_radius_code;
+  a.gmin = d_group_min;
+  a.gstep = d_group_step;
+  const int64_t grid = (a.nvec + kThreads * kVpt - 1) / (kThreads * kVpt);
+  if (!launch_ok((const void*)k_encode, dim3((unsigned)grid), dim3(kThreads), (hipStream_t)stream, a))
+    return SPH_ERR_HIP;
+  return SPH_OK;
+}
+
+sph_status sph_kmeans_workspace_bytes(const sph_format* fmt, int64_t n, int64_t k, int64_t n_samples,
+                                      size_t* bytes) {
+  if (!fmt || !bytes) return SPH_ERR_NULL;
+  int st = sph_host_check_format(fmt);
+  if (st) return (sph_status)st;
+  st = sph_host_check_shape(n, k);
+  if (st) return (sph_status)st;
+  if (n_samples < 1 || n_samples > kMaxSamples) return SPH_ERR_SHAPE;
+  *bytes = (size_t)km_plan(fmt, n, k, n_samples).total;
+  return SPH_OK;
+}
+
+sph_status sph_kmeans_codebook(const sph_format* fmt, int64_t n, int64_t k, const float* d_w, int64_t ldw,
+                               const double* d_u, int64_t n_samples, int32_t iters,
+                               const uint16_t* d_init, uint16_t* d_codebook, double* d_objective,
+                               int64_t* d_sample_idx, void* d_ws, size_t ws_bytes, void* stream) {
+  if (!fmt || !d_u || !d_init || !d_codebook || !d_ws) return SPH_ERR_NULL;
+  const int st = check_common(fmt, n, k, d_w, ldw);
+  if (st) return (sph_status)st;
+  if (n_samples < 1 || n_samples > kMaxSamples || iters < 0 || iters > kMaxIters) return SPH_ERR_SHAPE;
+  if ((uintptr_t)d_u % 8 || (uintptr_t)d_init % 2 || (uintptr_t)d_codebook % 2 ||
+      (uintptr_t)d_objective % 8 || (uintptr_t)d_sample_idx % 8 || (uintptr_t)d_ws % 256)
+    return SPH_ERR_SHAPE;
+  const KmPlan P = km_plan(fmt, n, k, n_samples);
+  if (ws_bytes < P.total) return SPH_ERR_BUFFER_TOO_SMALL;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)d_ws;
+  double* cdf = (double*)(ws + P.off_cdf);
+  double* bsum = (double*)(ws + P.off_bsum);
+  double* ds = (double*)(ws + P.off_ds);
+  int32_t* z = (int32_t*)(ws + P.off_z);
+  double* opart = (double*)(ws + P.off_opart);
+  double* cen = (double*)(ws + P.off_cen);
+  double* part = (double*)(ws + P.off_part);
+  const int64_t ns = n_samples, nv = k / SPH_VEC, ncb8 = (int64_t)P.ncb * 8;
+  const dim3 blk(kThreads);
+  const unsigned g_cb = (unsigned)((ncb8 + kThreads - 1) / kThreads);
+  const unsigned g_s = (unsigned)((ns + kThreads - 1) / kThreads);
+  bool ok = launch_ok((const void*)k_r2, dim3((unsigned)P.nb), blk, s, d_w, ldw, nv, P.nvec, cdf, bsum) &&
+            launch_ok((const void*)k_scan_blocks, dim3(1), blk, s, bsum, P.nb) &&
+            launch_ok((const void*)k_scan_apply, dim3((unsigned)P.nb), blk, s, cdf, (const double*)bsum, P.nvec) &&
+            launch_ok((const void*)k_sample, dim3(g_s), blk, s, d_w, ldw, nv, P.nvec, (const double*)cdf, d_u, ns,
+                      ds, d_sample_idx) &&
+            launch_ok((const void*)k_init_centres, dim3(g_cb), blk, s, d_init, ncb8, cen);
+  const dim3 g_part((unsigned)((P.ncb + kPartialThreads - 1) / kPartialThreads), (unsigned)P.np);
+  for (int32_t it = 0; ok && it <= iters; ++it) {
+    ok = launch_ok((const void*)k_assign, dim3((unsigned)P.nab), blk, s, (const double*)ds, ns,
+                   (const double*)cen, P.ncb, z, opart);
+    if (ok && d_objective)
+      ok = launch_ok((const void*)k_objective, dim3(1), dim3(64), s, (const double*)opart, P.nab,
+                     d_objective + it);
+    if (ok && it < iters)
+      ok = launch_ok((const void*)k_partial, g_part, dim3(kPartialThreads), s, (const double*)ds, ns,
+                     (const int32_t*)z, P.ncb, P.ch, P.np, part) &&
+           launch_ok((const void*)k_update, dim3((unsigned)P.ncb), dim3(64), s, (const double*)part, P.np, cen);
+  }
+  if (ok) ok = launch_ok((const void*)k_centres_to_f16, dim3(g_cb), blk, s, (const double*)cen, ncb8, d_codebook);
+  return ok ? SPH_OK : SPH_ERR_HIP;
+}
+
+}  // extern "C"

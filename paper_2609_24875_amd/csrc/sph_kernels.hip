@@ -968,7 +968,6 @@ int num_cus() {
   return c;
 }
 
-size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
 
 // Work plan. Vector-ALU path: one 16-wave workgroup per CU, every wave a contiguous range of

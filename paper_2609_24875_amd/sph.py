@@ -25,7 +25,8 @@ STATUS = {
 
 # Every symbol include/sph.h declares.
 EXPORTS = ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
-           "sph_workspace_bytes", "sph_unpack", "sph_format_supported", "sph_status_str")
+           "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
+           "sph_kmeans_codebook", "sph_format_supported", "sph_status_str")
 
 FORMATS = {
     "W2": (6, 4), "W3": (13, 3), "W2_cfg": (4, 4), "W3_cfg": (8, 8), "W2_16": (6, 2),
@@ -73,12 +74,17 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sph_gemm_small.argtypes = [pw, P, I64, I64, P, I64, I32, P, SZ, P]
     lib.sph_workspace_bytes.argtypes = [pw, I64, ctypes.POINTER(SZ)]
     lib.sph_unpack.argtypes = [pw, P, P, P, P]
+    lib.sph_encode.argtypes = [pf, I64, I64, P, I64, P, P, P, P, P, P, P]
+    lib.sph_kmeans_workspace_bytes.argtypes = [pf, I64, I64, I64, ctypes.POINTER(SZ)]
+    lib.sph_kmeans_codebook.argtypes = [pf, I64, I64, P, I64, P, I64, ctypes.c_int32, P, P, P, P,
+                                        P, SZ, P]
     lib.sph_format_supported.argtypes = [pf]
     lib.sph_format_supported.restype = I32
     lib.sph_status_str.argtypes = [I32]
     lib.sph_status_str.restype = ctypes.c_char_p
     for name in ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
-                 "sph_workspace_bytes", "sph_unpack"):
+                 "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
+                 "sph_kmeans_codebook"):
         getattr(lib, name).restype = I32
     _lib = lib
     return lib
@@ -227,3 +233,79 @@ def unpack(w: SphWeights, stream=None) -> dict:
     _check(st, "sph_unpack")
     torch.cuda.synchronize(dev)
     return {"signs": s.cpu().numpy(), "dir": d.cpu().numpy().view(np.uint16), "q": q.cpu().numpy()}
+
+
+def _dev_f32_matrix(w):
+    import torch
+    if w.dtype != torch.float32 or w.dim() != 2 or w.stride(1) != 1 or w.stride(0) % 4 != 0:
+        raise ValueError("w must be a device fp32 matrix with unit column stride and a row stride "
+                         "that is a multiple of 4")
+    return w
+
+
+def encode(dir_bits: int, radius_bits: int, w, codebook, stream=None) -> dict:
+    """Spherical quantisation of a device fp32 matrix w[n][k] against a device fp16-bit codebook
+    [2^D][8] (sph_encode). Returns device tensors: signs uint8, dir int16 (bits of uint16), q
+    uint8 ([n][k/8]), gmin, gstep int16 (fp16 bits, [n][k/128])."""
+    import torch
+    w = _dev_f32_matrix(w)
+    n, k = w.shape
+    dev = w.device
+    cb = codebook.contiguous()
+    out = {"signs": torch.empty((n, k // 8), dtype=torch.uint8, device=dev),
+           "dir": torch.empty((n, k // 8), dtype=torch.int16, device=dev),
+           "q": torch.empty((n, k // 8), dtype=torch.uint8, device=dev),
+           "gmin": torch.empty((n, k // 128), dtype=torch.int16, device=dev),
+           "gstep": torch.empty((n, k // 128), dtype=torch.int16, device=dev)}
+    st = load_library().sph_encode(ctypes.byref(make_format(dir_bits, radius_bits)), n, k,
+                                   w.data_ptr(), w.stride(0), cb.data_ptr(),
+                                   out["signs"].data_ptr(), out["dir"].data_ptr(),
+                                   out["q"].data_ptr(), out["gmin"].data_ptr(),
+                                   out["gstep"].data_ptr(), _stream_handle(stream))
+    _check(st, "sph_encode")
+    return out
+
+
+def codes_to_host(codes: dict) -> dict:
+    """Device codes from ``encode`` as numpy arrays with the dtypes ``pack`` takes."""
+    h = {key: v.cpu().numpy() for key, v in codes.items()}
+    for key in ("dir", "gmin", "gstep"):
+        h[key] = h[key].view(np.uint16)
+    return h
+
+
+def kmeans_workspace_bytes(dir_bits: int, radius_bits: int, n: int, k: int, n_samples: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().sph_kmeans_workspace_bytes(ctypes.byref(make_format(dir_bits, radius_bits)),
+                                                     n, k, n_samples, ctypes.byref(out)),
+           "sph_kmeans_workspace_bytes")
+    return out.value
+
+
+def kmeans_codebook(dir_bits: int, radius_bits: int, w, u, init, iters: int = 20, workspace=None,
+                    stream=None):
+    """Radius-weighted spherical k-means codebook of a device fp32 matrix w[n][k]
+    (sph_kmeans_codebook). ``u``: device fp64 uniforms, one per sample; ``init``: device fp16-bit
+    centres [2^D][8]. Returns (codebook int16 [2^D][8] of fp16 bits, objective fp64 [iters + 1],
+    sample indices int64 [len(u)]), all on the device."""
+    import torch
+    w = _dev_f32_matrix(w)
+    n, k = w.shape
+    dev = w.device
+    ns = u.numel()
+    if u.dtype != torch.float64:
+        raise ValueError("u must be fp64")
+    nb = kmeans_workspace_bytes(dir_bits, radius_bits, n, k, ns)
+    if workspace is None or workspace.numel() < nb:
+        workspace = torch.empty(nb, dtype=torch.uint8, device=dev)
+    cb = torch.empty((1 << dir_bits, 8), dtype=torch.int16, device=dev)
+    obj = torch.empty(iters + 1, dtype=torch.float64, device=dev)
+    idx = torch.empty(ns, dtype=torch.int64, device=dev)
+    init = init.contiguous()
+    u = u.contiguous()
+    st = load_library().sph_kmeans_codebook(
+        ctypes.byref(make_format(dir_bits, radius_bits)), n, k, w.data_ptr(), w.stride(0),
+        u.data_ptr(), ns, iters, init.data_ptr(), cb.data_ptr(), obj.data_ptr(), idx.data_ptr(),
+        workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
+    _check(st, "sph_kmeans_codebook")
+    return cb, obj, idx

@@ -152,3 +152,43 @@ def _load_fresh(path):
         return B.load_library(path)
     finally:
         B._lib = saved
+
+
+@needs_lib
+def test_encode_validation_errors_before_any_hip_call():
+    lib = pkg.load_library()
+    f = B.make_format(6, 4)
+    W, CB, S, D, Q, GM, GS = 0x10000, 0x20000, 0x30000, 0x40000, 0x50000, 0x60000, 0x70000
+
+    def st(fmt=f, n=16, k=128, w=W, ldw=128, cb=CB, s=S, d=D, q=Q, gm=GM, gs=GS):
+        return lib.sph_encode(ctypes.byref(fmt) if fmt is not None else None, n, k, w, ldw, cb,
+                              s, d, q, gm, gs, None)
+    assert st(fmt=None) == 1 and st(w=0) == 1 and st(cb=0) == 1 and st(gs=0) == 1
+    assert st(fmt=B.make_format(7, 4)) == 3 and st(fmt=B.make_format(6, 4, vec_dim=4)) == 3
+    assert st(k=100) == 2 and st(n=0) == 2
+    assert st(ldw=120) == 2 and st(ldw=130) == 2       # ldw < k, ldw not a multiple of 4
+    assert st(w=0x10008) == 2 and st(d=0x40001) == 2    # misaligned weights / direction indices
+
+
+@needs_lib
+def test_kmeans_workspace_and_validation():
+    lib = pkg.load_library()
+    f = B.make_format(6, 4)
+    n, k, ns = 1024, 4096, 65536
+    nb = pkg.kmeans_workspace_bytes(6, 4, n, k, ns)
+    nvec = n * k // 8
+    # running r^2 per vector, per sample a direction (64 B) and an index (4 B), per centre 64 B,
+    # per (centre, chunk) pair 64 B
+    assert nb >= nvec * 8 + ns * 68 + 64 * 64 + 65536 * 64
+    assert nb <= nvec * 8 + ns * 68 + 64 * 64 + 65536 * 64 + (nvec // 2048 + ns // 1024) * 8 + 8 * 256
+    with pytest.raises(pkg.SphError) as e:
+        pkg.kmeans_workspace_bytes(6, 4, n, k, 0)
+    assert e.value.status == 2
+
+    def st(ns=1000, iters=5, ws_bytes=1 << 40, ws=0x100000, u=0x10000, ldw=k):
+        return lib.sph_kmeans_codebook(ctypes.byref(f), n, k, 0x20000, ldw, u, ns, iters, 0x30000,
+                                       0x40000, 0x50000, 0x60000, ws, ws_bytes, None)
+    assert st(u=0) == 1 and st(ws=0) == 1
+    assert st(ns=0) == 2 and st(ns=(1 << 24) + 1) == 2 and st(iters=-1) == 2 and st(iters=10001) == 2
+    assert st(ws=0x100080) == 2 and st(u=0x10004) == 2 and st(ldw=k - 4) == 2
+    assert st(ws_bytes=pkg.kmeans_workspace_bytes(6, 4, n, k, 1000) - 1) == 6

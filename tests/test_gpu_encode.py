@@ -1,0 +1,286 @@
+"""GPU parity of the device encoder and the radius-weighted spherical k-means (through the C ABI)
+against the fp64 oracle.
+
+Both sides compute in fp64, so every integer they produce is compared exactly. The one
+allowance: a decision that floating point takes between two candidates whose fp64 scores differ
+by less than the rounding of the two implementations' different summation orders (a cosine
+near-tie in Eq. 5, a radius level near a rounding boundary, a sampled vector whose running r^2
+sits on the draw). Such places are found from the oracle's own values and listed; everything else
+must match bit for bit.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import sph as O
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import paper_2609_24875_amd as pkg  # noqa: E402
+
+DEV = torch.device("cuda:0")
+FMTS = ["W2", "W3", "W2_cfg", "W3_cfg", "W2_16", "W3_25", "W2_63", "W2_72", "W2_82"]
+TIE = 1e-12          # cosine gap below which either direction index is accepted
+LEVEL_TIE = 1e-9     # distance of (r~ - min)/step from a half-integer below which q may differ
+
+
+def weights32(n, k, seed):
+    return synth.outlier_gaussian_weights(n, k, synth.rng(seed, n, k, synth.STREAM_WEIGHTS)).astype(np.float32)
+
+
+def dev_bits(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(DEV)
+
+
+def gpu_encode(D, V, w32, cb, ldw=None):
+    n, k = w32.shape
+    if ldw is None or ldw == k:
+        wd = torch.from_numpy(w32).to(DEV)
+    else:
+        buf = torch.full((n, ldw), float("nan"), dtype=torch.float32, device=DEV)
+        buf[:, :k] = torch.from_numpy(w32).to(DEV)
+        wd = buf[:, :k]
+    out = pkg.encode(D, V, wd, dev_bits(cb))
+    torch.cuda.synchronize()
+    return pkg.codes_to_host(out)
+
+
+def compare_codes(w32, cb, V, got, ref, rows=None):
+    """Exact equality of every code, except near-ties located from the oracle's fp64 values.
+    Returns the number of excused vectors."""
+    w = w32.astype(np.float64)
+    n, k = w.shape
+    nv = k // 8
+    assert np.array_equal(got["signs"], ref["signs"])
+    c = O.f16_to_f64(cb)
+    _neg, wp, _r, d = O.decompose(w.reshape(n, nv, 8))
+    dz = got["dir"] != ref["dir"]
+    excused = 0
+    if dz.any():
+        ii = np.argwhere(dz)
+        for (a, b) in ii:
+            s_got = d[a, b] @ c[got["dir"][a, b]]
+            s_ref = d[a, b] @ c[ref["dir"][a, b]]
+            assert abs(s_got - s_ref) <= TIE, (a, b, s_got, s_ref)
+        excused += len(ii)
+    # groups whose directions all agree: parameters and levels are exact, up to level near-ties
+    gz = dz.reshape(n, nv // 16, 16).any(axis=2)
+    assert np.array_equal(got["gmin"][~gz], ref["gmin"][~gz])
+    assert np.array_equal(got["gstep"][~gz], ref["gstep"][~gz])
+    qdiff = (got["q"] != ref["q"]) & ~np.repeat(gz, 16, axis=1)
+    if qdiff.any():
+        rt = O.ls_radius(wp, c[ref["dir"]])
+        lo = np.repeat(O.f16_to_f64(ref["gmin"]), 16, axis=1)
+        st = np.repeat(O.f16_to_f64(ref["gstep"]), 16, axis=1)
+        x = (rt - lo) / st
+        assert np.all(np.abs(np.abs(x - np.floor(x)) - 0.5)[qdiff] < LEVEL_TIE)
+        assert np.all(np.abs(got["q"].astype(int) - ref["q"].astype(int))[qdiff] == 1)
+        excused += int(qdiff.sum())
+    return excused
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("n,k", [(87, 640), (16, 128), (1, 256), (300, 2048)])
+def test_encode_parity(fmt, n, k):
+    D, V = synth.FORMATS[fmt]
+    w32 = weights32(n, k, 11)
+    cb = synth.random_codebook(D, synth.rng(11, n, k, synth.STREAM_CODEBOOK))
+    got = gpu_encode(D, V, w32, cb)
+    ref = O.encode(w32.astype(np.float64), cb, V)
+    assert compare_codes(w32, cb, V, got, ref) == 0
+
+
+def test_encode_leading_dimension():
+    D, V = synth.FORMATS["W2"]
+    w32 = weights32(40, 384, 12)
+    cb = synth.random_codebook(D, synth.rng(12, synth.STREAM_CODEBOOK))
+    got = gpu_encode(D, V, w32, cb, ldw=396)
+    ref = O.encode(w32.astype(np.float64), cb, V)
+    assert compare_codes(w32, cb, V, got, ref) == 0
+
+
+def test_encode_edge_values():
+    """Zero and negative-zero vectors, constant groups (zero step), fp16 rounding ties, fp16
+    subnormal and overflowing offsets, against the oracle with a codebook whose every entry is
+    e_0 (so r~ = |w_0| exactly and every cosine ties: the lowest index, 0, must win)."""
+    D, V = synth.FORMATS["W2"]
+    cb = np.zeros((1 << D, 8), np.uint16)
+    cb[:, 0] = 0x3C00
+    firsts = [0.0, -0.0, 1 + 2.0**-11, 1 + 3 * 2.0**-11, 65504.0, 65519.0, 65520.0, 70000.0,
+              2.0**-24, 2.0**-25, 1.5 * 2.0**-25, 3 * 2.0**-25, 2.0**-14 - 2.0**-25, 2.0**-14 + 2.0**-25,
+              1e-30, 0.1]
+    n, k = len(firsts) * 2, 256
+    w = np.zeros((n, k), np.float32)
+    for r, x in enumerate(firsts):
+        w[r, 0::8] = np.float32(x)                      # row r: 32 equal vectors (zero step)
+        w[len(firsts) + r, 0::8] = np.float32(x)
+        w[len(firsts) + r, 8::16] = np.float32(x) * np.float32(1.75)   # two values per group
+    w[3, 1] = -0.0
+    w[5, 3::8] = -0.0
+    got = gpu_encode(D, V, w, cb)
+    ref = O.encode(w.astype(np.float64), cb, V)
+    assert np.all(got["dir"] == 0)
+    for key in ("signs", "dir", "q", "gmin", "gstep"):
+        assert np.array_equal(got[key], ref[key]), key
+
+
+def test_encode_duplicate_entries_take_lowest_index():
+    D, V = synth.FORMATS["W2"]
+    cb = synth.random_codebook(D, synth.rng(13, synth.STREAM_CODEBOOK))
+    cb[40] = cb[7]
+    cb[63] = cb[7]
+    c7 = O.f16_to_f64(cb[7])
+    n, k = 4, 128
+    g = np.random.default_rng(13)
+    scale = g.uniform(0.1, 2.0, (n, k // 8, 1)) * np.where(g.random((n, k // 8, 8)) < 0.5, -1, 1)
+    w = (scale * c7).reshape(n, k).astype(np.float32)
+    got = gpu_encode(D, V, w, cb)
+    ref = O.encode(w.astype(np.float64), cb, V)
+    assert np.all(ref["dir"] == 7)
+    for key in ("signs", "dir", "q", "gmin", "gstep"):
+        assert np.array_equal(got[key], ref[key]), key
+
+
+def test_encode_pack_gemv_pipeline():
+    """Device-encoded codes packed and multiplied: equal to the oracle's decode of its own codes."""
+    D, V = synth.FORMATS["W2"]
+    n, k = 200, 1024
+    w32 = weights32(n, k, 14)
+    cb = synth.random_codebook(D, synth.rng(14, synth.STREAM_CODEBOOK))
+    got = gpu_encode(D, V, w32, cb)
+    ref = O.encode(w32.astype(np.float64), cb, V)
+    assert compare_codes(w32, cb, V, got, ref) == 0
+    pw = pkg.pack(D, V, got, cb, device=DEV)
+    x = synth.activations(1, k, synth.rng(14, synth.STREAM_X))
+    xd = torch.from_numpy(x.view(np.int16)).to(DEV).view(torch.float16)
+    y = pkg.gemv(pw, xd[0]).cpu().numpy()
+    assert O.rel_err(y, O.gemv(ref, cb, x)) <= 2e-3
+
+
+@pytest.mark.parametrize("fmt", ["W2", "W3"])
+def test_encode_full_size_sampled_rows(fmt):
+    """Full-size matrices (12288 x 4096, one of the 8B-class MLP projections) encoded in one launch;
+    the oracle recomputes a sample of rows (encoding is row-local)."""
+    D, V = synth.FORMATS[fmt]
+    n, k = 12288, 4096
+    w32 = weights32(n, k, 15)
+    cb = synth.random_codebook(D, synth.rng(15, synth.STREAM_CODEBOOK))
+    got = gpu_encode(D, V, w32, cb)
+    rows = np.sort(np.random.default_rng(15).choice(n, 24, replace=False))
+    rows[0], rows[-1] = 0, n - 1
+    ref = O.encode(w32[rows].astype(np.float64), cb, V)
+    sub = {key: v[rows] for key, v in got.items()}
+    assert compare_codes(w32[rows], cb, V, sub, ref) <= 2
+
+
+# ------------------------------------------------------------------------------------ k-means
+
+def gpu_kmeans(D, V, w32, u, init, iters):
+    wd = torch.from_numpy(w32).to(DEV)
+    cb, obj, idx = pkg.kmeans_codebook(D, V, wd, torch.from_numpy(u).to(DEV), dev_bits(init), iters)
+    torch.cuda.synchronize()
+    return cb.cpu().numpy().view(np.uint16), obj.cpu().numpy(), idx.cpu().numpy()
+
+
+def oracle_kmeans(w32, u, init, iters):
+    w = w32.astype(np.float64)
+    n, k = w.shape
+    _neg, _wp, r, d = O.decompose(w.reshape(n, k // 8, 8))
+    idx = O.sample_by_squared_radius(r, u)
+    c, obj = O.spherical_kmeans(d.reshape(-1, 8)[idx], init, iters)
+    return O.f64_to_f16(c), np.array(obj), idx, c, r
+
+
+def sample_flips_excused(r, u, idx_got, idx_ref):
+    """Indices where the draw differs must sit on a boundary of the oracle's running r^2."""
+    cdf = np.cumsum(r.reshape(-1) ** 2)
+    bad = np.flatnonzero(idx_got != idx_ref)
+    for j in bad:
+        t = u[j] * cdf[-1]
+        edge = cdf[min(idx_got[j], idx_ref[j])]
+        assert abs(edge - t) <= 1e-12 * cdf[-1], (j, idx_got[j], idx_ref[j])
+    return len(bad)
+
+
+def compare_codebook(cb_got, cb_ref, c_ref):
+    diff = cb_got != cb_ref
+    if diff.any():
+        # only entries whose fp64 value sits on an fp16 rounding boundary may differ
+        lo = O.f16_to_f64(np.minimum(cb_got, cb_ref))
+        hi = O.f16_to_f64(np.maximum(cb_got, cb_ref))
+        mid = (lo + hi) / 2
+        assert np.all(np.abs(c_ref - mid)[diff] <= 1e-12 * np.abs(mid)[diff])
+    return int(diff.sum())
+
+
+@pytest.mark.parametrize("fmt", ["W2", "W3", "W2_cfg", "W3_cfg"])
+def test_kmeans_parity(fmt):
+    D, V = synth.FORMATS[fmt]
+    n, k, ns, iters = 64, 512, 3000, 6
+    w32 = weights32(n, k, 21)
+    g = synth.rng(21, ns, synth.STREAM_CODES)
+    u = g.random(ns)
+    init = synth.random_codebook(D, synth.rng(21, synth.STREAM_CODEBOOK))
+    cb, obj, idx = gpu_kmeans(D, V, w32, u, init, iters)
+    cb_ref, obj_ref, idx_ref, c_ref, r = oracle_kmeans(w32, u, init, iters)
+    assert sample_flips_excused(r, u, idx, idx_ref) == 0
+    assert np.allclose(obj, obj_ref, rtol=1e-12, atol=0)
+    assert np.all(np.diff(obj) >= -1e-9)
+    assert compare_codebook(cb, cb_ref, c_ref) == 0
+
+
+def test_kmeans_repeatable_and_zero_iterations():
+    D, V = synth.FORMATS["W2"]
+    w32 = weights32(48, 256, 22)
+    u = np.random.default_rng(22).random(1000)
+    init = synth.random_codebook(D, synth.rng(22, synth.STREAM_CODEBOOK))
+    a = gpu_kmeans(D, V, w32, u, init, 4)
+    b = gpu_kmeans(D, V, w32, u, init, 4)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    cb0, obj0, _ = gpu_kmeans(D, V, w32, u, init, 0)
+    assert np.array_equal(cb0, init) and obj0.shape == (1,)
+    assert np.isclose(obj0[0], a[1][0], rtol=0, atol=0)
+
+
+def test_kmeans_zero_matrix():
+    """All radii zero: every draw clamps to the last vector, whose direction is zero; every centre
+    keeps its position and the objective is zero."""
+    D, V = synth.FORMATS["W2"]
+    w32 = np.zeros((16, 128), np.float32)
+    u = np.random.default_rng(23).random(300)
+    init = synth.random_codebook(D, synth.rng(23, synth.STREAM_CODEBOOK))
+    cb, obj, idx = gpu_kmeans(D, V, w32, u, init, 3)
+    cb_ref, obj_ref, idx_ref, _c, _r = oracle_kmeans(w32, u, init, 3)
+    assert np.all(idx == 16 * 16 - 1) and np.array_equal(idx, idx_ref)
+    assert np.array_equal(cb, init) and np.array_equal(cb, cb_ref)
+    assert np.all(obj == 0) and np.all(obj_ref == 0)
+
+
+@pytest.mark.parametrize("fmt,iters", [("W2", 20), ("W3", 2)])
+def test_kmeans_full_size(fmt, iters):
+    """Sec. 4.1's settings (65,536 samples; 20 iterations for W2, 2 for W3 to keep the fp64 oracle
+    in seconds) on a 12288 x 4096 matrix. A draw may flip where the running r^2 lands on the
+    boundary (the two sides sum 6.3 M squared radii in different orders); then the codebooks can
+    drift apart slightly and only the objective trace is compared, loosely."""
+    D, V = synth.FORMATS[fmt]
+    n, k, ns = 12288, 4096, 65536
+    w32 = weights32(n, k, 24)
+    u = synth.rng(24, ns, synth.STREAM_CODES).random(ns)
+    init = synth.random_codebook(D, synth.rng(24, synth.STREAM_CODEBOOK))
+    cb, obj, idx = gpu_kmeans(D, V, w32, u, init, iters)
+    cb_ref, obj_ref, idx_ref, c_ref, r = oracle_kmeans(w32, u, init, iters)
+    flips = sample_flips_excused(r, u, idx, idx_ref)
+    assert flips <= 3
+    assert np.all(np.diff(obj) >= -1e-9 * abs(obj[0]))
+    if flips == 0:
+        assert np.allclose(obj, obj_ref, rtol=1e-12, atol=0)
+        assert compare_codebook(cb, cb_ref, c_ref) <= 2
+    else:
+        assert np.allclose(obj, obj_ref, rtol=1e-4, atol=0)

@@ -68,6 +68,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
     ap.add_argument("--unfused", action="store_true", help="launch q, k, v, gate, up separately")
+    ap.add_argument("--path", default="decode", choices=("decode", "encode"),
+                    help="decode: the default benchmark; encode: device encoder and k-means codebook")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (HBM counter calibration)")
     return ap.parse_args()
@@ -144,12 +146,97 @@ def cpu_baseline(mats, budget_s, step_bytes_total, per_mat_bytes, layers):
     }
 
 
+FP64_PEAK_TFS = 78.6   # MI355X fp64 vector peak
+
+
+def encode_main(args):
+    """Encoder benchmark: a step is sph_encode of one 12288x4096 fp32 matrix (the 8B-class
+    gate/up shape) plus sph_kmeans_codebook on it with the paper's 65,536 samples and 20
+    iterations. The dominant kernel is the Eq. 5 nearest-direction search inside the encoder,
+    bound by the fp64 vector ALUs: 2^D cosines of 8 terms (8 multiplies + 7 adds) per vector."""
+    import torch
+
+    import paper_2609_24875_amd as pkg
+
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    fmt = args.fmt or "W3"
+    D, V = synth.FORMATS[fmt]
+    n, k, ns, iters = 12288, 4096, 65536, 20
+    w64 = synth.outlier_gaussian_weights(n, k, synth.rng(7, n, k, synth.STREAM_WEIGHTS))
+    w32 = w64.astype(np.float32)
+    cb = synth.random_codebook(D, synth.rng(7, synth.STREAM_CODEBOOK))
+    wd = torch.from_numpy(w32).to(dev)
+    cbd = torch.from_numpy(cb.view(np.int16)).to(dev)
+    ud = torch.from_numpy(synth.rng(7, ns, synth.STREAM_CODES).random(ns)).to(dev)
+    ws = torch.empty(pkg.kmeans_workspace_bytes(D, V, n, k, ns), dtype=torch.uint8, device=dev)
+
+    def timed(fn, reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    enc = lambda: pkg.encode(D, V, wd, cbd)  # noqa: E731
+    km = lambda: pkg.kmeans_codebook(D, V, wd, ud, cbd, iters, workspace=ws)  # noqa: E731
+    for _ in range(args.warmup):
+        enc()
+        km()
+    torch.cuda.synchronize()
+    enc_ms = timed(enc, args.steps)
+    km_ms = timed(km, max(1, args.steps // 4))
+    nvec = n * k // 8
+    flops = nvec * (1 << D) * 15
+    out = {
+        "metric": "device encoder: weights encoded per second (Eq. 3, 5-7) and k-means codebook time",
+        "value": round(n * k / (enc_ms / 1e3) / 1e9, 3),
+        "unit": "Gweights/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(enc_ms + km_ms, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64 (from fp32 weights)",
+        "data": "synthetic: N(0, 0.02^2) weights with 0.1% Student-t outliers x20, random positive "
+                "unit fp16 codebook, uniform draws",
+        "config": {"workload": f"encode-{fmt}-{n}x{k}", "format": f"{fmt} (8 sign + {D} direction + "
+                   f"{V} radius bits)", "kmeans_samples": ns, "kmeans_iters": iters,
+                   "encode_ms": round(enc_ms, 4), "kmeans_ms": round(km_ms, 4)},
+        "roofline": {"kernel": f"k_encode {fmt} {n}x{k}", "bound": "alu",
+                     "achieved": round(flops / (enc_ms / 1e3) / 1e12, 2), "peak": FP64_PEAK_TFS,
+                     "unit": "TFLOP/s", "frac": round(flops / (enc_ms / 1e3) / 1e12 / FP64_PEAK_TFS, 4),
+                     "traffic": None, "flops_per_launch": flops},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import sph as O
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            threads = int(os.environ.get("OMP_NUM_THREADS") or os.cpu_count())
+        rows, t0 = 0, time.perf_counter()
+        step = 16 if D > 8 else 256
+        while time.perf_counter() - t0 < args.cpu_sample_seconds and rows < n:
+            O.encode(w32[rows:rows + step].astype(np.float64), cb, V)
+            rows += step
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(rows * k / dt / 1e9, 6), "unit": "Gweights/s",
+                               "cores": int(threads), "kind": "oracle",
+                               "sample": f"oracle encode of the first {rows} of {n} rows in {dt:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.path == "encode":
+        return encode_main(args)
     import torch
 
     import paper_2609_24875_amd as pkg

@@ -153,9 +153,12 @@ sph_status sph_encode(const sph_format* fmt, int64_t n, int64_t k, const float* 
                       void* stream);
 
 /* Device workspace needed by sph_kmeans_codebook for an n x k matrix and n_samples samples
- * (1 <= n_samples <= 2^24): 8 bytes per 8-D vector of the matrix for the running sum of squared
- * radii, 68 bytes per sample, and 64 bytes per codebook entry times the number of sample chunks
- * (about 64 K entry-chunk pairs), plus alignment. */
+ * (1 <= n_samples <= 2^24): 8 bytes per 8-D vector of the matrix (running sum of squared radii),
+ * 76 bytes per sample (direction, assignment, objective part), 12 bytes per sample and codebook
+ * split of the assignment (splits x samples stays below about 2^20 + n_samples), 64 bytes per
+ * codebook entry (the fp64 centre), and 192 bytes per codebook entry and sample chunk for the
+ * fixed-point centre sums (about 128 / ceil(2^D / 512) chunks, fewer when samples are few),
+ * plus alignment. */
 sph_status sph_kmeans_workspace_bytes(const sph_format* fmt, int64_t n, int64_t k, int64_t n_samples,
                                       size_t* bytes);
 

@@ -13,12 +13,15 @@
 //                128-weight group; the codebook is staged in LDS as fp64 in 512-entry chunks and
 //                read by broadcast.
 //   k-means      squared radii and their running sum (three-pass scan), inverse-CDF sampling by
-//                binary search, then per iteration: assignment (as in the encoder), per-centre
-//                partial sums over fixed sample chunks in sample order, and one workgroup per
-//                centre summing those partials in a fixed order and renormalising.
+//                binary search, then per iteration: assignment (the centre range split over
+//                workgroups, splits combined in ascending order), exact fixed-point centre sums
+//                (integer LDS atomics per block, integer sums across blocks, so the order of
+//                arrival does not matter), renormalisation.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+
+#include <algorithm>
 
 #include "sph_host.h"
 #include "sph_layout.h"
@@ -31,8 +34,7 @@ constexpr int kVpt = 4;          // vectors (or samples) per thread in the assig
 constexpr int kChunk = 512;      // codebook entries per LDS pass: 32 KiB of fp64
 constexpr int kScanItems = 8;    // vectors per thread in the radius scan
 constexpr int kScanBlock = kThreads * kScanItems;
-constexpr int kPartialThreads = 64;
-constexpr int64_t kPartialTarget = 65536;  // centre x chunk pairs per partial-sum launch
+constexpr int kTargetBlocks = 1024;  // workgroups the k-means launches aim for (256 CUs)
 
 __device__ __forceinline__ double h2d(uint16_t b) { return (double)(float)__builtin_bit_cast(_Float16, b); }
 
@@ -115,14 +117,14 @@ __device__ __forceinline__ void argmax_chunk(const double* __restrict__ cl, int 
   }
 }
 
-// Stage the codebook chunk by chunk into LDS and run the argmax over it. The source is either the
-// fp16 codebook or fp64 centres. Every thread of the block must call this.
+// Stage entries [c0, c1) of the codebook chunk by chunk into LDS and run the argmax over them.
+// The source is either the fp16 codebook or fp64 centres. Every thread of the block must call this.
 template <typename T>
-__device__ __forceinline__ void argmax_codebook(const T* __restrict__ src, int ncb, double* cl,
+__device__ __forceinline__ void argmax_codebook(const T* __restrict__ src, int c0, int c1, double* cl,
                                                 const double (&d)[kVpt][8], double (&best)[kVpt],
                                                 int (&bz)[kVpt]) {
-  for (int base = 0; base < ncb; base += kChunk) {
-    const int cnt = min(kChunk, ncb - base);
+  for (int base = c0; base < c1; base += kChunk) {
+    const int cnt = min(kChunk, c1 - base);
     __syncthreads();
     for (int t = threadIdx.x; t < cnt * 8; t += kThreads) {
       if constexpr (sizeof(T) == 2)
@@ -171,7 +173,7 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a) {
       for (int j = 0; j < 8; ++j) d[u][j] = 0.0;
     }
   }
-  argmax_codebook(a.cb, a.ncb, cl, d, best, bz);
+  argmax_codebook(a.cb, 0, a.ncb, cl, d, best, bz);
 #pragma unroll
   for (int u = 0; u < kVpt; ++u) {
     const int64_t i = blk + u * kThreads + threadIdx.x;
@@ -323,92 +325,171 @@ __global__ __launch_bounds__(kThreads) void k_init_centres(const uint16_t* __res
   if (t < count) cen[t] = h2d(init[t]);
 }
 
-// Eq. 5 for every sample against the current centres; z[j] gets the nearest centre and each
-// block writes the sum of the samples' cosines to their centre (summed per sample in pairwise
-// order, then in a fixed order over the block).
-__global__ __launch_bounds__(kThreads) void k_assign(const double* __restrict__ ds, int64_t ns,
-                                                     const double* __restrict__ cen, int ncb,
-                                                     int32_t* __restrict__ z, double* __restrict__ opart) {
+// Eq. 5 for every sample against centres [split * per, (split + 1) * per): the best cosine and its
+// index per sample and split (blockIdx.y is the split).
+__global__ __launch_bounds__(kThreads) void k_assign_split(const double* __restrict__ ds, int64_t ns,
+                                                           const double* __restrict__ cen, int ncb, int per,
+                                                           double* __restrict__ sbest, int32_t* __restrict__ sidx) {
   __shared__ double cl[kChunk * 8];
-  __shared__ double sh[kThreads / 64];
   const int64_t blk = (int64_t)blockIdx.x * kThreads * kVpt;
+  const int c0 = blockIdx.y * per, c1 = min(ncb, c0 + per);
   double d[kVpt][8], best[kVpt];
   int bz[kVpt];
 #pragma unroll
   for (int u = 0; u < kVpt; ++u) {
     const int64_t j = blk + u * kThreads + threadIdx.x;
     best[u] = -INFINITY;
-    bz[u] = 0;
+    bz[u] = c0;
 #pragma unroll
     for (int c = 0; c < 8; ++c) d[u][c] = j < ns ? ds[j * 8 + c] : 0.0;
   }
-  argmax_codebook(cen, ncb, cl, d, best, bz);
-  double s = 0.0;
+  argmax_codebook(cen, c0, c1, cl, d, best, bz);
 #pragma unroll
   for (int u = 0; u < kVpt; ++u) {
     const int64_t j = blk + u * kThreads + threadIdx.x;
     if (j < ns) {
-      z[j] = bz[u];
-      s += dot8_pairwise(d[u], cen + (int64_t)bz[u] * 8);
+      sbest[blockIdx.y * ns + j] = best[u];
+      sidx[blockIdx.y * ns + j] = bz[u];
     }
   }
+}
+
+// The splits combined in ascending order with a strict comparison (the same decision as one scan
+// over all centres); z[j] gets the nearest centre and each block writes the sum of its samples'
+// cosines to their centre (each summed in pairwise order, then in a fixed order over the block).
+__global__ __launch_bounds__(kThreads) void k_assign_final(const double* __restrict__ ds, int64_t ns,
+                                                           const double* __restrict__ cen, int nsplit,
+                                                           const double* __restrict__ sbest,
+                                                           const int32_t* __restrict__ sidx,
+                                                           int32_t* __restrict__ z, double* __restrict__ opart) {
+  __shared__ double sh[kThreads / 64];
+  const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  double v = 0.0;
+  if (j < ns) {
+    double best = sbest[j];
+    int bz = sidx[j];
+    for (int t = 1; t < nsplit; ++t) {
+      const double b = sbest[t * ns + j];
+      if (b > best) {
+        best = b;
+        bz = sidx[t * ns + j];
+      }
+    }
+    z[j] = bz;
+    double d[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) d[c] = ds[j * 8 + c];
+    v = dot8_pairwise(d, cen + (int64_t)bz * 8);
+  }
   double total;
-  block_exclusive(s, sh, total);
+  block_exclusive(v, sh, total);
   if (threadIdx.x == 0) opart[blockIdx.x] = total;
 }
 
-// Objective of one assignment: the blocks' sums added in block order.
+// Objective of one assignment: the blocks' sums, lane-strided in block order and then combined
+// by a fixed lane tree.
 __global__ __launch_bounds__(64) void k_objective(const double* __restrict__ opart, int64_t nblk,
                                                   double* __restrict__ out) {
-  if (threadIdx.x != 0) return;
   double s = 0.0;
-  for (int64_t b = 0; b < nblk; ++b) s += opart[b];
-  *out = s;
+  for (int64_t b = threadIdx.x; b < nblk; b += 64) s += opart[b];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  if (threadIdx.x == 0) *out = s;
 }
 
-// Sum of the directions assigned to centre c among samples [p*ch, (p+1)*ch), in sample order.
-__global__ __launch_bounds__(kPartialThreads) void k_partial(const double* __restrict__ ds, int64_t ns,
-                                                             const int32_t* __restrict__ z, int ncb,
-                                                             int64_t ch, int np, double* __restrict__ part) {
-  const int c = blockIdx.x * kPartialThreads + threadIdx.x;
+// Centre sums by exact fixed-point accumulation. A direction component v in [0, 1 + 2^-52] is
+// truncated to T = floor(v * 2^100) and added as three 40-bit limbs in 64-bit integers. Integer
+// addition is associative, so the sums do not depend on the order in which samples are added,
+// and 2^24 samples cannot overflow a limb. The sum is exact up to the 2^-100 truncation of each
+// term. Block (r, p) adds the samples of chunk p whose centre lies in range r with LDS atomics
+// and stores its limbs; one wave per centre then adds the chunks' limbs.
+constexpr int kFixBits = 100;
+constexpr int kLimbBits = 40;
+constexpr uint64_t kLimbMask = (1ull << kLimbBits) - 1;
+constexpr int kLimbs = 8 * 3;       // limbs per centre
+constexpr int kAccRange = 512;      // centres per LDS accumulator: 96 KiB
+
+__device__ __forceinline__ void to_limbs(double v, uint64_t& l0, uint64_t& l1, uint64_t& l2) {
+  const uint64_t bits = __builtin_bit_cast(uint64_t, v);
+  const int ex = (int)(bits >> 52);  // components are >= 0; 0 for zero and subnormals
+  unsigned __int128 t = 0;
+  if (ex != 0) {
+    const uint64_t m = (bits & 0xFFFFFFFFFFFFFull) | 0x10000000000000ull;
+    const int sh = ex - 1075 + kFixBits;  // v = m * 2^(ex - 1075)
+    if (sh >= 0)
+      t = (unsigned __int128)m << sh;
+    else if (sh > -64)
+      t = m >> -sh;
+  }
+  l0 = (uint64_t)t & kLimbMask;
+  l1 = (uint64_t)(t >> kLimbBits) & kLimbMask;
+  l2 = (uint64_t)(t >> (2 * kLimbBits));
+}
+
+__global__ __launch_bounds__(kThreads) void k_accumulate(const double* __restrict__ ds, int64_t ns,
+                                                         const int32_t* __restrict__ z, int ncb, int64_t ch,
+                                                         unsigned long long* __restrict__ part) {
+  __shared__ unsigned long long la[kAccRange * kLimbs];
+  const int c0 = blockIdx.x * kAccRange, c1 = min(ncb, c0 + kAccRange), nc = c1 - c0;
   const int p = blockIdx.y;
+  for (int t = threadIdx.x; t < nc * kLimbs; t += kThreads) la[t] = 0;
+  __syncthreads();
   const int64_t j0 = (int64_t)p * ch, j1 = min(ns, j0 + ch);
-  double s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int64_t j = j0; j < j1; ++j) {
-    if (z[j] == c) {
+  for (int64_t j = j0 + threadIdx.x; j < j1; j += kThreads) {
+    const int c = z[j];
+    if (c < c0 || c >= c1) continue;
+    unsigned long long* a = la + (c - c0) * kLimbs;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s[e] += ds[j * 8 + e];
+    for (int e = 0; e < 8; ++e) {
+      uint64_t l0, l1, l2;
+      to_limbs(ds[j * 8 + e], l0, l1, l2);
+      if (l0) atomicAdd(a + 3 * e, (unsigned long long)l0);
+      if (l1) atomicAdd(a + 3 * e + 1, (unsigned long long)l1);
+      if (l2) atomicAdd(a + 3 * e + 2, (unsigned long long)l2);
     }
   }
-  if (c < ncb) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) part[((int64_t)c * np + p) * 8 + e] = s[e];
-  }
+  __syncthreads();
+  unsigned long long* out = part + ((int64_t)p * ncb + c0) * kLimbs;
+  for (int t = threadIdx.x; t < nc * kLimbs; t += kThreads) out[t] = la[t];
 }
 
-// New centre c: the chunk partials summed in a fixed order (lane-strided, then a fixed lane
-// tree), normalised to unit length; a centre without directions keeps its position.
-__global__ __launch_bounds__(64) void k_update(const double* __restrict__ part, int np,
+// New centre c: the chunks' limbs added (integers, so in any order), converted to fp64 and the
+// sum normalised to unit length; a centre without directions keeps its position.
+__global__ __launch_bounds__(64) void k_update(const unsigned long long* __restrict__ part, int np, int ncb,
                                                double* __restrict__ cen) {
 #pragma clang fp contract(off)
   const int c = blockIdx.x;
   const int lane = threadIdx.x;
-  double s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int p = lane; p < np; p += 64) {
+  uint64_t l[kLimbs];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s[e] += part[((int64_t)c * np + p) * 8 + e];
+  for (int t = 0; t < kLimbs; ++t) l[t] = 0;
+  for (int p = lane; p < np; p += 64) {
+    const unsigned long long* a = part + ((int64_t)p * ncb + c) * kLimbs;
+#pragma unroll
+    for (int t = 0; t < kLimbs; ++t) l[t] += a[t];
   }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s[e] += __shfl_xor(s[e], o, 64);
+    for (int t = 0; t < kLimbs; ++t) l[t] += __shfl_xor(l[t], o, 64);
   }
-  if (lane == 0) {
-    const double norm = sqrt(dot8_pairwise(s, s));
-    if (norm > 0.0) {
+  if (lane != 0) return;
+  double s[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) cen[(int64_t)c * 8 + e] = s[e] / norm;
-    }
+  for (int e = 0; e < 8; ++e) {
+    uint64_t l0 = l[3 * e], l1 = l[3 * e + 1], l2 = l[3 * e + 2];
+    l1 += l0 >> kLimbBits;
+    l0 &= kLimbMask;
+    l2 += l1 >> kLimbBits;
+    l1 &= kLimbMask;
+    // l2 < 2^53 and l1, l0 < 2^40 convert exactly; two roundings combine them
+    const double hi = ((double)l2 * 0x1p40 + (double)l1) * 0x1p40;
+    s[e] = (hi + (double)l0) * 0x1p-100;
+  }
+  const double norm = sqrt(dot8_pairwise(s, s));
+  if (norm > 0.0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cen[(int64_t)c * 8 + e] = s[e] / norm;
   }
 }
 
@@ -423,9 +504,9 @@ __global__ __launch_bounds__(kThreads) void k_centres_to_f16(const double* __res
 inline uint64_t align256(uint64_t x) { return (x + 255) / 256 * 256; }
 
 struct KmPlan {
-  int64_t nvec, nb, nab, ch;
-  int ncb, np;
-  uint64_t off_cdf, off_bsum, off_ds, off_z, off_opart, off_cen, off_part, total;
+  int64_t nvec, nb, nab, nfb, ch;
+  int ncb, nsplit, per, nr, np;
+  uint64_t off_cdf, off_bsum, off_ds, off_z, off_opart, off_cen, off_acc, off_sbest, off_sidx, total;
 };
 
 KmPlan km_plan(const sph_format* fmt, int64_t n, int64_t k, int64_t ns) {
@@ -433,9 +514,17 @@ KmPlan km_plan(const sph_format* fmt, int64_t n, int64_t k, int64_t ns) {
   P.nvec = n * (k / SPH_VEC);
   P.nb = (P.nvec + kScanBlock - 1) / kScanBlock;
   P.nab = (ns + kThreads * kVpt - 1) / (kThreads * kVpt);
+  P.nfb = (ns + kThreads - 1) / kThreads;
   P.ncb = 1 << fmt->dir_bits;
-  int64_t np = kPartialTarget / P.ncb;
-  np = np < 1 ? 1 : np > ns ? ns : np;
+  // centre splits of the assignment: enough workgroups for the chip, at least 64 centres each
+  int64_t sp = (kTargetBlocks + P.nab - 1) / P.nab;
+  sp = std::min<int64_t>(sp, std::max(1, P.ncb / 64));
+  P.per = (int)((P.ncb + sp - 1) / sp);
+  P.nsplit = (P.ncb + P.per - 1) / P.per;
+  // centre ranges x sample chunks of the accumulation: about 128 workgroups
+  P.nr = (P.ncb + kAccRange - 1) / kAccRange;
+  int64_t np = (128 + P.nr - 1) / P.nr;
+  np = std::min<int64_t>(np, (ns + kThreads - 1) / kThreads);
   P.ch = (ns + np - 1) / np;
   P.np = (int)((ns + P.ch - 1) / P.ch);
   uint64_t p = 0;
@@ -448,11 +537,15 @@ KmPlan km_plan(const sph_format* fmt, int64_t n, int64_t k, int64_t ns) {
   P.off_z = p;
   p = align256(p + (uint64_t)ns * 4);
   P.off_opart = p;
-  p = align256(p + (uint64_t)P.nab * 8);
+  p = align256(p + (uint64_t)P.nfb * 8);
   P.off_cen = p;
   p = align256(p + (uint64_t)P.ncb * 64);
-  P.off_part = p;
-  p = align256(p + (uint64_t)P.ncb * P.np * 64);
+  P.off_acc = p;
+  p = align256(p + (uint64_t)P.np * P.ncb * kLimbs * 8);
+  P.off_sbest = p;
+  p = align256(p + (uint64_t)P.nsplit * ns * 8);
+  P.off_sidx = p;
+  p = align256(p + (uint64_t)P.nsplit * ns * 4);
   P.total = p;
   return P;
 }
@@ -544,7 +637,9 @@ sph_status sph_kmeans_codebook(const sph_format* fmt, int64_t n, int64_t k, cons
   int32_t* z = (int32_t*)(ws + P.off_z);
   double* opart = (double*)(ws + P.off_opart);
   double* cen = (double*)(ws + P.off_cen);
-  double* part = (double*)(ws + P.off_part);
+  unsigned long long* acc = (unsigned long long*)(ws + P.off_acc);
+  double* sbest = (double*)(ws + P.off_sbest);
+  int32_t* sidx = (int32_t*)(ws + P.off_sidx);
   const int64_t ns = n_samples, nv = k / SPH_VEC, ncb8 = (int64_t)P.ncb * 8;
   const dim3 blk(kThreads);
   const unsigned g_cb = (unsigned)((ncb8 + kThreads - 1) / kThreads);
@@ -555,17 +650,20 @@ sph_status sph_kmeans_codebook(const sph_format* fmt, int64_t n, int64_t k, cons
             launch_ok((const void*)k_sample, dim3(g_s), blk, s, d_w, ldw, nv, P.nvec, (const double*)cdf, d_u, ns,
                       ds, d_sample_idx) &&
             launch_ok((const void*)k_init_centres, dim3(g_cb), blk, s, d_init, ncb8, cen);
-  const dim3 g_part((unsigned)((P.ncb + kPartialThreads - 1) / kPartialThreads), (unsigned)P.np);
+  const dim3 g_split((unsigned)P.nab, (unsigned)P.nsplit);
   for (int32_t it = 0; ok && it <= iters; ++it) {
-    ok = launch_ok((const void*)k_assign, dim3((unsigned)P.nab), blk, s, (const double*)ds, ns,
-                   (const double*)cen, P.ncb, z, opart);
+    ok = launch_ok((const void*)k_assign_split, g_split, blk, s, (const double*)ds, ns, (const double*)cen, P.ncb,
+                   P.per, sbest, sidx) &&
+         launch_ok((const void*)k_assign_final, dim3((unsigned)P.nfb), blk, s, (const double*)ds, ns,
+                   (const double*)cen, P.nsplit, (const double*)sbest, (const int32_t*)sidx, z, opart);
     if (ok && d_objective)
-      ok = launch_ok((const void*)k_objective, dim3(1), dim3(64), s, (const double*)opart, P.nab,
+      ok = launch_ok((const void*)k_objective, dim3(1), dim3(64), s, (const double*)opart, P.nfb,
                      d_objective + it);
     if (ok && it < iters)
-      ok = launch_ok((const void*)k_partial, g_part, dim3(kPartialThreads), s, (const double*)ds, ns,
-                     (const int32_t*)z, P.ncb, P.ch, P.np, part) &&
-           launch_ok((const void*)k_update, dim3((unsigned)P.ncb), dim3(64), s, (const double*)part, P.np, cen);
+      ok = launch_ok((const void*)k_accumulate, dim3((unsigned)P.nr, (unsigned)P.np), blk, s, (const double*)ds, ns,
+                     (const int32_t*)z, P.ncb, P.ch, acc) &&
+           launch_ok((const void*)k_update, dim3((unsigned)P.ncb), dim3(64), s, (const unsigned long long*)acc, P.np,
+                     P.ncb, cen);
   }
   if (ok) ok = launch_ok((const void*)k_centres_to_f16, dim3(g_cb), blk, s, (const double*)cen, ncb8, d_codebook);
   return ok ? SPH_OK : SPH_ERR_HIP;

@@ -177,10 +177,16 @@ def test_kmeans_workspace_and_validation():
     n, k, ns = 1024, 4096, 65536
     nb = pkg.kmeans_workspace_bytes(6, 4, n, k, ns)
     nvec = n * k // 8
-    # running r^2 per vector, per sample a direction (64 B) and an index (4 B), per centre 64 B,
-    # per (centre, chunk) pair 64 B
-    assert nb >= nvec * 8 + ns * 68 + 64 * 64 + 65536 * 64
-    assert nb <= nvec * 8 + ns * 68 + 64 * 64 + 65536 * 64 + (nvec // 2048 + ns // 1024) * 8 + 8 * 256
+    # running r^2 per vector; per sample a direction (64 B), an assignment (4 B), an objective
+    # part per 256 samples, and a (cosine, index) pair per codebook split; per centre the fp64
+    # centre (64 B) and, per sample chunk, its fixed-point sum (8 components x 3 limbs x 8 B)
+    for D, V in ((6, 4), (13, 3)):
+        ncb = 1 << D
+        chunks = -(-128 // -(-ncb // 512))
+        nb = pkg.kmeans_workspace_bytes(D, V, n, k, ns)
+        assert nb >= nvec * 8 + ns * (64 + 4 + 12) + ncb * (64 + 192 * chunks)
+        assert nb <= (nvec * 8 + ns * 80 + 12 * (ns + 2**20) + ncb * (64 + 192 * chunks) + 10 * 256
+                      + (nvec // 2048 + ns // 256 + 2) * 8)
     with pytest.raises(pkg.SphError) as e:
         pkg.kmeans_workspace_bytes(6, 4, n, k, 0)
     assert e.value.status == 2

@@ -6,7 +6,8 @@ shares no code with the HIP path: it reads the logical codes (see ``synth``) and
 computes with NumPy in fp64, step by step in the paper's order and notation.
 
 References are to the SPHQuant paper: Sec. 1 (introduction, worked radius example),
-Sec. 3.1 (spherical quantisation, Eq. 3-7), Sec. 3.3 (angular codebook, Eq. 9-10),
+Sec. 3.1 (spherical quantisation, Eq. 3-7), Sec. 3.3 (angular codebook, Eq. 9-10, and the
+softplus radius with straight-through fake quantisation), App. A (the layer-wise procedure),
 Sec. 3.4 and App. D (W2 packed layout and fused decode), App. B (payload accounting),
 Tab. 7 (codebook sizes by vector dimension).
 
@@ -341,6 +342,101 @@ def angular_codebook(theta) -> np.ndarray:
         sprod = sprod * np.sin(theta[..., i])
     out[..., VEC - 1] = sprod
     return out
+
+
+def logits_from_codebook(c, eps: float = 1e-4) -> np.ndarray:
+    """Inverse of Eq. 9-10 for a positive unit direction: theta_i = atan2(||c_{i+1..8}||, c_i)
+    (the angle between c's tail from coordinate i on and axis i), then phi = logit of
+    t = (theta - eps) / (pi/2 - 2 eps). Reading: t is clamped to [1e-6, 1 - 1e-6], so an angle
+    at or beyond the interval's ends (a zero coordinate) gives a finite phi (|phi| <= 13.8)."""
+    c = np.asarray(c, dtype=np.float64)
+    tail = np.sqrt(np.cumsum((c * c)[..., ::-1], axis=-1)[..., ::-1])   # ||c_{i..8}||
+    theta = np.arctan2(tail[..., 1:], c[..., :VEC - 1])
+    t = np.clip((theta - eps) / (np.pi / 2 - 2 * eps), 1e-6, 1 - 1e-6)
+    return np.log(t) - np.log1p(-t)
+
+
+def angular_codebook_backward(phi, grad_c, eps: float = 1e-4) -> np.ndarray:
+    """Gradient of a loss L through Eq. 10 and Eq. 9: given dL/dc [..., 8], returns dL/dphi
+    [..., 7]. With c_i = (prod_{j<i} sin t_j) cos t_i, dc_i/dt_j = c_i cot t_j for j < i,
+    -(prod_{k<i} sin t_k) sin t_i for j = i (i <= 7), 0 for j > i; and c_8 = prod sin t_j
+    gives dc_8/dt_j = c_8 cot t_j. Then dt_j/dphi_j = (pi/2 - 2 eps) s (1 - s), s = sigmoid."""
+    phi = np.asarray(phi, dtype=np.float64)
+    g = np.asarray(grad_c, dtype=np.float64)
+    th = angles_from_logits(phi, eps)
+    c = angular_codebook(th)
+    sprod = np.ones(phi.shape[:-1])
+    dth = np.zeros(phi.shape)
+    for j in range(VEC - 1):
+        later = np.sum(g[..., j + 1:] * c[..., j + 1:], axis=-1)        # sum over i > j
+        dth[..., j] = later * np.cos(th[..., j]) / np.sin(th[..., j]) - g[..., j] * sprod * np.sin(th[..., j])
+        sprod = sprod * np.sin(th[..., j])
+    sg = 1.0 / (1.0 + np.exp(-phi))
+    return dth * (np.pi / 2 - 2 * eps) * sg * (1.0 - sg)
+
+
+# ------------------------------- pseudo-quantised module (Sec. 3.3, App. A steps 7-8)
+
+def softplus(rho) -> np.ndarray:
+    """Sec. 3.3's radius parameterisation r = softplus(rho) = log(1 + e^rho)."""
+    return np.logaddexp(0.0, np.asarray(rho, dtype=np.float64))
+
+
+def fake_quant_radius(rho, radius_bits: int):
+    """Group-wise V-bit fake quantisation of r = softplus(rho) (Sec. 3.3, App. A step 8).
+    ``rho`` is [n, k/8]; groups are 16 consecutive vectors of a row, with Eq. 7's offset (min)
+    and step ((max - min) / (2^V - 1)). Readings: the offset and step are rounded to fp16, as
+    the finalised codes store them, and the level is computed from the rounded values (as in
+    ``encode``), half to even, 0 for a zero step. Returns (r, r_hat, q)."""
+    r = softplus(rho)
+    n, nv = r.shape
+    rg = r.reshape(n, nv // VPG, VPG)
+    lo16, st16 = group_offset_step(rg, radius_bits)
+    q = quantize_radius(rg, lo16, st16, radius_bits)
+    r_hat = f16_to_f64(lo16)[..., None] + q * f16_to_f64(st16)[..., None]
+    return r, r_hat.reshape(n, nv), q.reshape(n, nv)
+
+
+def fake_quant_weights(rho, signs, dir_idx, codebook, radius_bits: int) -> np.ndarray:
+    """App. A step 8: W^ with w^_i = r^_i s_i (.) c_{z_i}, from radius parameters, fixed signs and
+    direction indices and an fp64 codebook [2^D, 8] (e.g. from ``angular_codebook``)."""
+    _r, r_hat, _q = fake_quant_radius(rho, radius_bits)
+    c = np.asarray(codebook, dtype=np.float64)
+    w = r_hat[..., None] * sign_factors(signs) * c[np.asarray(dir_idx, dtype=np.int64)]
+    n, nv = r_hat.shape
+    return w.reshape(n, nv * VEC)
+
+
+def fake_quant_backward(rho, signs, dir_idx, codebook, grad_w, radius_bits: int):
+    """Gradients of a loss L through ``fake_quant_weights`` given dL/dW^ [n, k]: the
+    straight-through estimator treats the rounding of the radius as the identity
+    (d r^ / d r = 1), so dL/drho_i = sigmoid(rho_i) * sum_j dL/dw^_ij s_ij c_{z_i, j}, and
+    dL/dc_z = sum over vectors i with z_i = z of r^_i s_i (.) dL/dw^_i. Returns
+    (dL/drho [n, k/8], dL/dcodebook [2^D, 8])."""
+    rho = np.asarray(rho, dtype=np.float64)
+    _r, r_hat, _q = fake_quant_radius(rho, radius_bits)
+    c = np.asarray(codebook, dtype=np.float64)
+    n, nv = rho.shape
+    g = np.asarray(grad_w, dtype=np.float64).reshape(n, nv, VEC)
+    sf = sign_factors(signs)
+    z = np.asarray(dir_idx, dtype=np.int64)
+    d_rhat = np.sum(g * sf * c[z], axis=-1)
+    d_rho = d_rhat / (1.0 + np.exp(-rho))
+    d_c = np.zeros_like(c)
+    np.add.at(d_c, z.reshape(-1), (r_hat[..., None] * sf * g).reshape(-1, VEC))
+    return d_rho, d_c
+
+
+def init_rho(w, dir_idx, codebook) -> np.ndarray:
+    """App. A steps 6-7: the pre-quantisation radius r~ = <|w_i|, c_{z_i}> (Eq. 6) mapped through
+    the inverse of softplus, rho = log(e^r~ - 1). Reading: r~ is floored at 1e-6 so that rho is
+    finite for a zero vector."""
+    w = np.asarray(w, dtype=np.float64)
+    n, k = w.shape
+    c = np.asarray(codebook, dtype=np.float64)
+    rt = ls_radius(np.abs(w.reshape(n, k // VEC, VEC)), c[np.asarray(dir_idx, dtype=np.int64)])
+    rt = np.maximum(rt, 1e-6)
+    return np.log(np.expm1(rt))
 
 
 # ----------------------------------------------------------------- comparison metric

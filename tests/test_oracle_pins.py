@@ -341,6 +341,109 @@ def pin_angular_codebook(o):
     assert np.allclose(o.angular_codebook(np.zeros(7)), np.eye(8)[0])
 
 
+def pin_angular_backward(o):
+    """Eq. 9-10 gradient against central finite differences of sum(g * c(phi)) in fp64, and the
+    inverse map: phi -> c -> phi and c -> phi -> c round trips; an axis direction (zero tail)
+    gives finite logits whose codebook entry is within 2e-4 of the axis."""
+    g = np.random.default_rng(41)
+    phi = g.standard_normal((6, 7)) * 2
+    gc = g.standard_normal((6, 8))
+    d = o.angular_codebook_backward(phi, gc)
+    h = 1e-6
+    for a in range(6):
+        for j in range(7):
+            p, m = phi[a].copy(), phi[a].copy()
+            p[j] += h
+            m[j] -= h
+            fd = (gc[a] @ o.angular_codebook(o.angles_from_logits(p))
+                  - gc[a] @ o.angular_codebook(o.angles_from_logits(m))) / (2 * h)
+            assert abs(fd - d[a, j]) <= 1e-8 * (1 + abs(fd)), (a, j, fd, d[a, j])
+    c = o.angular_codebook(o.angles_from_logits(phi))
+    assert np.allclose(o.logits_from_codebook(c), phi, atol=1e-12)
+    cr = np.abs(g.standard_normal((50, 8))) + 0.05
+    cr /= np.linalg.norm(cr, axis=1, keepdims=True)
+    assert np.allclose(o.angular_codebook(o.angles_from_logits(o.logits_from_codebook(cr))), cr, atol=1e-12)
+    ax = o.logits_from_codebook(np.eye(8)[0])
+    assert np.all(np.isfinite(ax)) and np.all(np.abs(ax) < 14)
+    assert np.allclose(o.angular_codebook(o.angles_from_logits(ax)), np.eye(8)[0], atol=2e-4)
+
+
+def pin_fake_quant_radius(o):
+    """Softplus closed forms; radii on an fp16-exact grid (offset 0.5, step 1/8, V = 4) are
+    reproduced exactly with their levels; a constant group has step 0 and r^ = fp16(r); in
+    general r^ sits within half a stored step (plus the fp16 rounding of offset and step) of r."""
+    assert abs(o.softplus(0.0) - np.log(2.0)) < 1e-16 and abs(o.softplus(50.0) - 50.0) < 1e-15
+    assert abs(o.softplus(-40.0) - np.exp(-40.0)) < 1e-30
+    lv = np.tile(np.arange(16), 2)
+    r = 0.5 + lv / 8.0
+    rho = np.log(np.expm1(r))[None, :]
+    _r, rh, q = o.fake_quant_radius(rho, 4)
+    assert np.array_equal(q[0], lv) and np.array_equal(rh[0], r)
+    _r, rh, q = o.fake_quant_radius(np.full((1, 16), 0.3), 3)
+    assert np.all(q == 0) and np.all(rh == O.f16_to_f64(O.f64_to_f16(o.softplus(0.3))))
+    g = np.random.default_rng(42)
+    rho = g.standard_normal((7, 64)) * 2
+    for v in (2, 3, 4):
+        r, rh, q = o.fake_quant_radius(rho, v)
+        rg = r.reshape(7, 4, 16)
+        lo, hi = rg.min(axis=2), rg.max(axis=2)
+        lo16 = O.f16_to_f64(O.f64_to_f16(lo))
+        st16 = O.f16_to_f64(O.f64_to_f16((hi - lo) / (2**v - 1)))
+        bound = 0.5 * st16 + np.abs(lo16 - lo) + (2**v - 1) * np.abs(st16 - (hi - lo) / (2**v - 1)) + 1e-15
+        assert np.all(np.abs(rh - r).reshape(7, 4, 16) <= bound[..., None])
+        assert q.min() >= 0 and q.max() <= 2**v - 1
+
+
+def pin_fake_quant_backward(o):
+    """Straight-through gradients: dL/dcodebook equals exact finite differences (L is linear in
+    the codebook), dL/drho equals central differences of the unrounded surrogate
+    sum(g * softplus(rho) s (.) c_z), and W^'s vectors have norm r^ ||c_z|| and the code's signs."""
+    g = np.random.default_rng(43)
+    n, k, D, V = 3, 256, 4, 3
+    rho = g.standard_normal((n, k // 8))
+    signs = g.integers(0, 256, (n, k // 8)).astype(np.uint8)
+    z = g.integers(0, 1 << D, (n, k // 8))
+    phi = g.standard_normal((1 << D, 7))
+    c = o.angular_codebook(o.angles_from_logits(phi))
+    gw = g.standard_normal((n, k))
+    w = o.fake_quant_weights(rho, signs, z, c, V)
+    _r, rh, _q = o.fake_quant_radius(rho, V)
+    assert np.allclose(np.linalg.norm(w.reshape(n, -1, 8), axis=2), rh * np.linalg.norm(c[z], axis=2), atol=1e-14)
+    assert np.array_equal(np.signbit(w.reshape(n, -1, 8)) & (rh[..., None] > 0),
+                          (O.sign_factors(signs) < 0) & (rh[..., None] > 0))
+    d_rho, d_c = o.fake_quant_backward(rho, signs, z, c, gw, V)
+    L0 = np.sum(gw * w)
+    for (a, j) in ((0, 0), (3, 5), (int(z[1, 7]), 2)):
+        cp = c.copy()
+        cp[a, j] += 1.0
+        assert abs(np.sum(gw * o.fake_quant_weights(rho, signs, z, cp, V)) - L0 - d_c[a, j]) < 1e-9
+    sf = O.sign_factors(signs)
+
+    def surrogate(rr):
+        return np.sum(gw.reshape(n, -1, 8) * (o.softplus(rr)[..., None] * sf * c[z]))
+    h = 1e-6
+    for (a, b) in ((0, 0), (1, 13), (2, 31)):
+        p, m = rho.copy(), rho.copy()
+        p[a, b] += h
+        m[a, b] -= h
+        fd = (surrogate(p) - surrogate(m)) / (2 * h)
+        assert abs(fd - d_rho[a, b]) <= 1e-7 * (1 + abs(fd))
+
+
+def pin_init_rho(o):
+    """softplus(init_rho) is Eq. 6's radius <|w|, c_z>, floored at 1e-6 for a zero vector."""
+    g = np.random.default_rng(44)
+    w = g.standard_normal((2, 128)) * 0.05
+    w[1, :8] = 0
+    cb = synth.random_codebook(4, synth.rng(45))
+    c = O.f16_to_f64(cb)
+    z = g.integers(0, 16, (2, 16))
+    rt = np.sum(np.abs(w.reshape(2, 16, 8)) * c[z], axis=2)
+    got = o.softplus(o.init_rho(w, z, c))
+    assert np.allclose(got[rt > 0], rt[rt > 0], rtol=1e-12)
+    assert abs(got[1, 0] - 1e-6) < 1e-18
+
+
 def pin_sample_by_squared_radius(o):
     """Sec. 3.1's r^2-proportional sampling: its definition on a tiny input (uniforms chosen away
     from the cumulative boundaries), zero radii never drawn, equal radii give floor(u * N), and
@@ -429,8 +532,9 @@ PINS = [pin_worked_radius, pin_spherical_roundtrip, pin_bit_budget, pin_decompos
         pin_assign, pin_ls_radius, pin_radius_quant, pin_decode_norm_and_sign,
         pin_decode_one_hot, pin_gemm_exact_rational, pin_gemm_special_cases,
         pin_encode_roundtrip_bruteforce, pin_encode_group_params_recovered, pin_w2_layout,
-        pin_angular_codebook, pin_sample_by_squared_radius, pin_spherical_kmeans,
-        pin_kmeans_codebook, pin_rel_err]
+        pin_angular_codebook, pin_angular_backward, pin_fake_quant_radius, pin_fake_quant_backward,
+        pin_init_rho, pin_sample_by_squared_radius, pin_spherical_kmeans, pin_kmeans_codebook,
+        pin_rel_err]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
@@ -534,6 +638,55 @@ def _mut_kmeans_empty_zero(d, init_bits, iters):
     return c, obj
 
 
+def _mut_angular_backward_no_sigmoid(phi, grad_c, eps=1e-4):
+    sg = 1.0 / (1.0 + np.exp(-np.asarray(phi, dtype=np.float64)))
+    return O.angular_codebook_backward(phi, grad_c, eps) / (sg * (1 - sg))
+
+
+def _mut_angular_backward_same_index(phi, grad_c, eps=1e-4):
+    # the j = i term taken with the sign of the later terms
+    phi = np.asarray(phi, dtype=np.float64)
+    th = O.angles_from_logits(phi, eps)
+    g = np.asarray(grad_c, dtype=np.float64)
+    base = O.angular_codebook_backward(phi, grad_c, eps)
+    c = O.angular_codebook(th)
+    sg = 1.0 / (1.0 + np.exp(-phi))
+    extra = 2 * g[..., :7] * c[..., :7] * np.tan(th) * (np.pi / 2 - 2 * eps) * sg * (1 - sg)
+    return base + extra
+
+
+def _mut_logits_swapped(c, eps=1e-4):
+    c = np.asarray(c, dtype=np.float64)
+    tail = np.sqrt(np.cumsum((c * c)[..., ::-1], axis=-1)[..., ::-1])
+    theta = np.arctan2(c[..., :7], tail[..., 1:])
+    t = np.clip((theta - eps) / (np.pi / 2 - 2 * eps), 1e-6, 1 - 1e-6)
+    return np.log(t) - np.log1p(-t)
+
+
+def _mut_fq_backward_no_sigmoid(rho, signs, dir_idx, codebook, grad_w, radius_bits):
+    d_rho, d_c = O.fake_quant_backward(rho, signs, dir_idx, codebook, grad_w, radius_bits)
+    return d_rho * (1.0 + np.exp(-np.asarray(rho, dtype=np.float64))), d_c
+
+
+def _mut_fq_backward_no_radius(rho, signs, dir_idx, codebook, grad_w, radius_bits):
+    d_rho, _ = O.fake_quant_backward(rho, signs, dir_idx, codebook, grad_w, radius_bits)
+    n, nv = np.asarray(rho).shape
+    g = np.asarray(grad_w, dtype=np.float64).reshape(n, nv, 8)
+    d_c = np.zeros_like(np.asarray(codebook, dtype=np.float64))
+    np.add.at(d_c, np.asarray(dir_idx).reshape(-1), (O.sign_factors(signs) * g).reshape(-1, 8))
+    return d_rho, d_c
+
+
+def _mut_fq_radius_no_f16(rho, radius_bits):
+    r = O.softplus(rho)
+    n, nv = r.shape
+    rg = r.reshape(n, nv // 16, 16)
+    lo = rg.min(axis=-1, keepdims=True)
+    st = (rg.max(axis=-1, keepdims=True) - lo) / (2**radius_bits - 1)
+    q = np.clip(np.rint((rg - lo) / np.where(st > 0, st, 1)), 0, 2**radius_bits - 1)
+    return r, (lo + q * st).reshape(n, nv), q.reshape(n, nv).astype(np.uint8)
+
+
 MUTANTS = {
     "sign_bit_order": dict(sign_factors=_mut_sign_order),
     "dropped_group_offset": dict(dequantize_radius=_mut_drop_min),
@@ -547,6 +700,12 @@ MUTANTS = {
     "sample_by_radius": dict(sample_by_squared_radius=_mut_sample_by_radius),
     "kmeans_mean_not_normalised": dict(spherical_kmeans=_mut_kmeans_mean),
     "kmeans_empty_centre_zero": dict(spherical_kmeans=_mut_kmeans_empty_zero),
+    "angular_backward_no_sigmoid": dict(angular_codebook_backward=_mut_angular_backward_no_sigmoid),
+    "angular_backward_same_index_sign": dict(angular_codebook_backward=_mut_angular_backward_same_index),
+    "logits_swapped_atan2": dict(logits_from_codebook=_mut_logits_swapped),
+    "fake_quant_backward_no_sigmoid": dict(fake_quant_backward=_mut_fq_backward_no_sigmoid),
+    "fake_quant_backward_no_radius": dict(fake_quant_backward=_mut_fq_backward_no_radius),
+    "fake_quant_radius_unrounded_params": dict(fake_quant_radius=_mut_fq_radius_no_f16),
 }
 
 

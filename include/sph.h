@@ -181,6 +181,73 @@ sph_status sph_kmeans_codebook(const sph_format* fmt, int64_t n, int64_t k, cons
                                const uint16_t* d_init, uint16_t* d_codebook, double* d_objective,
                                int64_t* d_sample_idx, void* d_ws, size_t ws_bytes, void* stream);
 
+/* ---- Fine-tuning side (Sec. 3.3; App. A steps 6-10). fp32 device arrays unless stated. ---- */
+
+/* Angular codebook (Sec. 3.3, Eq. 9-10): for each of the 2^D entries, seven angle logits phi
+ * (d_phi fp32[2^D][7]) give theta_j = eps + (pi/2 - 2 eps) sigmoid(phi_j) and the positive unit
+ * direction c_1 = cos t_1, c_i = (prod_{j<i} sin t_j) cos t_i (2 <= i <= 7), c_8 = prod_j sin t_j,
+ * written to d_codebook fp32[2^D][8]. 1 <= dir_bits <= 13, 0 <= eps < 0.25. Asynchronous. */
+sph_status sph_angular_codebook(int32_t dir_bits, const float* d_phi, float eps, float* d_codebook, void* stream);
+
+/* Gradient of a loss through sph_angular_codebook: d_grad_codebook fp32[2^D][8] (dL/dc) gives
+ * d_grad_phi fp32[2^D][7] (dL/dphi), from the closed-form derivatives of Eq. 9 and Eq. 10. */
+sph_status sph_angular_codebook_backward(int32_t dir_bits, const float* d_phi, float eps,
+                                         const float* d_grad_codebook, float* d_grad_phi, void* stream);
+
+/* Inverse of Eq. 9-10 (initialises the angle logits from a codebook, App. A step 7):
+ * theta_i = atan2(||c_{i+1..8}||, c_i), t = (theta - eps)/(pi/2 - 2 eps) clamped to
+ * [1e-6, 1 - 1e-6], phi = log t - log(1 - t). d_codebook fp32[2^D][8] of non-negative unit
+ * directions; d_phi fp32[2^D][7]. */
+sph_status sph_angular_logits(int32_t dir_bits, const float* d_codebook, float eps, float* d_phi, void* stream);
+
+/* Host-only, synchronous: the vectors grouped by direction index, for the codebook gradient
+ * of sph_fake_quant_backward. dir_idx: host uint16[count] (< 2^D); perm: host int32[count]
+ * receives the vector indices sorted by direction, stably (ascending index within a
+ * direction); offsets: host int64[2^D + 1], direction z owns perm[offsets[z] .. offsets[z+1]).
+ * 1 <= count < 2^31. SPH_ERR_CODE_RANGE for an index >= 2^D. */
+sph_status sph_direction_groups(int32_t dir_bits, int64_t count, const uint16_t* dir_idx, int32_t* perm,
+                                int64_t* offsets);
+
+/* Radius parameters from a dense matrix (App. A steps 6-7): rho_i = log(exp(r~_i) - 1), the
+ * inverse of softplus, of Eq. 6's radius r~_i = <|w_i|, c_{z_i}> floored at 1e-6. d_w fp32[n][ldw]
+ * (ldw >= k, ldw % 4 == 0, 16-byte aligned), d_dir_idx uint16[n][k/8], d_codebook fp32[2^D][8]
+ * (16-byte aligned), d_rho fp32[n][k/8]. */
+sph_status sph_fake_quant_init_rho(const sph_format* fmt, int64_t n, int64_t k, const float* d_w, int64_t ldw,
+                                   const uint16_t* d_dir_idx, const float* d_codebook, float* d_rho, void* stream);
+
+/* The pseudo-quantised weight of a linear module (Sec. 3.3; App. A step 8): r = softplus(rho),
+ * group-wise V-bit fake quantisation with Eq. 7's offset min_G and step (max_G - min_G)/(2^V - 1),
+ * both rounded to fp16 as the finalised codes store them, q = clip(round((r - min_G)/step_G),
+ * 0, 2^V - 1) half to even (0 for a zero step), r^ = min_G + q step_G, and w^_i = r^_i s_i (.)
+ * c_{z_i} written to d_w_hat fp32[n][ldw] (ldw >= k, ldw % 4 == 0, 16-byte aligned). The radius,
+ * offset, step and level are computed in fp64. d_rho fp32[n][k/8]; d_signs, d_dir_idx as in
+ * sph_pack_weights; d_codebook fp32[2^D][8] (e.g. from sph_angular_codebook), not validated.
+ * Optional outputs (NULL to skip): d_r_hat fp32[n][k/8] (needed by the backward), and together
+ * d_radius_code uint8[n][k/8], d_group_min, d_group_step fp16 bits [n][k/128] -- the finalised
+ * codes of App. A step 10. Asynchronous; results do not depend on the launch. */
+sph_status sph_fake_quant_forward(const sph_format* fmt, int64_t n, int64_t k, const float* d_rho,
+                                  const uint8_t* d_signs, const uint16_t* d_dir_idx, const float* d_codebook,
+                                  float* d_w_hat, int64_t ldw, float* d_r_hat, uint8_t* d_radius_code,
+                                  uint16_t* d_group_min, uint16_t* d_group_step, void* stream);
+
+/* Device workspace of sph_fake_quant_backward for a 2^D-entry codebook (needs no zero-fill). */
+sph_status sph_fake_quant_backward_workspace_bytes(int32_t dir_bits, size_t* bytes);
+
+/* Gradients through sph_fake_quant_forward with the straight-through estimator (the rounding of
+ * the radius is taken as the identity): given d_grad_w fp32[n][ldg] (dL/dW^; ldg >= k,
+ * ldg % 4 == 0, 16-byte aligned), writes d_grad_rho fp32[n][k/8] with
+ * dL/drho_i = sigmoid(rho_i) sum_j dL/dw^_ij s_ij c_{z_i,j}, and d_grad_codebook fp32[2^D][8]
+ * with dL/dc_z = sum over vectors i of direction z of r^_i s_i (.) dL/dw^_i. d_r_hat is the
+ * forward's r^; d_perm int32[n*k/8] and d_offsets int64[2^D + 1] are device copies of
+ * sph_direction_groups for the same d_dir_idx (not validated). Sums run in a fixed order without
+ * atomics, so repeated calls give bitwise identical results. d_ws: sph_fake_quant_backward_
+ * workspace_bytes bytes, 16-byte aligned. Asynchronous. */
+sph_status sph_fake_quant_backward(const sph_format* fmt, int64_t n, int64_t k, const float* d_rho,
+                                   const uint8_t* d_signs, const uint16_t* d_dir_idx, const float* d_codebook,
+                                   const float* d_r_hat, const float* d_grad_w, int64_t ldg, const int32_t* d_perm,
+                                   const int64_t* d_offsets, float* d_grad_rho, float* d_grad_codebook, void* d_ws,
+                                   size_t ws_bytes, void* stream);
+
 /* Whether (dir_bits, radius_bits) is one of the built-in formats: 1 yes, 0 no. */
 int sph_format_supported(const sph_format* fmt);
 

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = [os.path.join(CSRC, "sph_kernels.hip"), os.path.join(CSRC, "sph_encode.hip"),
-           os.path.join(CSRC, "sph_pack.cpp")]
+           os.path.join(CSRC, "sph_train.hip"), os.path.join(CSRC, "sph_pack.cpp")]
 OUT = os.path.join(HERE, "libsph.so")
 
 HIPCC_FLAGS = [

@@ -26,7 +26,10 @@ STATUS = {
 # Every symbol include/sph.h declares.
 EXPORTS = ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
            "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
-           "sph_kmeans_codebook", "sph_format_supported", "sph_status_str")
+           "sph_kmeans_codebook", "sph_angular_codebook", "sph_angular_codebook_backward",
+           "sph_angular_logits", "sph_direction_groups", "sph_fake_quant_init_rho",
+           "sph_fake_quant_forward", "sph_fake_quant_backward_workspace_bytes",
+           "sph_fake_quant_backward", "sph_format_supported", "sph_status_str")
 
 FORMATS = {
     "W2": (6, 4), "W3": (13, 3), "W2_cfg": (4, 4), "W3_cfg": (8, 8), "W2_16": (6, 2),
@@ -78,13 +81,25 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sph_kmeans_workspace_bytes.argtypes = [pf, I64, I64, I64, ctypes.POINTER(SZ)]
     lib.sph_kmeans_codebook.argtypes = [pf, I64, I64, P, I64, P, I64, ctypes.c_int32, P, P, P, P,
                                         P, SZ, P]
+    F = ctypes.c_float
+    lib.sph_angular_codebook.argtypes = [I32, P, F, P, P]
+    lib.sph_angular_codebook_backward.argtypes = [I32, P, F, P, P, P]
+    lib.sph_angular_logits.argtypes = [I32, P, F, P, P]
+    lib.sph_direction_groups.argtypes = [I32, I64, P, P, P]
+    lib.sph_fake_quant_init_rho.argtypes = [pf, I64, I64, P, I64, P, P, P, P]
+    lib.sph_fake_quant_forward.argtypes = [pf, I64, I64, P, P, P, P, P, I64, P, P, P, P, P]
+    lib.sph_fake_quant_backward_workspace_bytes.argtypes = [I32, ctypes.POINTER(SZ)]
+    lib.sph_fake_quant_backward.argtypes = [pf, I64, I64, P, P, P, P, P, P, I64, P, P, P, P, P, SZ, P]
     lib.sph_format_supported.argtypes = [pf]
     lib.sph_format_supported.restype = I32
     lib.sph_status_str.argtypes = [I32]
     lib.sph_status_str.restype = ctypes.c_char_p
     for name in ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
                  "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
-                 "sph_kmeans_codebook"):
+                 "sph_kmeans_codebook", "sph_angular_codebook", "sph_angular_codebook_backward",
+                 "sph_angular_logits", "sph_direction_groups", "sph_fake_quant_init_rho",
+                 "sph_fake_quant_forward", "sph_fake_quant_backward_workspace_bytes",
+                 "sph_fake_quant_backward"):
         getattr(lib, name).restype = I32
     _lib = lib
     return lib
@@ -309,3 +324,114 @@ def kmeans_codebook(dir_bits: int, radius_bits: int, w, u, init, iters: int = 20
         workspace.data_ptr(), workspace.numel(), _stream_handle(stream))
     _check(st, "sph_kmeans_codebook")
     return cb, obj, idx
+
+
+# ------------------------------------------------------------------ fine-tuning side
+
+ANGLE_EPS = 1e-4
+
+
+def _ptr(t):
+    return t.data_ptr() if t is not None else None
+
+
+def angular_codebook(dir_bits: int, phi, eps: float = ANGLE_EPS, out=None, stream=None):
+    """Eq. 9-10 on the device: fp32 logits [2^D][7] -> fp32 codebook [2^D][8]."""
+    import torch
+    phi = phi.contiguous()
+    if out is None:
+        out = torch.empty((1 << dir_bits, 8), dtype=torch.float32, device=phi.device)
+    _check(load_library().sph_angular_codebook(dir_bits, phi.data_ptr(), eps, out.data_ptr(),
+                                               _stream_handle(stream)), "sph_angular_codebook")
+    return out
+
+
+def angular_codebook_backward(dir_bits: int, phi, grad_c, eps: float = ANGLE_EPS, stream=None):
+    import torch
+    phi, grad_c = phi.contiguous(), grad_c.contiguous()
+    out = torch.empty_like(phi)
+    _check(load_library().sph_angular_codebook_backward(dir_bits, phi.data_ptr(), eps, grad_c.data_ptr(),
+                                                        out.data_ptr(), _stream_handle(stream)),
+           "sph_angular_codebook_backward")
+    return out
+
+
+def angular_logits(dir_bits: int, codebook, eps: float = ANGLE_EPS, stream=None):
+    """Inverse of Eq. 9-10 on the device: fp32 codebook [2^D][8] -> logits [2^D][7]."""
+    import torch
+    cb = codebook.contiguous()
+    out = torch.empty((1 << dir_bits, 7), dtype=torch.float32, device=cb.device)
+    _check(load_library().sph_angular_logits(dir_bits, cb.data_ptr(), eps, out.data_ptr(),
+                                             _stream_handle(stream)), "sph_angular_logits")
+    return out
+
+
+def direction_groups(dir_bits: int, dir_idx) -> tuple:
+    """Host: (perm int32[count], offsets int64[2^D + 1]) of the vectors sorted by direction."""
+    d = np.ascontiguousarray(np.asarray(dir_idx).reshape(-1), dtype=np.uint16)
+    perm = np.empty(d.size, dtype=np.int32)
+    off = np.empty((1 << dir_bits) + 1, dtype=np.int64)
+    _check(load_library().sph_direction_groups(dir_bits, d.size, d.ctypes.data, perm.ctypes.data,
+                                               off.ctypes.data), "sph_direction_groups")
+    return perm, off
+
+
+def fake_quant_init_rho(dir_bits: int, radius_bits: int, w, dir_idx, codebook, stream=None):
+    import torch
+    w = _dev_f32_matrix(w)
+    n, k = w.shape
+    rho = torch.empty((n, k // 8), dtype=torch.float32, device=w.device)
+    _check(load_library().sph_fake_quant_init_rho(
+        ctypes.byref(make_format(dir_bits, radius_bits)), n, k, w.data_ptr(), w.stride(0),
+        dir_idx.contiguous().data_ptr(), codebook.contiguous().data_ptr(), rho.data_ptr(),
+        _stream_handle(stream)), "sph_fake_quant_init_rho")
+    return rho
+
+
+def fake_quant_forward(dir_bits: int, radius_bits: int, rho, signs, dir_idx, codebook,
+                       want_codes: bool = False, stream=None):
+    """W^ (fp32 [n][k]) and r^ (fp32 [n][k/8]); with ``want_codes`` also the finalised levels
+    and fp16 group parameters."""
+    import torch
+    n, nv = rho.shape
+    k = nv * 8
+    dev = rho.device
+    w = torch.empty((n, k), dtype=torch.float32, device=dev)
+    r_hat = torch.empty((n, nv), dtype=torch.float32, device=dev)
+    q = gmin = gstep = None
+    if want_codes:
+        q = torch.empty((n, nv), dtype=torch.uint8, device=dev)
+        gmin = torch.empty((n, k // 128), dtype=torch.int16, device=dev)
+        gstep = torch.empty((n, k // 128), dtype=torch.int16, device=dev)
+    _check(load_library().sph_fake_quant_forward(
+        ctypes.byref(make_format(dir_bits, radius_bits)), n, k, rho.contiguous().data_ptr(),
+        signs.contiguous().data_ptr(), dir_idx.contiguous().data_ptr(), codebook.contiguous().data_ptr(),
+        w.data_ptr(), k, r_hat.data_ptr(), _ptr(q), _ptr(gmin), _ptr(gstep), _stream_handle(stream)),
+        "sph_fake_quant_forward")
+    if want_codes:
+        return w, r_hat, {"q": q, "gmin": gmin, "gstep": gstep}
+    return w, r_hat
+
+
+def fake_quant_backward(dir_bits: int, radius_bits: int, rho, signs, dir_idx, codebook, r_hat, grad_w,
+                        perm, offsets, workspace=None, stream=None):
+    """(dL/drho fp32 [n][k/8], dL/dcodebook fp32 [2^D][8]) with the straight-through estimator."""
+    import torch
+    n, nv = rho.shape
+    k = nv * 8
+    dev = rho.device
+    nb = ctypes.c_size_t(0)
+    _check(load_library().sph_fake_quant_backward_workspace_bytes(dir_bits, ctypes.byref(nb)),
+           "sph_fake_quant_backward_workspace_bytes")
+    if workspace is None or workspace.numel() < nb.value:
+        workspace = torch.empty(nb.value, dtype=torch.uint8, device=dev)
+    grad_w = grad_w.contiguous()
+    g_rho = torch.empty_like(rho)
+    g_cb = torch.empty((1 << dir_bits, 8), dtype=torch.float32, device=dev)
+    _check(load_library().sph_fake_quant_backward(
+        ctypes.byref(make_format(dir_bits, radius_bits)), n, k, rho.contiguous().data_ptr(),
+        signs.contiguous().data_ptr(), dir_idx.contiguous().data_ptr(), codebook.contiguous().data_ptr(),
+        r_hat.contiguous().data_ptr(), grad_w.data_ptr(), grad_w.stride(0), perm.data_ptr(),
+        offsets.data_ptr(), g_rho.data_ptr(), g_cb.data_ptr(), workspace.data_ptr(), workspace.numel(),
+        _stream_handle(stream)), "sph_fake_quant_backward")
+    return g_rho, g_cb

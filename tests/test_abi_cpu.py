@@ -198,3 +198,40 @@ def test_kmeans_workspace_and_validation():
     assert st(ns=0) == 2 and st(ns=(1 << 24) + 1) == 2 and st(iters=-1) == 2 and st(iters=10001) == 2
     assert st(ws=0x100080) == 2 and st(u=0x10004) == 2 and st(ldw=k - 4) == 2
     assert st(ws_bytes=pkg.kmeans_workspace_bytes(6, 4, n, k, 1000) - 1) == 6
+
+
+@needs_lib
+def test_direction_groups_host_counting_sort():
+    z = np.random.default_rng(5).integers(0, 64, 10000).astype(np.uint16)
+    perm, off = B.direction_groups(6, z)
+    assert np.array_equal(perm, np.argsort(z, kind="stable"))
+    assert np.array_equal(off, np.concatenate([[0], np.cumsum(np.bincount(z, minlength=64))]))
+    with pytest.raises(pkg.SphError) as e:
+        B.direction_groups(4, z)                # indices >= 16
+    assert e.value.status == 4
+
+
+@needs_lib
+def test_training_entry_points_validate_before_any_hip_call():
+    lib = pkg.load_library()
+    f = B.make_format(6, 4)
+    assert lib.sph_angular_codebook(0, 0x1000, 1e-4, 0x2000, None) == 2
+    assert lib.sph_angular_codebook(14, 0x1000, 1e-4, 0x2000, None) == 2
+    assert lib.sph_angular_codebook(6, 0x1000, 0.3, 0x2000, None) == 2
+    assert lib.sph_angular_codebook(6, None, 1e-4, 0x2000, None) == 1
+    assert lib.sph_angular_logits(6, 0x1000, 1e-4, None, None) == 1
+    P = 0x10000
+    assert lib.sph_fake_quant_forward(ctypes.byref(f), 16, 100, P, P, P, P, P, 128, None, None, None, None, None) == 2
+    assert lib.sph_fake_quant_forward(ctypes.byref(f), 16, 128, P, P, P, P, P, 120, None, None, None, None, None) == 2
+    assert lib.sph_fake_quant_forward(ctypes.byref(f), 16, 128, P, P, P, P, P, 128, None, P, None, None, None) == 1
+    assert lib.sph_fake_quant_forward(ctypes.byref(f), 16, 128, P, P, P, P, P + 8, 128, None, None, None, None,
+                                      None) == 2
+    assert lib.sph_fake_quant_forward(ctypes.byref(B.make_format(7, 4)), 16, 128, P, P, P, P, P, 128, None, None,
+                                      None, None, None) == 3
+    nb = ctypes.c_size_t(0)
+    assert lib.sph_fake_quant_backward_workspace_bytes(13, ctypes.byref(nb)) == 0 and nb.value == 8192 * 32
+    assert lib.sph_fake_quant_backward_workspace_bytes(6, ctypes.byref(nb)) == 0 and nb.value == 64 * 16 * 32
+    assert lib.sph_fake_quant_backward(ctypes.byref(f), 16, 128, P, P, P, P, P, P, 128, P, P, P, P, P,
+                                       64 * 16 * 32 - 1, None) == 6
+    assert lib.sph_fake_quant_backward(ctypes.byref(f), 16, 128, P, P, P, P, P, P, 128, P, P, P, P, None,
+                                       1 << 20, None) == 1

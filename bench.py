@@ -68,8 +68,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
     ap.add_argument("--unfused", action="store_true", help="launch q, k, v, gate, up separately")
-    ap.add_argument("--path", default="decode", choices=("decode", "encode"),
-                    help="decode: the default benchmark; encode: device encoder and k-means codebook")
+    ap.add_argument("--path", default="decode", choices=("decode", "encode", "train"),
+                    help="decode: the default benchmark; encode: device encoder and k-means codebook; "
+                         "train: pseudo-quantised weight rebuild and its straight-through backward")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (HBM counter calibration)")
     return ap.parse_args()
@@ -229,6 +230,96 @@ def encode_main(args):
     print(json.dumps(out), flush=True)
 
 
+def train_main(args):
+    """Fine-tuning benchmark: a step rebuilds the pseudo-quantised weight of one 12288x4096 layer
+    (angular codebook, softplus radius, group fake quantisation, w^ = r^ s (.) c_z) and runs its
+    straight-through backward (radius and codebook gradients, then the angle-logit gradient).
+    The dominant kernel is the weight rebuild, bound by HBM: per 8-D vector it reads rho (4 B),
+    signs (1 B) and the direction index (2 B) and writes w^ (32 B) and r^ (4 B)."""
+    import torch
+
+    from paper_2609_24875_amd import sph as B
+
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    fmt = args.fmt or "W2"
+    D, V = synth.FORMATS[fmt]
+    n, k = 12288, 4096
+    nv = k // 8
+    g = np.random.default_rng(8)
+    rho = (g.standard_normal((n, nv)) - 3.0).astype(np.float32)
+    signs = g.integers(0, 256, (n, nv)).astype(np.uint8)
+    z = g.integers(0, 1 << D, (n, nv)).astype(np.uint16)
+    phi = (g.standard_normal((1 << D, 7))).astype(np.float32)
+    gw = (g.standard_normal((n, k)) * 1e-3).astype(np.float32)
+    perm, off = B.direction_groups(D, z)
+    t = {key: torch.from_numpy(np.ascontiguousarray(v)).to(dev)
+         for key, v in dict(rho=rho, signs=signs, z=z.view(np.int16), phi=phi, gw=gw, perm=perm, off=off).items()}
+    c = B.angular_codebook(D, t["phi"])
+    w, r_hat = B.fake_quant_forward(D, V, t["rho"], t["signs"], t["z"], c)
+    ws = torch.empty(1 << 22, dtype=torch.uint8, device=dev)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    for _ in range(args.warmup):
+        B.fake_quant_forward(D, V, t["rho"], t["signs"], t["z"], c)
+    fwd_ms = timed(lambda: B.fake_quant_forward(D, V, t["rho"], t["signs"], t["z"], c), args.steps)
+    bwd_ms = timed(lambda: B.fake_quant_backward(D, V, t["rho"], t["signs"], t["z"], c, r_hat, t["gw"],
+                                                 t["perm"], t["off"], workspace=ws), args.steps)
+    ang_ms = timed(lambda: B.angular_codebook_backward(D, t["phi"], B.angular_codebook(D, t["phi"])), args.steps)
+    nvec = n * nv
+    fwd_bytes = nvec * (4 + 1 + 2 + 32 + 4)
+    bwd_bytes = nvec * ((32 + 2 + 1 + 4 + 4) + (4 + 32 + 4 + 1))
+    step_ms = fwd_ms + bwd_ms + ang_ms
+    out = {
+        "metric": "pseudo-quantised weight rebuild + straight-through backward: algorithmic GB/s",
+        "value": round((fwd_bytes + bwd_bytes) / (step_ms / 1e3) / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32 weights and gradients, f64 level decisions",
+        "data": "synthetic: N(-3, 1) radius parameters, uniform signs and directions, N(0, 1) angle "
+                "logits, N(0, 1e-6) weight gradients",
+        "config": {"workload": f"finetune-{fmt}-{n}x{k}", "format": f"{fmt} (8 sign + {D} direction + {V} "
+                   f"radius bits)", "forward_ms": round(fwd_ms, 4), "backward_ms": round(bwd_ms, 4),
+                   "angular_fwd_bwd_ms": round(ang_ms, 4), "backward_bytes": bwd_bytes},
+        "roofline": {"kernel": f"k_fq_forward {fmt} {n}x{k}", "bound": "hbm",
+                     "achieved": round(fwd_bytes / (fwd_ms / 1e3) / 1e9, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(fwd_bytes / (fwd_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": fwd_bytes},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import sph as O
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            threads = int(os.environ.get("OMP_NUM_THREADS") or os.cpu_count())
+        c64 = c.cpu().numpy().astype(np.float64)
+        rows, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < args.cpu_sample_seconds and rows < n:
+            sl = slice(rows, rows + 256)
+            O.fake_quant_weights(rho[sl].astype(np.float64), signs[sl], z[sl], c64, V)
+            O.fake_quant_backward(rho[sl].astype(np.float64), signs[sl], z[sl], c64, gw[sl].astype(np.float64), V)
+            rows += 256
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round((fwd_bytes + bwd_bytes) * rows / n / dt / 1e9, 4), "unit": "GB/s",
+                               "cores": int(threads), "kind": "oracle",
+                               "sample": f"oracle forward + backward of the first {rows} of {n} rows in {dt:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -237,6 +328,8 @@ def main():
         sys.exit(2)
     if args.path == "encode":
         return encode_main(args)
+    if args.path == "train":
+        return train_main(args)
     import torch
 
     import paper_2609_24875_amd as pkg

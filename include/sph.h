@@ -116,11 +116,22 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
                           int64_t ldy, sph_dtype y_dtype, void* d_ws, size_t ws_bytes,
                           void* stream);
 
-/* Device workspace needed by sph_gemv (m = 1) or sph_gemm_small for this matrix and batch on
- * the current device (0 when the call needs none; d_ws may then be NULL). The workspace holds
- * split-K partial sums and one arrival counter per 16-row tile: it must be 256-byte aligned and
- * zero-filled before its first use, every call leaves it zero-filled again, and calls that may
- * run concurrently must not share one. */
+/* Y = X W^T for any batch 1 <= m <= 65536 (prefill and large batches): m <= 32 is sph_gemm_small;
+ * larger batches run on the matrix cores (16x16x32 fp16 MFMA, fp32 accumulation) with each
+ * weight rebuilt as fp16(r * t) once per 64- or 128-row slice of X (128 for the nibble formats,
+ * 64 for D = 13) and per 128-column chunk of K. Same argument rules as sph_gemm_small. When the
+ * grid would not cover the chip, K is split and fp32 partial outputs go through the workspace
+ * (sph_workspace_bytes(w, m); for m > 32 it needs no zero-fill) and are added in a fixed order,
+ * so repeated calls give bitwise identical results. Asynchronous on `stream`. */
+sph_status sph_gemm(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y, int64_t ldy,
+                    sph_dtype y_dtype, void* d_ws, size_t ws_bytes, void* stream);
+
+/* Device workspace needed by sph_gemv (m = 1), sph_gemm_small or sph_gemm for this matrix and
+ * batch (1 <= m <= 65536) on the current device (0 when the call needs none; d_ws may then be
+ * NULL). For m <= 32 the workspace holds split-K partial sums and one arrival counter per 16-row
+ * tile: it must be 256-byte aligned and zero-filled before its first use, every call leaves it
+ * zero-filled again. For m > 32 it holds fp32 partial outputs and needs no initial contents.
+ * Calls that may run concurrently must not share one. */
 sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes);
 
 /* Read the packed matrix back as logical codes, on the device, with the same bit extraction the

@@ -55,6 +55,10 @@ struct KArgs {
   int pmax;           // slot parts per tile
   int ts;
   uint64_t* ws_slot;  // [nt][pmax][M][16] tagged partial sums of split tiles, zero between calls
+  // prefill path (batch > 32): K split into ks ranges; with ks > 1 each range writes fp32 partial
+  // outputs [ks][m][nt * 16] to ws_part and a second kernel adds them in range order
+  int ks;
+  float* ws_part;
 };
 
 // ------------------------------------------------------------------------------------------
@@ -882,6 +886,180 @@ __global__ void __launch_bounds__(256) k_unpack(KArgs a, uint8_t* signs, uint16_
 }
 
 // ------------------------------------------------------------------------------------------
+// Prefill kernel (batch > 32): Y = X W^T on 16x16x32 MFMA tiles with the weights rebuilt once per
+// workgroup and k-chunk.
+//
+// A workgroup of PF_WAVES waves owns PF_TPW 16-row tiles per wave and MC batch rows (one grid
+// column per MC-row slice of X), and walks K in chunks of 128 (16 vector positions = one radius
+// group). Per chunk the X slice [MC][128] is staged in LDS (rows padded by 16 bytes against bank
+// conflicts); each lane rebuilds, for each of its tiles, row lane % 16 at positions 4i + lane / 16
+// (i = 0..3) as fp16(r * t) -- the operand layout of the batch 9..32 tile mode -- and every rebuilt
+// operand meets all MC / 16 column blocks of X, each X fragment serving both tiles. With ks > 1
+// the grid's third dimension splits K and the partial outputs are added in range order by
+// k_prefill_reduce. The order of every sum is fixed, so results are reproducible.
+// ------------------------------------------------------------------------------------------
+constexpr int PF_WAVES = 4;
+constexpr int PF_TPW = 2;
+constexpr int PF_THREADS = 64 * PF_WAVES;
+constexpr int PF_XROW = 128 * 2 + 16;   // bytes per staged X row (128 fp16 + padding)
+#define SPH_MAX_BATCH 65536
+
+template <int KIND>
+constexpr int pf_mc() { return IS_CB<KIND> ? 64 : 128; }
+
+template <int KIND, int D>
+struct PfLds {
+  static constexpr uint32_t tables = Tables<KIND, D>::bytes;
+  static constexpr uint32_t x_off = (tables + 15u) / 16u * 16u;
+  static constexpr uint32_t bytes = x_off + pf_mc<KIND>() * PF_XROW;
+};
+
+template <int KIND, int D>
+__device__ __forceinline__ uint4 pf_rebuild(const uint32_t ra, const uint32_t rb, const uint32_t rc, float lo,
+                                            float st, const unsigned char* lds, uint32_t mask_off, int r) {
+  uint4 tt;
+  uint32_t q;
+  if constexpr (IS_CB<KIND>) {
+    uint32_t sg, z;
+    decode_cb13(ra, r % 4, rb, r & 1, sg, z, q);
+    if constexpr (KIND == SPH_KIND_CB13Q4) q |= ((rc >> r) & 1u) << 3;
+    tt = signed_dir_cb13(lds, mask_off, sg, z);
+  } else {
+    uint32_t l, hh, qx = 0;
+    if constexpr (KIND == SPH_KIND_W2) qx = (rb >> (4 * (r / 2))) & 15u;
+    if constexpr (KIND == SPH_KIND_NIB16Q2) qx = (rb >> (2 * r)) & 3u;
+    if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (rb >> (8 * (r % 4))) & 0xFFu;
+    decode_nib<KIND, D>(ra, r & 1, qx, l, hh, q);
+    tt = signed_dir_nib<KIND, D>(lds, l, hh);
+  }
+  return scale_dir(tt, fmaf((float)q, st, lo));   // fp16(r * t), one rounding
+}
+
+template <int KIND, int D>
+__global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
+  constexpr int MC = pf_mc<KIND>();
+  constexpr int NB = MC / 16;
+  constexpr bool B1 = KIND == SPH_KIND_W2 || KIND == SPH_KIND_NIB16Q2;
+  constexpr int ADW_REC = IS_CB<KIND> ? 4 : 8;
+  constexpr int BDW_REC = B1 ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
+  __shared__ __align__(16) unsigned char lds[PfLds<KIND, D>::bytes];
+  unsigned char* xl = lds + PfLds<KIND, D>::x_off;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane & 15, j = lane >> 4;
+  const int mc0 = blockIdx.y * MC;
+  const int nc = a.ng;
+  const int c0 = (int)((int64_t)nc * blockIdx.z / a.ks), c1 = (int)((int64_t)nc * (blockIdx.z + 1) / a.ks);
+  // lookup tables (and, for the codebook kinds, the sign masks) into LDS
+  {
+    const int n16 = (int)((Tables<KIND, D>::bytes - (IS_CB<KIND> ? 128u : 0u)) / 16u);
+    for (int t = threadIdx.x; t < n16; t += PF_THREADS) ((uint4*)lds)[t] = a.T[t];
+    if constexpr (IS_CB<KIND>) {
+      if (threadIdx.x < 16) {
+        const uint32_t sm = threadIdx.x;
+        uint2 mk;
+        mk.x = ((sm & 1u) << 15) | ((sm & 2u) << 30);
+        mk.y = ((sm & 4u) << 13) | ((sm & 8u) << 28);
+        *(uint2*)(lds + a.t_bytes + sm * 8u) = mk;
+      }
+    }
+  }
+  int tile[PF_TPW];
+  bool act[PF_TPW];
+#pragma unroll
+  for (int u = 0; u < PF_TPW; ++u) {
+    tile[u] = ((int)blockIdx.x * PF_WAVES + wave) * PF_TPW + u;
+    act[u] = tile[u] < a.nt;
+    if (!act[u]) tile[u] = a.nt - 1;   // inactive tiles read valid records and store nothing
+  }
+  float acc[PF_TPW][NB][4];
+#pragma unroll
+  for (int u = 0; u < PF_TPW; ++u)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[u][nb][e] = 0.0f;
+  const int adw = IS_CB<KIND> ? r / 4 : r / 2;
+  const int bdw = B1 ? 0 : (KIND == SPH_KIND_NIB16Q8) ? r / 4 : r / 2;
+  for (int c = c0; c < c1; ++c) {
+    // this chunk's codes and group parameters for the lane's rows
+    uint32_t ra[PF_TPW][4], rb[PF_TPW][4], rc[PF_TPW][4], pw[PF_TPW];
+#pragma unroll
+    for (int u = 0; u < PF_TPW; ++u) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t rec = (int64_t)tile[u] * a.nv + c * 16 + 4 * i + j;
+        ra[u][i] = a.A[rec * ADW_REC + adw];
+        if constexpr (KIND != SPH_KIND_NIB16) rb[u][i] = a.B[rec * BDW_REC + bdw];
+        else rb[u][i] = 0;
+        if constexpr (KIND == SPH_KIND_CB13Q4) rc[u][i] = a.C[rec];
+        else rc[u][i] = 0;
+      }
+      pw[u] = a.P[((int64_t)tile[u] * a.ng + c) * 16 + r];
+    }
+    __syncthreads();   // the previous chunk's X is no longer read (and the tables are in place)
+    // stage X[mc0 .. mc0 + MC)[c*128 .. c*128 + 128) as fp16; rows past the batch repeat the last
+    // row (their outputs are never stored)
+    for (int t = threadIdx.x; t < MC * 16; t += PF_THREADS) {
+      const int row = t >> 4, piece = t & 15;
+      const int b = min(mc0 + row, a.m - 1);
+      const uint4 v = *(const uint4*)(a.x + (int64_t)b * a.ldx + (int64_t)c * 128 + piece * 8);
+      *(uint4*)(xl + row * PF_XROW + piece * 16) = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint4 w[PF_TPW];
+#pragma unroll
+      for (int u = 0; u < PF_TPW; ++u)
+        w[u] = pf_rebuild<KIND, D>(ra[u][i], rb[u][i], rc[u][i], f16lo(pw[u]), f16hi(pw[u]), lds, a.t_bytes, r);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const uint4 xb = *(const uint4*)(xl + (16 * nb + r) * PF_XROW + (4 * i + j) * 16);
+#pragma unroll
+        for (int u = 0; u < PF_TPW; ++u) {
+          f32x4 d = {acc[u][nb][0], acc[u][nb][1], acc[u][nb][2], acc[u][nb][3]};
+          d = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, w[u]), __builtin_bit_cast(f16x8, xb),
+                                                     d, 0, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[u][nb][e] = d[e];
+        }
+      }
+    }
+  }
+  // D[row][col] of a 16x16 block: lane holds col lane % 16 (batch row) and rows 4 * (lane / 16) + e
+#pragma unroll
+  for (int u = 0; u < PF_TPW; ++u) {
+    if (!act[u]) continue;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int b = mc0 + 16 * nb + r;
+      if (b >= a.m) continue;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = tile[u] * 16 + 4 * j + e;
+        if (a.ks > 1) {
+          a.ws_part[((int64_t)blockIdx.z * a.m + b) * ((int64_t)a.nt * 16) + row] = acc[u][nb][e];
+        } else if (row < a.n) {
+          store_y(a, b, row, acc[u][nb][e]);
+        }
+      }
+    }
+  }
+}
+
+// y[b][row] = sum over the K ranges, in range order, of the prefill partials.
+__global__ void __launch_bounds__(256) k_prefill_reduce(KArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t npad = (int64_t)a.nt * 16;
+  if (t >= (int64_t)a.m * a.n) return;
+  const int b = (int)(t / a.n), row = (int)(t % a.n);
+  float s = 0.0f;
+  for (int z = 0; z < a.ks; ++z) s += a.ws_part[((int64_t)z * a.m + b) * npad + row];
+  store_y(a, b, row, s);
+}
+
+// ------------------------------------------------------------------------------------------
 // Host dispatch
 // ------------------------------------------------------------------------------------------
 namespace {
@@ -937,6 +1115,24 @@ const void* pick(int D, int V, int M) {
   return nullptr;
 }
 
+const void* prefill_fn(int D, int V) {
+  switch (sph_kind_of(D, V)) {
+    case SPH_KIND_W2:
+      return D == 7 ? (const void*)k_gemm_prefill<SPH_KIND_W2, 7> : (const void*)k_gemm_prefill<SPH_KIND_W2, 6>;
+    case SPH_KIND_NIB16:
+      if (D == 4) return (const void*)k_gemm_prefill<SPH_KIND_NIB16, 4>;
+      if (D == 5) return (const void*)k_gemm_prefill<SPH_KIND_NIB16, 5>;
+      return (const void*)k_gemm_prefill<SPH_KIND_NIB16, 6>;
+    case SPH_KIND_NIB16Q8: return (const void*)k_gemm_prefill<SPH_KIND_NIB16Q8, 8>;
+    case SPH_KIND_NIB16Q2: return (const void*)k_gemm_prefill<SPH_KIND_NIB16Q2, 8>;
+    case SPH_KIND_CB13: return (const void*)k_gemm_prefill<SPH_KIND_CB13, 13>;
+    case SPH_KIND_CB13Q4: return (const void*)k_gemm_prefill<SPH_KIND_CB13Q4, 13>;
+  }
+  return nullptr;
+}
+
+int prefill_mc(int D, int V) { return sph_is_codebook_kind(sph_kind_of(D, V)) ? 64 : 128; }
+
 const void* unpack_fn(int D, int V) {
   switch (sph_kind_of(D, V)) {
     case SPH_KIND_W2: return D == 7 ? (const void*)k_unpack<SPH_KIND_W2, 7> : (const void*)k_unpack<SPH_KIND_W2, 6>;
@@ -969,6 +1165,27 @@ int num_cus() {
 }
 
 
+
+// Prefill plan: workgroups of PF_WAVES * PF_TPW tiles by MC batch rows; K is split only while the
+// grid has fewer workgroups than CUs (each split adds a pass over fp32 partial outputs).
+struct PrefillPlan {
+  int gx, gy, ks;
+  size_t ws_bytes;
+};
+
+PrefillPlan prefill_plan(const sph_weights* w, int64_t m) {
+  PrefillPlan P{};
+  const int64_t nt = (w->n + 15) / 16, ng = w->k / 128;
+  const int mc = prefill_mc(w->fmt.dir_bits, w->fmt.radius_bits);
+  P.gx = (int)((nt + PF_WAVES * PF_TPW - 1) / (PF_WAVES * PF_TPW));
+  P.gy = (int)((m + mc - 1) / mc);
+  const int64_t g = (int64_t)P.gx * P.gy, cus = num_cus();
+  int64_t ks = 1;
+  while (g * ks < cus && ks * 2 <= ng && ks < 8) ks *= 2;
+  P.ks = (int)ks;
+  P.ws_bytes = ks > 1 ? (size_t)ks * m * nt * 16 * sizeof(float) : 0;
+  return P;
+}
 
 // Work plan. Vector-ALU path: one 16-wave workgroup per CU, every wave a contiguous range of
 // steps (at least one). Matrix-core path: a workgroup per tile, its waves splitting K.
@@ -1108,8 +1325,49 @@ sph_status sph_pack_weights(const sph_format* fmt, int64_t n, int64_t k, const u
 sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes) {
   if (!w || !bytes) return SPH_ERR_NULL;
   if (!valid_desc(w)) return SPH_ERR_BAD_DESCRIPTOR;
-  if (m < 1 || m > 32) return SPH_ERR_SHAPE;
-  *bytes = plan(w, (int)m).ws_bytes;
+  if (m < 1 || m > SPH_MAX_BATCH) return SPH_ERR_SHAPE;
+  *bytes = m <= 32 ? plan(w, (int)m).ws_bytes : prefill_plan(w, m).ws_bytes;
+  return SPH_OK;
+}
+
+sph_status sph_gemm(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y, int64_t ldy,
+                    sph_dtype y_dtype, void* d_ws, size_t ws_bytes, void* stream) {
+  if (!w) return SPH_ERR_NULL;
+  if (m >= 1 && m <= 32) return sph_gemm_small(w, d_x, m, ldx, d_y, ldy, y_dtype, d_ws, ws_bytes, stream);
+  if (!d_x || !d_y) return SPH_ERR_NULL;
+  if (!valid_desc(w)) return SPH_ERR_BAD_DESCRIPTOR;
+  if (m < 1 || m > SPH_MAX_BATCH) return SPH_ERR_SHAPE;
+  if (ldx < w->k || ldy < w->n || ldx % 8 != 0) return SPH_ERR_SHAPE;
+  if (y_dtype != SPH_F16 && y_dtype != SPH_F32) return SPH_ERR_SHAPE;
+  if ((uintptr_t)d_x % 16 != 0 || (uintptr_t)d_y % 4 != 0) return SPH_ERR_SHAPE;
+  const void* fn = prefill_fn(w->fmt.dir_bits, w->fmt.radius_bits);
+  if (!fn) return SPH_ERR_UNSUPPORTED_FORMAT;
+  const PrefillPlan P = prefill_plan(w, m);
+  if (P.ws_bytes > 0) {
+    if (!d_ws) return SPH_ERR_NULL;
+    if (ws_bytes < P.ws_bytes) return SPH_ERR_BUFFER_TOO_SMALL;
+    if ((uintptr_t)d_ws % 256 != 0) return SPH_ERR_SHAPE;
+  }
+  KArgs a = make_args(w);
+  a.x = (const uint16_t*)d_x;
+  a.ldx = ldx;
+  a.y = d_y;
+  a.ldy = ldy;
+  a.y_f16 = (y_dtype == SPH_F16);
+  a.m = (int)m;
+  a.ks = P.ks;
+  a.ws_part = (float*)d_ws;
+  void* kargs[] = {&a};
+  hipStream_t s = (hipStream_t)stream;
+  if (hipLaunchKernel(fn, dim3(P.gx, P.gy, P.ks), dim3(PF_THREADS), kargs, 0, s) != hipSuccess) return SPH_ERR_HIP;
+  if (hipGetLastError() != hipSuccess) return SPH_ERR_HIP;
+  if (P.ks > 1) {
+    const int64_t total = (int64_t)m * w->n;
+    if (hipLaunchKernel((const void*)k_prefill_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), kargs, 0, s) !=
+        hipSuccess)
+      return SPH_ERR_HIP;
+    if (hipGetLastError() != hipSuccess) return SPH_ERR_HIP;
+  }
   return SPH_OK;
 }
 

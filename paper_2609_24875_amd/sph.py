@@ -24,7 +24,7 @@ STATUS = {
 }
 
 # Every symbol include/sph.h declares.
-EXPORTS = ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
+EXPORTS = ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small", "sph_gemm",
            "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
            "sph_kmeans_codebook", "sph_angular_codebook", "sph_angular_codebook_backward",
            "sph_angular_logits", "sph_direction_groups", "sph_fake_quant_init_rho",
@@ -75,6 +75,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sph_pack_weights.argtypes = [pf, I64, I64, P, P, P, P, P, P, P, SZ, P, pw]
     lib.sph_gemv.argtypes = [pw, P, P, I32, P, SZ, P]
     lib.sph_gemm_small.argtypes = [pw, P, I64, I64, P, I64, I32, P, SZ, P]
+    lib.sph_gemm.argtypes = [pw, P, I64, I64, P, I64, I32, P, SZ, P]
     lib.sph_workspace_bytes.argtypes = [pw, I64, ctypes.POINTER(SZ)]
     lib.sph_unpack.argtypes = [pw, P, P, P, P]
     lib.sph_encode.argtypes = [pf, I64, I64, P, I64, P, P, P, P, P, P, P]
@@ -94,7 +95,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sph_format_supported.restype = I32
     lib.sph_status_str.argtypes = [I32]
     lib.sph_status_str.restype = ctypes.c_char_p
-    for name in ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
+    for name in ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small", "sph_gemm",
                  "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
                  "sph_kmeans_codebook", "sph_angular_codebook", "sph_angular_codebook_backward",
                  "sph_angular_logits", "sph_direction_groups", "sph_fake_quant_init_rho",
@@ -232,6 +233,22 @@ def gemm_small(w: SphWeights, x, out=None, out_dtype=None, stream=None):
                                        ws.data_ptr() if ws is not None else None, nb,
                                        _stream_handle(stream))
     _check(st, "sph_gemm_small")
+    return out
+
+
+def gemm(w: SphWeights, x, out=None, out_dtype=None, stream=None):
+    """Y = X W^T for device fp16 X[m][k], any 1 <= m <= 65536 (sph_gemm): the matrix-core prefill
+    kernel above m = 32."""
+    import torch
+    out_dtype = out_dtype or torch.float32
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, w.n), dtype=out_dtype, device=x.device)
+    ws, nb = _workspace(w, m, x.device)
+    st = load_library().sph_gemm(ctypes.byref(w.desc), x.data_ptr(), m, x.stride(0), out.data_ptr(),
+                                 out.stride(0), SPH_F16 if out.dtype == torch.float16 else SPH_F32,
+                                 ws.data_ptr() if ws is not None else None, nb, _stream_handle(stream))
+    _check(st, "sph_gemm")
     return out
 
 

@@ -186,3 +186,52 @@ def test_full_size_sampled(fmt, n, k, kind, m):
     ref = O.gemm_rows(codes, cb, x, rows)
     # Row RMS for the metric's floor is taken over the sampled outputs.
     assert O.rel_err(y[:, rows], ref) <= TOL
+
+
+# ------------------------------------------------------------------ prefill (batch > 32)
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("n,k,m", [(87, 640, 33), (300, 2048, 100), (16, 128, 64), (1, 256, 129)])
+def test_prefill_gemm_parity(fmt, n, k, m):
+    D, V, codes, cb = uniform_case(fmt, n, k, 5)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = synth.activations(m, k, synth.rng(5, n, k, m, synth.STREAM_X))
+    y = pkg.gemm(w, to_dev_f16(x)).cpu().numpy()
+    ref = O.gemm(codes, cb, x)
+    if n >= 16:    # with one output per row the row-RMS floor of rel_err is |y*| itself
+        assert O.rel_err(y, ref) <= TOL
+    assert np.all(np.abs(y - ref) <= f16_weight_bound(codes, cb, x, k))
+
+
+@pytest.mark.parametrize("fmt", ["W2", "W3"])
+def test_prefill_gemm_fp16_out_strided_repeatable(fmt):
+    n, k, m = 200, 1024, 80
+    D, V, codes, cb = uniform_case(fmt, n, k, 6)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = synth.activations(m, k, synth.rng(6, n, k, m, synth.STREAM_X))
+    xbuf = torch.zeros((m, k + 64), dtype=torch.float16, device=DEV)
+    xbuf[:, :k] = to_dev_f16(x)
+    ybuf = torch.full((m, n + 8), float("nan"), dtype=torch.float32, device=DEV)
+    y1 = pkg.gemm(w, xbuf[:, :k], out=ybuf[:, :n]).cpu().numpy()
+    y2 = pkg.gemm(w, xbuf[:, :k]).cpu().numpy()
+    assert np.array_equal(y1, y2)
+    assert torch.isnan(ybuf[:, n:]).all()
+    y16 = pkg.gemm(w, xbuf[:, :k], out_dtype=torch.float16).cpu().numpy()
+    assert np.array_equal(y16, y2.astype(np.float16))
+    assert O.rel_err(y2, O.gemm(codes, cb, x)) <= TOL
+
+
+@pytest.mark.parametrize("fmt", ["W2", "W3"])
+def test_prefill_gemm_full_size_sampled_rows(fmt):
+    """The paper's 256-token prefill on a full 12288 x 4096 projection, compared on sampled output
+    rows; and the 4096 x 12288 down projection, whose smaller grid splits K."""
+    for (n, k) in ((12288, 4096), (4096, 12288)):
+        D, V, codes, cb = uniform_case(fmt, n, k, 7)
+        w = pkg.pack(D, V, codes, cb, device=DEV)
+        m = 256
+        x = synth.activations(m, k, synth.rng(7, n, k, m, synth.STREAM_X))
+        y = pkg.gemm(w, to_dev_f16(x)).cpu().numpy()
+        rows = np.sort(np.random.default_rng(7).choice(n, 48, replace=False))
+        rows[0], rows[-1] = 0, n - 1
+        ref = O.gemm_rows(codes, cb, x, rows)
+        assert O.rel_err(y[:, rows], ref) <= TOL

@@ -898,20 +898,39 @@ __global__ void __launch_bounds__(256) k_unpack(KArgs a, uint8_t* signs, uint16_
 // the grid's third dimension splits K and the partial outputs are added in range order by
 // k_prefill_reduce. The order of every sum is fixed, so results are reproducible.
 // ------------------------------------------------------------------------------------------
-constexpr int PF_WAVES = 4;
+constexpr int PF_WAVES = 8;
 constexpr int PF_TPW = 2;
 constexpr int PF_THREADS = 64 * PF_WAVES;
 constexpr int PF_XROW = 128 * 2 + 16;   // bytes per staged X row (128 fp16 + padding)
 #define SPH_MAX_BATCH 65536
 
-template <int KIND>
-constexpr int pf_mc() { return IS_CB<KIND> ? 64 : 128; }
+// Per-chunk staging of the prefill kernel: the X slice and, for the workgroup's PF_WAVES * PF_TPW
+// tiles, their records of the chunk (streams A, B, C) and group parameters. Each lands in LDS with
+// one barrier; the next chunk's is meanwhile loaded into registers, so the multiply phase reads
+// LDS only.
+template <int KIND, int MC>
+struct PfStage {
+  static constexpr int TILES = PF_WAVES * PF_TPW;
+  static constexpr bool B1 = KIND == SPH_KIND_W2 || KIND == SPH_KIND_NIB16Q2;
+  static constexpr int ADW = IS_CB<KIND> ? 4 : 8;                                 // dwords per record
+  static constexpr int BDW = KIND == SPH_KIND_NIB16 ? 0 : B1 ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
+  static constexpr int CH = KIND == SPH_KIND_CB13Q4 ? 1 : 0;                      // halves per record
+  // 16-byte pieces per tile and chunk (16 records; 16 rows of parameters)
+  static constexpr int A16 = 16 * ADW / 4, B16 = 16 * BDW / 4, C16 = 16 * CH * 2 / 16, P16 = 4;
+  static constexpr int CODE16 = TILES * (A16 + B16 + C16 + P16);
+  static constexpr int X16 = MC * 16;
+  static constexpr int PER = (X16 + CODE16 + PF_THREADS - 1) / PF_THREADS;
+  // byte offsets inside one stage buffer
+  static constexpr uint32_t x_bytes = MC * PF_XROW;
+  static constexpr uint32_t a_off = x_bytes, b_off = a_off + TILES * A16 * 16, c_off = b_off + TILES * B16 * 16,
+                            p_off = c_off + TILES * C16 * 16, bytes = p_off + TILES * P16 * 16;
+};
 
-template <int KIND, int D>
+template <int KIND, int D, int MC>
 struct PfLds {
-  static constexpr uint32_t tables = Tables<KIND, D>::bytes;
-  static constexpr uint32_t x_off = (tables + 15u) / 16u * 16u;
-  static constexpr uint32_t bytes = x_off + pf_mc<KIND>() * PF_XROW;
+  static constexpr int nbuf = IS_CB<KIND> ? 1 : 2;
+  static constexpr uint32_t x_off = (Tables<KIND, D>::bytes + 15u) / 16u * 16u;
+  static constexpr uint32_t bytes = x_off + nbuf * PfStage<KIND, MC>::bytes;
 };
 
 template <int KIND, int D>
@@ -935,22 +954,70 @@ __device__ __forceinline__ uint4 pf_rebuild(const uint32_t ra, const uint32_t rb
   return scale_dir(tt, fmaf((float)q, st, lo));   // fp16(r * t), one rounding
 }
 
-template <int KIND, int D>
+// Load the PER 16-byte pieces of chunk c that this thread stages (X rows past the batch repeat
+// the last row; tiles past the matrix repeat the last tile: neither is ever stored).
+template <int KIND, int MC>
+struct PfPre {
+  uint4 v[PfStage<KIND, MC>::PER];
+};
+
+template <int KIND, int MC>
+__device__ __forceinline__ void pf_fetch(PfPre<KIND, MC>& pr, const KArgs& a, int t0, int mc0, int c) {
+  using S = PfStage<KIND, MC>;
+#pragma unroll
+  for (int p = 0; p < S::PER; ++p) {
+    int q = (int)threadIdx.x + PF_THREADS * p;
+    uint4 val = make_uint4(0, 0, 0, 0);
+    // divisors of empty streams are never used; max(1, .) keeps them defined
+    constexpr int a16 = S::A16 > 0 ? S::A16 : 1, b16 = S::B16 > 0 ? S::B16 : 1, c16 = S::C16 > 0 ? S::C16 : 1;
+    if (q < S::X16) {
+      const int b = min(mc0 + (q >> 4), a.m - 1);
+      val = *(const uint4*)(a.x + (int64_t)b * a.ldx + (int64_t)c * 128 + (q & 15) * 8);
+    } else if ((q -= S::X16) < S::TILES * S::A16) {
+      const int64_t t = min(t0 + q / a16, a.nt - 1);
+      val = ((const uint4*)(a.A + (t * a.nv + c * 16) * S::ADW))[q % a16];
+    } else if ((q -= S::TILES * S::A16) < S::TILES * S::B16) {
+      const int64_t t = min(t0 + q / b16, a.nt - 1);
+      val = ((const uint4*)(a.B + (t * a.nv + c * 16) * S::BDW))[q % b16];
+    } else if ((q -= S::TILES * S::B16) < S::TILES * S::C16) {
+      const int64_t t = min(t0 + q / c16, a.nt - 1);
+      val = ((const uint4*)(a.C + (t * a.nv + c * 16) * S::CH))[q % c16];
+    } else if ((q -= S::TILES * S::C16) < S::TILES * S::P16) {
+      const int64_t t = min(t0 + q / S::P16, a.nt - 1);
+      val = ((const uint4*)(a.P + (t * a.ng + c) * 16))[q % S::P16];
+    }
+    pr.v[p] = val;
+  }
+}
+
+template <int KIND, int MC>
+__device__ __forceinline__ void pf_put(unsigned char* st, const PfPre<KIND, MC>& pr) {
+  using S = PfStage<KIND, MC>;
+#pragma unroll
+  for (int p = 0; p < S::PER; ++p) {
+    const int q = (int)threadIdx.x + PF_THREADS * p;
+    if (q < S::X16)
+      *(uint4*)(st + (q >> 4) * PF_XROW + (q & 15) * 16) = pr.v[p];
+    else if (q < S::X16 + S::CODE16)
+      *(uint4*)(st + S::a_off + (q - S::X16) * 16) = pr.v[p];
+  }
+}
+
+template <int KIND, int D, int MC>
 __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
-  constexpr int MC = pf_mc<KIND>();
   constexpr int NB = MC / 16;
-  constexpr bool B1 = KIND == SPH_KIND_W2 || KIND == SPH_KIND_NIB16Q2;
-  constexpr int ADW_REC = IS_CB<KIND> ? 4 : 8;
-  constexpr int BDW_REC = B1 ? 1 : (KIND == SPH_KIND_NIB16Q8) ? 4 : 8;
-  __shared__ __align__(16) unsigned char lds[PfLds<KIND, D>::bytes];
-  unsigned char* xl = lds + PfLds<KIND, D>::x_off;
+  using S = PfStage<KIND, MC>;
+  using L = PfLds<KIND, D, MC>;
+  __shared__ __align__(16) unsigned char lds[L::bytes];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, j = lane >> 4;
   const int mc0 = blockIdx.y * MC;
+  const int t0 = (int)blockIdx.x * S::TILES;
   const int nc = a.ng;
   const int c0 = (int)((int64_t)nc * blockIdx.z / a.ks), c1 = (int)((int64_t)nc * (blockIdx.z + 1) / a.ks);
-  // lookup tables (and, for the codebook kinds, the sign masks) into LDS
+  PfPre<KIND, MC> pre;
+  pf_fetch<KIND, MC>(pre, a, t0, mc0, c0);
   {
     const int n16 = (int)((Tables<KIND, D>::bytes - (IS_CB<KIND> ? 128u : 0u)) / 16u);
     for (int t = threadIdx.x; t < n16; t += PF_THREADS) ((uint4*)lds)[t] = a.T[t];
@@ -964,80 +1031,63 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
       }
     }
   }
-  int tile[PF_TPW];
-  bool act[PF_TPW];
-#pragma unroll
-  for (int u = 0; u < PF_TPW; ++u) {
-    tile[u] = ((int)blockIdx.x * PF_WAVES + wave) * PF_TPW + u;
-    act[u] = tile[u] < a.nt;
-    if (!act[u]) tile[u] = a.nt - 1;   // inactive tiles read valid records and store nothing
-  }
-  float acc[PF_TPW][NB][4];
+  f32x4 acc[PF_TPW][NB];
 #pragma unroll
   for (int u = 0; u < PF_TPW; ++u)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[u][nb][e] = 0.0f;
+    for (int nb = 0; nb < NB; ++nb) acc[u][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  // the row's dword in streams A and B, as in the batch 9..32 tile mode
   const int adw = IS_CB<KIND> ? r / 4 : r / 2;
-  const int bdw = B1 ? 0 : (KIND == SPH_KIND_NIB16Q8) ? r / 4 : r / 2;
+  const int bdw = S::B1 ? 0 : (KIND == SPH_KIND_NIB16Q8) ? r / 4 : r / 2;
   for (int c = c0; c < c1; ++c) {
-    // this chunk's codes and group parameters for the lane's rows
-    uint32_t ra[PF_TPW][4], rb[PF_TPW][4], rc[PF_TPW][4], pw[PF_TPW];
-#pragma unroll
-    for (int u = 0; u < PF_TPW; ++u) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t rec = (int64_t)tile[u] * a.nv + c * 16 + 4 * i + j;
-        ra[u][i] = a.A[rec * ADW_REC + adw];
-        if constexpr (KIND != SPH_KIND_NIB16) rb[u][i] = a.B[rec * BDW_REC + bdw];
-        else rb[u][i] = 0;
-        if constexpr (KIND == SPH_KIND_CB13Q4) rc[u][i] = a.C[rec];
-        else rc[u][i] = 0;
-      }
-      pw[u] = a.P[((int64_t)tile[u] * a.ng + c) * 16 + r];
-    }
-    __syncthreads();   // the previous chunk's X is no longer read (and the tables are in place)
-    // stage X[mc0 .. mc0 + MC)[c*128 .. c*128 + 128) as fp16; rows past the batch repeat the last
-    // row (their outputs are never stored)
-    for (int t = threadIdx.x; t < MC * 16; t += PF_THREADS) {
-      const int row = t >> 4, piece = t & 15;
-      const int b = min(mc0 + row, a.m - 1);
-      const uint4 v = *(const uint4*)(a.x + (int64_t)b * a.ldx + (int64_t)c * 128 + piece * 8);
-      *(uint4*)(xl + row * PF_XROW + piece * 16) = v;
-    }
+    unsigned char* st = lds + L::x_off + (L::nbuf == 2 ? (c & 1) : 0) * S::bytes;
+    // with one buffer, wait until every wave has finished reading the previous chunk
+    if constexpr (L::nbuf == 1) __syncthreads();
+    pf_put<KIND, MC>(st, pre);
+    // chunk c (and, first time round, the tables) become visible; with two buffers this also
+    // orders the reads of buffer (c & 1) at chunk c - 2 before this chunk's writes to it
     __syncthreads();
+    pf_fetch<KIND, MC>(pre, a, t0, mc0, min(c + 1, c1 - 1));   // in flight during the multiply
+    const uint32_t* sa = (const uint32_t*)(st + S::a_off);
+    const uint32_t* sb = (const uint32_t*)(st + S::b_off);
+    const uint16_t* sc = (const uint16_t*)(st + S::c_off);
+    const uint32_t* sp = (const uint32_t*)(st + S::p_off);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       uint4 w[PF_TPW];
 #pragma unroll
-      for (int u = 0; u < PF_TPW; ++u)
-        w[u] = pf_rebuild<KIND, D>(ra[u][i], rb[u][i], rc[u][i], f16lo(pw[u]), f16hi(pw[u]), lds, a.t_bytes, r);
+      for (int u = 0; u < PF_TPW; ++u) {
+        const int lt = wave * PF_TPW + u, rec = lt * 16 + 4 * i + j;
+        const uint32_t ra = sa[rec * S::ADW + adw];
+        uint32_t rb = 0u;
+        if constexpr (S::BDW > 0) rb = sb[rec * S::BDW + bdw];
+        uint32_t rc = 0u;
+        if constexpr (S::CH > 0) rc = sc[rec];
+        const uint32_t pw = sp[lt * 16 + r];
+        w[u] = pf_rebuild<KIND, D>(ra, rb, rc, f16lo(pw), f16hi(pw), lds, a.t_bytes, r);
+      }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        const uint4 xb = *(const uint4*)(xl + (16 * nb + r) * PF_XROW + (4 * i + j) * 16);
+        const uint4 xb = *(const uint4*)(st + (16 * nb + r) * PF_XROW + (4 * i + j) * 16);
 #pragma unroll
-        for (int u = 0; u < PF_TPW; ++u) {
-          f32x4 d = {acc[u][nb][0], acc[u][nb][1], acc[u][nb][2], acc[u][nb][3]};
-          d = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, w[u]), __builtin_bit_cast(f16x8, xb),
-                                                     d, 0, 0, 0);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) acc[u][nb][e] = d[e];
-        }
+        for (int u = 0; u < PF_TPW; ++u)
+          acc[u][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, w[u]),
+                                                              __builtin_bit_cast(f16x8, xb), acc[u][nb], 0, 0, 0);
       }
     }
   }
   // D[row][col] of a 16x16 block: lane holds col lane % 16 (batch row) and rows 4 * (lane / 16) + e
 #pragma unroll
   for (int u = 0; u < PF_TPW; ++u) {
-    if (!act[u]) continue;
+    const int tile = t0 + wave * PF_TPW + u;
+    if (tile >= a.nt) continue;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int b = mc0 + 16 * nb + r;
       if (b >= a.m) continue;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int row = tile[u] * 16 + 4 * j + e;
+        const int row = tile * 16 + 4 * j + e;
         if (a.ks > 1) {
           a.ws_part[((int64_t)blockIdx.z * a.m + b) * ((int64_t)a.nt * 16) + row] = acc[u][nb][e];
         } else if (row < a.n) {
@@ -1115,23 +1165,35 @@ const void* pick(int D, int V, int M) {
   return nullptr;
 }
 
-const void* prefill_fn(int D, int V) {
+template <int KIND, int D>
+const void* prefill_fn_mc(int mc) {
+  if constexpr (IS_CB<KIND>) {
+    return (const void*)k_gemm_prefill<KIND, D, 64>;
+  } else {
+    if (mc == 64) return (const void*)k_gemm_prefill<KIND, D, 64>;
+    return (const void*)k_gemm_prefill<KIND, D, 128>;
+  }
+}
+
+// Batch rows per workgroup: 128 for the nibble kinds at batches above 64, else 64.
+int prefill_mc(int D, int V, int64_t m) {
+  return (sph_is_codebook_kind(sph_kind_of(D, V)) || m <= 64) ? 64 : 128;
+}
+
+const void* prefill_fn(int D, int V, int mc) {
   switch (sph_kind_of(D, V)) {
-    case SPH_KIND_W2:
-      return D == 7 ? (const void*)k_gemm_prefill<SPH_KIND_W2, 7> : (const void*)k_gemm_prefill<SPH_KIND_W2, 6>;
+    case SPH_KIND_W2: return D == 7 ? prefill_fn_mc<SPH_KIND_W2, 7>(mc) : prefill_fn_mc<SPH_KIND_W2, 6>(mc);
     case SPH_KIND_NIB16:
-      if (D == 4) return (const void*)k_gemm_prefill<SPH_KIND_NIB16, 4>;
-      if (D == 5) return (const void*)k_gemm_prefill<SPH_KIND_NIB16, 5>;
-      return (const void*)k_gemm_prefill<SPH_KIND_NIB16, 6>;
-    case SPH_KIND_NIB16Q8: return (const void*)k_gemm_prefill<SPH_KIND_NIB16Q8, 8>;
-    case SPH_KIND_NIB16Q2: return (const void*)k_gemm_prefill<SPH_KIND_NIB16Q2, 8>;
-    case SPH_KIND_CB13: return (const void*)k_gemm_prefill<SPH_KIND_CB13, 13>;
-    case SPH_KIND_CB13Q4: return (const void*)k_gemm_prefill<SPH_KIND_CB13Q4, 13>;
+      if (D == 4) return prefill_fn_mc<SPH_KIND_NIB16, 4>(mc);
+      if (D == 5) return prefill_fn_mc<SPH_KIND_NIB16, 5>(mc);
+      return prefill_fn_mc<SPH_KIND_NIB16, 6>(mc);
+    case SPH_KIND_NIB16Q8: return prefill_fn_mc<SPH_KIND_NIB16Q8, 8>(mc);
+    case SPH_KIND_NIB16Q2: return prefill_fn_mc<SPH_KIND_NIB16Q2, 8>(mc);
+    case SPH_KIND_CB13: return prefill_fn_mc<SPH_KIND_CB13, 13>(mc);
+    case SPH_KIND_CB13Q4: return prefill_fn_mc<SPH_KIND_CB13Q4, 13>(mc);
   }
   return nullptr;
 }
-
-int prefill_mc(int D, int V) { return sph_is_codebook_kind(sph_kind_of(D, V)) ? 64 : 128; }
 
 const void* unpack_fn(int D, int V) {
   switch (sph_kind_of(D, V)) {
@@ -1169,16 +1231,17 @@ int num_cus() {
 // Prefill plan: workgroups of PF_WAVES * PF_TPW tiles by MC batch rows; K is split only while the
 // grid has fewer workgroups than CUs (each split adds a pass over fp32 partial outputs).
 struct PrefillPlan {
-  int gx, gy, ks;
+  int gx, gy, ks, mc;
   size_t ws_bytes;
 };
 
 PrefillPlan prefill_plan(const sph_weights* w, int64_t m) {
   PrefillPlan P{};
   const int64_t nt = (w->n + 15) / 16, ng = w->k / 128;
-  const int mc = prefill_mc(w->fmt.dir_bits, w->fmt.radius_bits);
+  const int mc = prefill_mc(w->fmt.dir_bits, w->fmt.radius_bits, m);
   P.gx = (int)((nt + PF_WAVES * PF_TPW - 1) / (PF_WAVES * PF_TPW));
   P.gy = (int)((m + mc - 1) / mc);
+  P.mc = mc;
   const int64_t g = (int64_t)P.gx * P.gy, cus = num_cus();
   int64_t ks = 1;
   while (g * ks < cus && ks * 2 <= ng && ks < 8) ks *= 2;
@@ -1340,9 +1403,9 @@ sph_status sph_gemm(const sph_weights* w, const void* d_x, int64_t m, int64_t ld
   if (ldx < w->k || ldy < w->n || ldx % 8 != 0) return SPH_ERR_SHAPE;
   if (y_dtype != SPH_F16 && y_dtype != SPH_F32) return SPH_ERR_SHAPE;
   if ((uintptr_t)d_x % 16 != 0 || (uintptr_t)d_y % 4 != 0) return SPH_ERR_SHAPE;
-  const void* fn = prefill_fn(w->fmt.dir_bits, w->fmt.radius_bits);
-  if (!fn) return SPH_ERR_UNSUPPORTED_FORMAT;
   const PrefillPlan P = prefill_plan(w, m);
+  const void* fn = prefill_fn(w->fmt.dir_bits, w->fmt.radius_bits, P.mc);
+  if (!fn) return SPH_ERR_UNSUPPORTED_FORMAT;
   if (P.ws_bytes > 0) {
     if (!d_ws) return SPH_ERR_NULL;
     if (ws_bytes < P.ws_bytes) return SPH_ERR_BUFFER_TOO_SMALL;

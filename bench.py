@@ -32,6 +32,7 @@ if ROOT not in sys.path:
 import synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFS = 2500.0   # MI355X dense fp16 matrix peak
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.hip")
 
 # HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE + WRITE_SIZE runs, each
@@ -373,8 +374,10 @@ def main():
             for label, n, k, copies, xd, ys in packed:
                 if m == 1:
                     pkg.gemv(copies[li], xd[0], out=ys[li][0])
-                else:
+                elif m <= 32:
                     pkg.gemm_small(copies[li], xd, out=ys[li])
+                else:
+                    pkg.gemm(copies[li], xd, out=ys[li])
 
     run_step()                                  # first calls outside capture
     torch.cuda.synchronize()
@@ -411,8 +414,10 @@ def main():
         for w, xd, y in dom_launches:
             if m == 1:
                 pkg.gemv(w, xd[0], out=y[0])
-            else:
+            elif m <= 32:
                 pkg.gemm_small(w, xd, out=y)
+            else:
+                pkg.gemm(w, xd, out=y)
     torch.cuda.synchronize()
     reps = max(3, args.steps // 2)
     d0 = torch.cuda.Event(enable_timing=True)
@@ -429,6 +434,7 @@ def main():
     dom_us = d0.elapsed_time(d1) * 1e3 / (reps * len(dom_launches))
     dom_bytes = sum(w.nbytes for w, _, _ in dom_launches) / len(dom_launches)
     dom_gbs = dom_bytes / (dom_us * 1e-6) / 1e9
+    dom_flops = 2.0 * m * big[0][1] * big[0][2]
 
     out = {
         "metric": "packed-weight GB/s & % HBM peak for W2/W3 sph_gemv; linear-layer tokens/s",
@@ -457,7 +463,7 @@ def main():
         },
         "tokens_per_s": round(m / (ms / 1e3), 2),
         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
-        "roofline": {
+        "roofline": ({
             "kernel": f"{kernel_label(fmt, m)} on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
             "bound": "hbm",
             "achieved": round(dom_gbs, 2),
@@ -467,7 +473,18 @@ def main():
             "traffic": TRAFFIC.get(kernel_source_hash(), {}).get(f"{big[0][1]}x{big[0][2]}-m{m}"),
             "avg_launch_us": round(dom_us, 3),
             "bytes_per_launch": int(dom_bytes),
-        },
+        } if m <= 32 else {
+            # batches above 32: a dense contraction on the matrix cores, 2 m n k flop per launch
+            "kernel": f"{kernel_label(fmt, m)} on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
+            "bound": "mfma",
+            "achieved": round(dom_flops / (dom_us * 1e-6) / 1e12, 2),
+            "peak": MFMA_F16_PEAK_TFS,
+            "unit": "TFLOP/s",
+            "frac": round(dom_flops / (dom_us * 1e-6) / 1e12 / MFMA_F16_PEAK_TFS, 4),
+            "traffic": None,
+            "avg_launch_us": round(dom_us, 3),
+            "flops_per_launch": int(dom_flops),
+        }),
         "setup_s": round(setup_s, 1),
     }
     if not args.no_cpu_baseline:
@@ -483,7 +500,9 @@ def kernel_label(fmt, m):
         return f"k_gemm_valu<{fmt},M=1> (vector ALU)"
     if m <= 8:
         return f"k_gemm_valu<{fmt},M={4 if m <= 4 else 8}> (4x4x4 MFMA blocks)"
-    return f"k_gemm_valu<{fmt},M={16 if m <= 16 else 32}> (16x16x32 MFMA tiles)"
+    if m <= 32:
+        return f"k_gemm_valu<{fmt},M={16 if m <= 16 else 32}> (16x16x32 MFMA tiles)"
+    return f"k_gemm_prefill<{fmt}> (16x16x32 MFMA, LDS-staged activations)"
 
 
 def clone_weights(pkg, w):

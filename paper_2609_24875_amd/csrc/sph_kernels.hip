@@ -1229,7 +1229,7 @@ int num_cus() {
 
 
 // Prefill plan: workgroups of PF_WAVES * PF_TPW tiles by MC batch rows; K is split only while the
-// grid has fewer workgroups than CUs (each split adds a pass over fp32 partial outputs).
+// split grid still fits in one round on the CUs (each split adds a pass over fp32 partial outputs).
 struct PrefillPlan {
   int gx, gy, ks, mc;
   size_t ws_bytes;
@@ -1243,8 +1243,9 @@ PrefillPlan prefill_plan(const sph_weights* w, int64_t m) {
   P.gy = (int)((m + mc - 1) / mc);
   P.mc = mc;
   const int64_t g = (int64_t)P.gx * P.gy, cus = num_cus();
+  // a split pays only while the doubled grid still fits in one round on the CUs
   int64_t ks = 1;
-  while (g * ks < cus && ks * 2 <= ng && ks < 8) ks *= 2;
+  while (g * ks * 2 <= cus && ks * 2 <= ng && ks < 8) ks *= 2;
   P.ks = (int)ks;
   P.ws_bytes = ks > 1 ? (size_t)ks * m * nt * 16 * sizeof(float) : 0;
   return P;

@@ -18,7 +18,9 @@ from __future__ import annotations
 
 import numpy as np
 
-VEC = 8                # Sec. 3.1: rows are cut along d_in into contiguous 8-D vectors
+VEC = 8                # Sec. 3.1: rows are cut along d_in into contiguous 8-D vectors (the
+                       # encoder, decoder and GEMM also take 4-D and 16-D codebooks, Tab. 7:
+                       # the vector size is the codebook's second dimension)
 GROUP = 128            # Sec. 3.1: a radius group is 128 consecutive scalars of one row
 VPG = GROUP // VEC     # = 16 vectors per group
 EPS = 1e-12            # Eq. 3's epsilon (its value is not printed; reading: 1e-12 in fp64)
@@ -107,8 +109,8 @@ def decompose(w):
 
 def assign_directions(d, codebook, chunk: int = 4096) -> np.ndarray:
     """Eq. 5: z_i = argmax_k <d_i, c_k>; ties go to the lowest index (reading)."""
-    d = np.asarray(d, dtype=np.float64).reshape(-1, VEC)
     c = np.asarray(codebook, dtype=np.float64)
+    d = np.asarray(d, dtype=np.float64).reshape(-1, c.shape[-1])
     z = np.empty(d.shape[0], dtype=np.int64)
     for a in range(0, d.shape[0], chunk):
         z[a:a + chunk] = np.argmax(d[a:a + chunk] @ c.T, axis=1)
@@ -145,10 +147,13 @@ def quantize_radius(r_tilde, gmin_bits, gstep_bits, radius_bits: int) -> np.ndar
 
 
 def signs_to_bits(neg) -> np.ndarray:
-    """Pack the 8 negative-flags of a vector into one byte, bit j <-> coordinate j."""
+    """Pack the negative-flags of a vector (last axis) into an integer, bit j <-> coordinate j:
+    a byte for 4-D and 8-D vectors, 16 bits for 16-D vectors."""
     neg = np.asarray(neg, dtype=bool)
-    weights = (1 << np.arange(VEC)).astype(np.uint16)
-    return (neg.astype(np.uint16) * weights).sum(axis=-1).astype(np.uint8)
+    dim = neg.shape[-1]
+    weights = (1 << np.arange(dim)).astype(np.uint32)
+    bits = (neg.astype(np.uint32) * weights).sum(axis=-1)
+    return bits.astype(np.uint8 if dim <= 8 else np.uint16)
 
 
 def encode(w, codebook_bits, radius_bits: int, params=None) -> dict:
@@ -163,17 +168,18 @@ def encode(w, codebook_bits, radius_bits: int, params=None) -> dict:
     if k % GROUP:
         raise ValueError("k must be a multiple of 128")
     c = f16_to_f64(codebook_bits)
-    vecs = w.reshape(n, k // VEC, VEC)
+    dim = c.shape[-1]
+    vecs = w.reshape(n, k // dim, dim)
     neg, w_plus, _r, d = decompose(vecs)
-    z = assign_directions(d, c).reshape(n, k // VEC)
+    z = assign_directions(d, c).reshape(n, k // dim)
     r_tilde = ls_radius(w_plus, c[z])
-    rg = r_tilde.reshape(n, k // GROUP, VPG)
+    rg = r_tilde.reshape(n, k // GROUP, GROUP // dim)
     if params is None:
         gmin, gstep = group_offset_step(rg, radius_bits)
     else:
         gmin = np.broadcast_to(np.asarray(params[0], np.uint16), (n, k // GROUP)).copy()
         gstep = np.broadcast_to(np.asarray(params[1], np.uint16), (n, k // GROUP)).copy()
-    q = quantize_radius(rg, gmin, gstep, radius_bits).reshape(n, k // VEC)
+    q = quantize_radius(rg, gmin, gstep, radius_bits).reshape(n, k // dim)
     return {"signs": signs_to_bits(neg), "dir": z.astype(np.uint16), "q": q,
             "gmin": gmin, "gstep": gstep}
 
@@ -228,30 +234,33 @@ def kmeans_codebook(w, init_bits, u, iters: int = 20):
 
 # ---------------------------------------------------------------- decoder (Eq. 4 and 7)
 
-def sign_factors(signs) -> np.ndarray:
-    """Byte of sign bits -> the +-1 factors s of Eq. 3/4, shape [..., 8]."""
-    b = np.asarray(signs, dtype=np.uint8)[..., None]
-    bit = (b >> np.arange(VEC, dtype=np.uint8)) & 1
+def sign_factors(signs, dim: int = VEC) -> np.ndarray:
+    """Sign bits of a vector -> the +-1 factors s of Eq. 3/4, shape [..., dim]."""
+    b = np.asarray(signs).astype(np.uint32)[..., None]
+    bit = (b >> np.arange(dim, dtype=np.uint32)) & 1
     return 1.0 - 2.0 * bit.astype(np.float64)
 
 
 def dequantize_radius(q, gmin_bits, gstep_bits) -> np.ndarray:
-    """Eq. 7: r^ = min_G + q * Delta_G, per vector; params are per group of 16 vectors."""
+    """Eq. 7: r^ = min_G + q * Delta_G, per vector; params are per group of 128 weights (16
+    vectors of 8-D, 32 of 4-D, 8 of 16-D)."""
     q = np.asarray(q, dtype=np.float64)
     n, nv = q.shape
-    lo = np.repeat(f16_to_f64(gmin_bits), VPG, axis=1)[:, :nv]
-    step = np.repeat(f16_to_f64(gstep_bits), VPG, axis=1)[:, :nv]
+    vpg = nv // np.asarray(gmin_bits).shape[1]
+    lo = np.repeat(f16_to_f64(gmin_bits), vpg, axis=1)[:, :nv]
+    step = np.repeat(f16_to_f64(gstep_bits), vpg, axis=1)[:, :nv]
     return lo + q * step
 
 
 def decode(codes: dict, codebook_bits) -> np.ndarray:
     """Eq. 4: w^ = r^ * s (.) c_z, assembled into the dense fp64 matrix W^[n][k]."""
     c = f16_to_f64(codebook_bits)
+    dim = c.shape[-1]
     r_hat = dequantize_radius(codes["q"], codes["gmin"], codes["gstep"])
-    s = sign_factors(codes["signs"])
+    s = sign_factors(codes["signs"], dim)
     vec = r_hat[..., None] * s * c[np.asarray(codes["dir"], dtype=np.int64)]
     n, nv = r_hat.shape
-    return vec.reshape(n, nv * VEC)
+    return vec.reshape(n, nv * dim)
 
 
 def _rows(codes: dict, a: int, b: int) -> dict:

@@ -299,6 +299,64 @@ def pin_encode_group_params_recovered(o):
         assert np.array_equal(back[key], codes[key]), key
 
 
+def pin_vector_dims(o):
+    """Tab. 7's 4-D and 16-D vectors through the same encoder and decoder: every (4 sign bits,
+    direction, level) code of a 4-entry 4-D codebook with 3 radius bits comes back from
+    decode then encode; 16-D codes (16 sign bits, 14-bit direction, 6 radius bits) come back
+    likewise; decoded vectors have norm r^ ||c_z|| and the code's signs; and with exactly-unit
+    4-D axes and both extreme levels in every 32-vector group, Eq. 7's parameters are recovered."""
+    g = np.random.default_rng(30)
+    cb4 = synth.random_codebook(2, g, dim=4)
+    combos = np.array(list(itertools.product(range(16), range(4), range(8))), dtype=np.int64)
+    n4 = combos.shape[0] // 32
+    codes = {"signs": combos[:, 0].astype(np.uint8).reshape(n4, 32),
+             "dir": combos[:, 1].astype(np.uint16).reshape(n4, 32),
+             "q": combos[:, 2].astype(np.uint8).reshape(n4, 32),
+             "gmin": np.full((n4, 1), synth.f16_bits(0.5), np.uint16),
+             "gstep": np.full((n4, 1), synth.f16_bits(0.1), np.uint16)}
+    w = o.decode(codes, cb4)
+    assert w.shape == (n4, 128)
+    back = o.encode(w, cb4, 3, params=(codes["gmin"], codes["gstep"]))
+    for key in ("signs", "dir", "q"):
+        assert np.array_equal(back[key], codes[key]), ("4d", key)
+    cb16 = synth.random_codebook(14, g, dim=16)
+    n16 = 6
+    c16 = {"signs": g.integers(0, 1 << 16, (n16, 16)).astype(np.uint16),
+           "dir": g.integers(0, 1 << 14, (n16, 16)).astype(np.uint16),
+           "q": g.integers(0, 64, (n16, 16)).astype(np.uint8),
+           "gmin": np.full((n16, 2), synth.f16_bits(0.25), np.uint16),
+           "gstep": np.full((n16, 2), synth.f16_bits(0.03125), np.uint16)}
+    w16 = o.decode(c16, cb16)
+    assert w16.shape == (n16, 256)
+    back = o.encode(w16, cb16, 6, params=(c16["gmin"], c16["gstep"]))
+    for key in ("signs", "dir", "q"):
+        assert np.array_equal(back[key], c16[key]), ("16d", key)
+    rh = 0.25 + c16["q"] * 0.03125
+    cz = O.f16_to_f64(cb16)[c16["dir"].astype(np.int64)]
+    v = w16.reshape(n16, 16, 16)
+    assert np.allclose(np.linalg.norm(v, axis=2), rh * np.linalg.norm(cz, axis=2), rtol=1e-14)
+    sbits = (c16["signs"][..., None].astype(np.int64) >> np.arange(16)) & 1
+    assert np.array_equal(np.signbit(v), sbits.astype(bool))
+    axes = synth.f16_bits(np.eye(4))
+    n, k = 5, 256
+    cg = synth.uniform_codes(n, k, 2, 3, g)
+    cg["signs"] = g.integers(0, 16, (n, k // 4)).astype(np.uint8)
+    cg["dir"] = g.integers(0, 4, (n, k // 4)).astype(np.uint16)
+    q = g.integers(0, 8, (n, k // 4)).reshape(n, 2, 32)
+    q[..., 3], q[..., 17] = 0, 7
+    cg["q"] = q.reshape(n, k // 4).astype(np.uint8)
+    lo = np.array([0.5, 0.25, 1.0, 2.0, 0.125])
+    cg["gmin"] = synth.f16_bits(np.repeat(lo[:, None], 2, axis=1))
+    cg["gstep"] = synth.f16_bits(np.repeat((lo / 4)[:, None], 2, axis=1))
+    back = o.encode(o.decode(cg, axes), axes, 3)
+    zero = np.eye(4)[cg["dir"].astype(int)] == 0
+    bits = (cg["signs"][..., None] >> np.arange(4)) & 1
+    canon = ((bits * ~zero) << np.arange(4)).sum(axis=-1).astype(np.uint8)
+    assert np.array_equal(back["signs"], canon)
+    for key in ("dir", "q", "gmin", "gstep"):
+        assert np.array_equal(back[key], cg[key]), ("4d groups", key)
+
+
 def pin_w2_layout(o):
     """Sec. 3.4 / App. D / Fig. 3b field positions, on hand-worked words; plus a bit-exact
     pack/unpack round trip on random codes."""
@@ -531,7 +589,7 @@ def pin_rel_err(o):
 PINS = [pin_worked_radius, pin_spherical_roundtrip, pin_bit_budget, pin_decompose,
         pin_assign, pin_ls_radius, pin_radius_quant, pin_decode_norm_and_sign,
         pin_decode_one_hot, pin_gemm_exact_rational, pin_gemm_special_cases,
-        pin_encode_roundtrip_bruteforce, pin_encode_group_params_recovered, pin_w2_layout,
+        pin_encode_roundtrip_bruteforce, pin_encode_group_params_recovered, pin_vector_dims, pin_w2_layout,
         pin_angular_codebook, pin_angular_backward, pin_fake_quant_radius, pin_fake_quant_backward,
         pin_init_rho, pin_sample_by_squared_radius, pin_spherical_kmeans, pin_kmeans_codebook,
         pin_rel_err]
@@ -544,9 +602,9 @@ def test_pin(pin):
 
 # ----------------------------------------------------------------- planted mistakes
 
-def _mut_sign_order(signs):
-    b = np.asarray(signs, dtype=np.uint8)[..., None]
-    bit = (b >> np.arange(7, -1, -1, dtype=np.uint8)) & 1      # reversed bit order
+def _mut_sign_order(signs, dim=8):
+    b = np.asarray(signs).astype(np.uint32)[..., None]
+    bit = (b >> np.arange(dim - 1, -1, -1, dtype=np.uint32)) & 1      # reversed bit order
     return 1.0 - 2.0 * bit.astype(np.float64)
 
 
@@ -714,26 +772,28 @@ def _rebind(ns):
     gemm use module globals): run pins against thin wrappers built on the namespace."""
     def decode(codes, cb):
         c = O.f16_to_f64(cb)
+        dim = c.shape[-1]
         r_hat = ns.dequantize_radius(codes["q"], codes["gmin"], codes["gstep"])
-        s = ns.sign_factors(codes["signs"])
+        s = ns.sign_factors(codes["signs"], dim)
         vec = r_hat[..., None] * s * c[np.asarray(codes["dir"], dtype=np.int64)]
         n, nv = r_hat.shape
-        return vec.reshape(n, nv * 8)
+        return vec.reshape(n, nv * dim)
 
     def encode(w, cb, v_bits, params=None):
         w = np.asarray(w, dtype=np.float64)
         n, k = w.shape
         c = O.f16_to_f64(cb)
-        vecs = w.reshape(n, k // 8, 8)
+        dim = c.shape[-1]
+        vecs = w.reshape(n, k // dim, dim)
         neg, wp, _r, d = ns.decompose(vecs)
-        z = ns.assign_directions(d, c).reshape(n, k // 8)
-        rt = ns.ls_radius(wp, c[z]).reshape(n, k // 128, 16)
+        z = ns.assign_directions(d, c).reshape(n, k // dim)
+        rt = ns.ls_radius(wp, c[z]).reshape(n, k // 128, 128 // dim)
         if params is None:
             gmin, gstep = ns.group_offset_step(rt, v_bits)
         else:
             gmin = np.broadcast_to(np.asarray(params[0], np.uint16), (n, k // 128)).copy()
             gstep = np.broadcast_to(np.asarray(params[1], np.uint16), (n, k // 128)).copy()
-        q = ns.quantize_radius(rt, gmin, gstep, v_bits).reshape(n, k // 8)
+        q = ns.quantize_radius(rt, gmin, gstep, v_bits).reshape(n, k // dim)
         return {"signs": O.signs_to_bits(neg), "dir": z.astype(np.uint16), "q": q,
                 "gmin": gmin, "gstep": gstep}
 

@@ -98,12 +98,13 @@ def layer_shapes(wl, fused: bool):
 def make_layer0(wl, fmt, m, shapes):
     """Codes, codebooks and activations of layer 0's matrices (seeded, uniform codes)."""
     D, V = synth.FORMATS[fmt]
+    dim = synth.fmt_dim(fmt)
     mats = []
     for mi, (label, n, k) in enumerate(shapes):
         g = synth.rng(wl_id(wl), 0, mi, synth.STREAM_CODES)
-        codes = synth.uniform_codes(n, k, D, V, g)
+        codes = synth.uniform_codes(n, k, D, V, g, dim=dim)
         codes["gmin"], codes["gstep"] = synth.row_scale_group_params(n, k, V, g)
-        cb = synth.random_codebook(D, synth.rng(wl_id(wl), 0, mi, synth.STREAM_CODEBOOK))
+        cb = synth.random_codebook(D, synth.rng(wl_id(wl), 0, mi, synth.STREAM_CODEBOOK), dim=dim)
         x = synth.activations(m, k, synth.rng(wl_id(wl), 0, mi, synth.STREAM_X))
         mats.append((label, n, k, codes, cb, x))
     return mats
@@ -359,7 +360,7 @@ def main():
     mats = make_layer0(wl, fmt, m, shapes)
     packed = []
     for label, n, k, codes, cb, x in mats:
-        w0 = pkg.pack(D, V, codes, cb, device=dev)
+        w0 = pkg.pack(D, V, codes, cb, device=dev, vec_dim=synth.fmt_dim(fmt))
         copies = [w0] + [clone_weights(pkg, w0) for _ in range(layers - 1)]
         xd = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.float16)
         ys = [torch.empty((m, n), dtype=torch.float32, device=dev) for _ in range(layers)]
@@ -452,7 +453,8 @@ def main():
                 "unit codebook, fp16 N(0,1) activations",
         "config": {
             "workload": f"{wl.name}-{fmt}-m{m}" if args.fmt else f"{wl.name}-m{m}",
-            "format": f"{fmt} (8 sign + {D} direction + {V} radius bits per 8-vector)",
+            "format": f"{fmt} ({synth.fmt_dim(fmt)} sign + {D} direction + {V} radius bits per "
+                      f"{synth.fmt_dim(fmt)}-vector)",
             "layers": layers,
             "shapes": [f"{label} {n}x{k}" for label, n, k, *_ in packed],
             "batch": m,
@@ -510,7 +512,7 @@ def clone_weights(pkg, w):
     buf = w.buffer.clone()
     d = type(w.desc).from_buffer_copy(w.desc)
     d.d_base = buf.data_ptr()
-    return pkg.SphWeights(d, buf, w.n, w.k, w.dir_bits, w.radius_bits)
+    return pkg.SphWeights(d, buf, w.n, w.k, w.dir_bits, w.radius_bits, vec_dim=w.vec_dim)
 
 
 if __name__ == "__main__":

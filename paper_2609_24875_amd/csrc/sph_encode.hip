@@ -526,8 +526,15 @@ KmPlan km_plan(const sph_format* fmt, int64_t n, int64_t k, int64_t ns) {
 constexpr int64_t kMaxSamples = int64_t(1) << 24;
 constexpr int32_t kMaxIters = 10000;
 
+// The encoder and k-means handle 8-D vectors (the 4-D and 16-D formats are decode-only).
+int check_fmt8(const sph_format* fmt) {
+  const int st = sph_host_check_format(fmt);
+  if (st) return st;
+  return fmt->vec_dim == SPH_VEC ? SPH_OK : SPH_ERR_UNSUPPORTED_FORMAT;
+}
+
 int check_common(const sph_format* fmt, int64_t n, int64_t k, const float* d_w, int64_t ldw) {
-  int st = sph_host_check_format(fmt);
+  int st = check_fmt8(fmt);
   if (st) return st;
   st = sph_host_check_shape(n, k);
   if (st) return st;
@@ -580,7 +587,7 @@ sph_status sph_encode(const sph_format* fmt, int64_t n, int64_t k, const float* 
 sph_status sph_kmeans_workspace_bytes(const sph_format* fmt, int64_t n, int64_t k, int64_t n_samples,
                                       size_t* bytes) {
   if (!fmt || !bytes) return SPH_ERR_NULL;
-  int st = sph_host_check_format(fmt);
+  int st = check_fmt8(fmt);
   if (st) return (sph_status)st;
   st = sph_host_check_shape(n, k);
   if (st) return (sph_status)st;

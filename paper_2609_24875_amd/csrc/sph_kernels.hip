@@ -37,6 +37,7 @@ struct KArgs {
   const uint32_t* P;
   const uint16_t* C;  // codebook kind with 4 radius bits: bit 3 of q, one 16-bit word per record
   const uint4* T;
+  const uint16_t* CB;  // the codebook as packed (read from memory by the 16-D kernel)
   uint32_t t_bytes;   // bytes of lookup tables staged into LDS
   const uint16_t* x;
   int64_t ldx;
@@ -1110,6 +1111,146 @@ __global__ void __launch_bounds__(256) k_prefill_reduce(KArgs a) {
 }
 
 // ------------------------------------------------------------------------------------------
+// Row-planar kernels for 4-D and 16-D vectors (Tab. 7), batch 1..32.
+//
+// One wave per output row. Per step a lane covers 64 consecutive weights of the row (16 4-D or
+// 4 16-D vectors, inside one 128-weight group), so a step covers 4096 weights; the row sum is a
+// wave reduction. The 4-D signed directions come from a 64-entry sign-folded table in LDS; a 16-D
+// codebook entry is read from memory (the 512 KiB codebook stays in L2) and its signs applied by
+// XOR on the fp16 sign bits. Batch 1 forms exact fp16 products with fp32 sums and applies the
+// radius in fp32, as the 8-D vector-ALU mode does; larger batches rebuild the lane's 64 weights
+// once as fp16(r * t) and reuse them for every activation row.
+// ------------------------------------------------------------------------------------------
+constexpr int RV_WAVES = 4;
+
+template <int KIND>
+__device__ __forceinline__ void rv_vector(const KArgs& a, const uint2* tab, const uint4 f, int u, uint32_t bw, int vin,
+                                          float lo, float st, float& r, uint32_t (&t)[8]) {
+  if constexpr (KIND == SPH_KIND_V4) {
+    const uint32_t word = u < 4 ? f.x : u < 8 ? f.y : u < 12 ? f.z : f.w;
+    const uint32_t byte = (word >> (8 * (u & 3))) & 0xFFu;
+    const uint32_t q = (byte >> 6) | (((bw >> (vin + u)) & 1u) << 2);
+    r = fmaf((float)q, st, lo);
+    const uint2 e = tab[byte & 63u];
+    t[0] = e.x;
+    t[1] = e.y;
+  } else {
+    const uint32_t fw = u == 0 ? f.x : u == 1 ? f.y : u == 2 ? f.z : f.w;
+    const uint32_t s = fw & 0xFFFFu, z = (fw >> 16) & 0x3FFFu;
+    const uint32_t q = (fw >> 30) | (((bw >> (4 * (vin + u))) & 15u) << 2);
+    r = fmaf((float)q, st, lo);
+    const uint4* cz = (const uint4*)(a.CB + (int64_t)z * 16);
+    const uint4 c0 = cz[0], c1 = cz[1];
+    const uint32_t c[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) t[i] = c[i] ^ ((((s >> (2 * i)) & 1u) << 15) | (((s >> (2 * i + 1)) & 1u) << 31));
+  }
+}
+
+template <int KIND, int MB>
+__global__ void __launch_bounds__(64 * RV_WAVES) k_gemm_rowvec(KArgs a) {
+  constexpr int VEC = KIND == SPH_KIND_V4 ? 4 : 16;
+  constexpr int NVL = 64 / VEC;              // vectors per lane and step
+  constexpr int TW = VEC / 2;                // fp16 pairs per vector
+  __shared__ uint2 tab[KIND == SPH_KIND_V4 ? 64 : 1];
+  if constexpr (KIND == SPH_KIND_V4) {
+    if (threadIdx.x < 64) tab[threadIdx.x] = ((const uint2*)a.T)[threadIdx.x];
+    __syncthreads();
+  }
+  const int lane = threadIdx.x & 63;
+  const int row = (int)blockIdx.x * RV_WAVES + (int)(threadIdx.x >> 6);
+  if (row >= a.n) return;   // after the only barrier
+  const int64_t k = (int64_t)a.ng * 128;
+  float acc[MB];
+#pragma unroll
+  for (int b = 0; b < MB; ++b) acc[b] = 0.0f;
+  for (int64_t k0 = 0; k0 < k; k0 += 4096) {
+    const int64_t kw = k0 + (int64_t)lane * 64;
+    if (kw >= k) continue;
+    const int g = (int)(kw >> 7);
+    const uint32_t pw = a.P[(int64_t)row * a.ng + g];
+    const uint32_t bw = a.B[(int64_t)row * a.ng + g];
+    const float lo = f16lo(pw), st = f16hi(pw);
+    const int vin = (int)((kw & 127) / VEC);
+    uint4 f;
+    if constexpr (KIND == SPH_KIND_V4)
+      f = *(const uint4*)((const uint8_t*)a.A + (int64_t)row * a.nv + kw / 4);
+    else
+      f = *(const uint4*)(a.A + (int64_t)row * a.nv + kw / 16);
+    if constexpr (MB == 1) {
+      const uint32_t* xp = (const uint32_t*)(a.x + kw);
+#pragma unroll
+      for (int u = 0; u < NVL; ++u) {
+        float r;
+        uint32_t t[8];
+        rv_vector<KIND>(a, tab, f, u, bw, vin, lo, st, r, t);
+        float d = 0.0f;
+#pragma unroll
+        for (int i = 0; i < TW; ++i) d = __builtin_amdgcn_fdot2(as_h2(t[i]), as_h2(xp[u * TW + i]), d, false);
+        acc[0] = fmaf(r, d, acc[0]);
+      }
+    } else {
+      uint32_t w[32];   // the lane's 64 weights as fp16(r * t)
+#pragma unroll
+      for (int u = 0; u < NVL; ++u) {
+        float r;
+        uint32_t t[8];
+        rv_vector<KIND>(a, tab, f, u, bw, vin, lo, st, r, t);
+#pragma unroll
+        for (int i = 0; i < TW; ++i) w[u * TW + i] = scale_h2(t[i], r);
+      }
+#pragma unroll
+      for (int b = 0; b < MB; ++b) {
+        if (b < a.m) {
+          const uint4* xp = (const uint4*)(a.x + (int64_t)b * a.ldx + kw);
+          float d = 0.0f;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const uint4 xv = xp[i];
+            d = __builtin_amdgcn_fdot2(as_h2(w[4 * i]), as_h2(xv.x), d, false);
+            d = __builtin_amdgcn_fdot2(as_h2(w[4 * i + 1]), as_h2(xv.y), d, false);
+            d = __builtin_amdgcn_fdot2(as_h2(w[4 * i + 2]), as_h2(xv.z), d, false);
+            d = __builtin_amdgcn_fdot2(as_h2(w[4 * i + 3]), as_h2(xv.w), d, false);
+          }
+          acc[b] += d;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < MB; ++b) {
+    float v = acc[b];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    if (lane == 0 && b < a.m) store_y(a, b, row, v);
+  }
+}
+
+// Logical codes of the row-planar kinds: signs (a byte for 4-D, a uint16 for 16-D), direction
+// index and level, one thread per vector.
+template <int KIND>
+__global__ void __launch_bounds__(256) k_unpack_rowvec(KArgs a, uint8_t* signs, uint16_t* dir, uint8_t* qo) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t nvec = (int64_t)a.n * a.nv;
+  if (i >= nvec) return;
+  const int64_t row = i / a.nv, v = i - row * a.nv;
+  constexpr int VPG = KIND == SPH_KIND_V4 ? 32 : 8;
+  const uint32_t bw = a.B[row * a.ng + v / VPG];
+  const int vin = (int)(v % VPG);
+  if constexpr (KIND == SPH_KIND_V4) {
+    const uint32_t byte = ((const uint8_t*)a.A)[i];
+    signs[i] = (uint8_t)(byte & 15u);
+    dir[i] = (uint16_t)((byte >> 4) & 3u);
+    qo[i] = (uint8_t)((byte >> 6) | (((bw >> vin) & 1u) << 2));
+  } else {
+    const uint32_t fw = a.A[i];
+    ((uint16_t*)signs)[i] = (uint16_t)(fw & 0xFFFFu);
+    dir[i] = (uint16_t)((fw >> 16) & 0x3FFFu);
+    qo[i] = (uint8_t)((fw >> 30) | (((bw >> (4 * vin)) & 15u) << 2));
+  }
+}
+
+// ------------------------------------------------------------------------------------------
 // Host dispatch
 // ------------------------------------------------------------------------------------------
 namespace {
@@ -1124,17 +1265,18 @@ struct Launch {
 
 KArgs make_args(const sph_weights* w) {
   KArgs a{};
-  const int kind = sph_kind_of(w->fmt.dir_bits, w->fmt.radius_bits);
+  const int kind = sph_kind_of_fmt(w->fmt.vec_dim, w->fmt.dir_bits, w->fmt.radius_bits);
   const char* base = (const char*)w->d_base;
   a.A = (const uint32_t*)(base + w->off[SPH_OFF_A]);
   a.B = (const uint32_t*)(base + w->off[SPH_OFF_B]);
   a.P = (const uint32_t*)(base + w->off[SPH_OFF_PARAMS]);
   a.C = (const uint16_t*)(base + w->off[SPH_OFF_C]);
   a.T = (const uint4*)(base + w->off[SPH_OFF_TABLES]);
+  a.CB = (const uint16_t*)(base + w->off[SPH_OFF_CODEBOOK]);
   a.t_bytes = (uint32_t)sph_table_bytes(kind, w->fmt.dir_bits);
   a.n = (int)w->n;
   a.nt = (int)((w->n + 15) / 16);
-  a.nv = (int)(w->k / 8);
+  a.nv = (int)(w->k / w->fmt.vec_dim);
   a.ng = (int)(w->k / 128);
   return a;
 }
@@ -1194,6 +1336,21 @@ const void* prefill_fn(int D, int V, int mc) {
   }
   return nullptr;
 }
+
+template <int KIND>
+const void* rowvec_fn_k(int m) {
+  if (m <= 1) return (const void*)k_gemm_rowvec<KIND, 1>;
+  if (m <= 4) return (const void*)k_gemm_rowvec<KIND, 4>;
+  if (m <= 8) return (const void*)k_gemm_rowvec<KIND, 8>;
+  if (m <= 16) return (const void*)k_gemm_rowvec<KIND, 16>;
+  return (const void*)k_gemm_rowvec<KIND, 32>;
+}
+
+const void* rowvec_fn(int kind, int m) {
+  return kind == SPH_KIND_V4 ? rowvec_fn_k<SPH_KIND_V4>(m) : rowvec_fn_k<SPH_KIND_V16>(m);
+}
+
+int fmt_kind(const sph_weights* w) { return sph_kind_of_fmt(w->fmt.vec_dim, w->fmt.dir_bits, w->fmt.radius_bits); }
 
 const void* unpack_fn(int D, int V) {
   switch (sph_kind_of(D, V)) {
@@ -1390,6 +1547,10 @@ sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes) {
   if (!w || !bytes) return SPH_ERR_NULL;
   if (!valid_desc(w)) return SPH_ERR_BAD_DESCRIPTOR;
   if (m < 1 || m > SPH_MAX_BATCH) return SPH_ERR_SHAPE;
+  if (sph_is_rowvec_kind(fmt_kind(w))) {
+    *bytes = 0;
+    return SPH_OK;
+  }
   *bytes = m <= 32 ? plan(w, (int)m).ws_bytes : prefill_plan(w, m).ws_bytes;
   return SPH_OK;
 }
@@ -1404,6 +1565,16 @@ sph_status sph_gemm(const sph_weights* w, const void* d_x, int64_t m, int64_t ld
   if (ldx < w->k || ldy < w->n || ldx % 8 != 0) return SPH_ERR_SHAPE;
   if (y_dtype != SPH_F16 && y_dtype != SPH_F32) return SPH_ERR_SHAPE;
   if ((uintptr_t)d_x % 16 != 0 || (uintptr_t)d_y % 4 != 0) return SPH_ERR_SHAPE;
+  if (sph_is_rowvec_kind(fmt_kind(w))) {
+    // the 4-D and 16-D formats run their batch kernel on slices of 32 activation rows
+    const size_t esz = y_dtype == SPH_F16 ? 2 : 4;
+    for (int64_t b0 = 0; b0 < m; b0 += 32) {
+      const sph_status st = sph_gemm_small(w, (const uint16_t*)d_x + b0 * ldx, std::min<int64_t>(32, m - b0), ldx,
+                                           (char*)d_y + b0 * ldy * esz, ldy, y_dtype, nullptr, 0, stream);
+      if (st != SPH_OK) return st;
+    }
+    return SPH_OK;
+  }
   const PrefillPlan P = prefill_plan(w, m);
   const void* fn = prefill_fn(w->fmt.dir_bits, w->fmt.radius_bits, P.mc);
   if (!fn) return SPH_ERR_UNSUPPORTED_FORMAT;
@@ -1443,6 +1614,20 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
   if (ldx < w->k || ldy < w->n || ldx % 8 != 0) return SPH_ERR_SHAPE;
   if (y_dtype != SPH_F16 && y_dtype != SPH_F32) return SPH_ERR_SHAPE;
   if ((uintptr_t)d_x % 16 != 0 || (uintptr_t)d_y % 4 != 0) return SPH_ERR_SHAPE;
+  if (sph_is_rowvec_kind(fmt_kind(w))) {
+    KArgs a = make_args(w);
+    a.x = (const uint16_t*)d_x;
+    a.ldx = ldx;
+    a.y = d_y;
+    a.ldy = ldy;
+    a.y_f16 = (y_dtype == SPH_F16);
+    a.m = (int)m;
+    void* kargs[] = {&a};
+    if (hipLaunchKernel(rowvec_fn(fmt_kind(w), (int)m), dim3((unsigned)((w->n + RV_WAVES - 1) / RV_WAVES)),
+                        dim3(64 * RV_WAVES), kargs, 0, (hipStream_t)stream) != hipSuccess)
+      return SPH_ERR_HIP;
+    return hipGetLastError() == hipSuccess ? SPH_OK : SPH_ERR_HIP;
+  }
   const Launch L = plan(w, (int)m);
   if (!L.fn) return SPH_ERR_UNSUPPORTED_FORMAT;
   if (L.ws_bytes > 0) {
@@ -1480,9 +1665,13 @@ sph_status sph_unpack(const sph_weights* w, uint8_t* d_signs, uint16_t* d_dir_id
   if (!w || !d_signs || !d_dir_idx || !d_radius_code) return SPH_ERR_NULL;
   if (!valid_desc(w)) return SPH_ERR_BAD_DESCRIPTOR;
   KArgs a = make_args(w);
-  const void* fn = unpack_fn(w->fmt.dir_bits, w->fmt.radius_bits);
+  const int kind = fmt_kind(w);
+  const void* fn = kind == SPH_KIND_V4    ? (const void*)k_unpack_rowvec<SPH_KIND_V4>
+                   : kind == SPH_KIND_V16 ? (const void*)k_unpack_rowvec<SPH_KIND_V16>
+                                          : unpack_fn(w->fmt.dir_bits, w->fmt.radius_bits);
   if (!fn) return SPH_ERR_UNSUPPORTED_FORMAT;
-  const int64_t total = (int64_t)a.nt * a.nv * 16;
+  if (kind == SPH_KIND_V16 && (uintptr_t)d_signs % 2) return SPH_ERR_SHAPE;
+  const int64_t total = sph_is_rowvec_kind(kind) ? (int64_t)a.n * a.nv : (int64_t)a.nt * a.nv * 16;
   const int64_t grid = (total + 255) / 256;
   uint8_t* s = d_signs;
   uint16_t* d = d_dir_idx;

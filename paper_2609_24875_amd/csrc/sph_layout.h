@@ -27,6 +27,15 @@
 //  kind CB13Q4   (D=13,V=4) A, B as CB13 with the low 3 bits of q in B
 //                           C: one 16-bit word per record, bit r = bit 3 of q(r)
 //
+//  Row-planar kinds for 4-D and 16-D vectors (Tab. 7); no tiles, rows stored one after another:
+//  kind V4  (vec 4, D=2, V=3)   A: one byte per vector [n][k/4]: s | z<<4 | (q & 3)<<6
+//                               B: one dword per row and group [n][k/128]: bit v = q(v) >> 2
+//                               table: 64 signed directions T[z<<4 | s] = 4 fp16 (sign-folded)
+//  kind V16 (vec 16, D=14, V=6) A: one dword per vector [n][k/16]: s | z<<16 | (q & 3)<<30
+//                               B: one dword per row and group: bits [4v+3:4v] = q(v) >> 2
+//                               the codebook (2^14 x 16 fp16, 512 KiB) is read from memory
+//  Group parameters of the row-planar kinds: half2 (offset, step) at [n][k/128].
+//
 // Nibble kinds (W2, NIB16*) look the signed direction up in two tables built from the codebook:
 //   T_lo[z*16 + s_lo]   = 4 fp16: element j of c_z for j = 0..3, negated where bit j of s_lo is set
 //   T_hi[s_hi*2^D + z]  = 4 fp16: element 4+j of c_z for j = 0..3, negated where bit j of s_hi is set
@@ -48,7 +57,7 @@
 
 enum sph_kind {
   SPH_KIND_W2 = 0, SPH_KIND_NIB16 = 1, SPH_KIND_NIB16Q8 = 2, SPH_KIND_CB13 = 3, SPH_KIND_NIB16Q2 = 4,
-  SPH_KIND_CB13Q4 = 5, SPH_KIND_NONE = -1
+  SPH_KIND_CB13Q4 = 5, SPH_KIND_V4 = 6, SPH_KIND_V16 = 7, SPH_KIND_NONE = -1
 };
 
 // Offsets inside the device blob (sph_weights.off[]).
@@ -66,6 +75,16 @@ static inline int sph_kind_of(int dir_bits, int radius_bits) {
   if (dir_bits == 13 && radius_bits == 4) return SPH_KIND_CB13Q4;
   return SPH_KIND_NONE;
 }
+
+// Kind of a full format (vector size, D, V): 8-D formats as above; one 4-D and one 16-D format.
+static inline int sph_kind_of_fmt(int vec_dim, int dir_bits, int radius_bits) {
+  if (vec_dim == 8) return sph_kind_of(dir_bits, radius_bits);
+  if (vec_dim == 4 && dir_bits == 2 && radius_bits == 3) return SPH_KIND_V4;
+  if (vec_dim == 16 && dir_bits == 14 && radius_bits == 6) return SPH_KIND_V16;
+  return SPH_KIND_NONE;
+}
+
+static inline bool sph_is_rowvec_kind(int kind) { return kind == SPH_KIND_V4 || kind == SPH_KIND_V16; }
 
 // The codebook kinds keep c_z itself in LDS; the others keep the sign-folded nibble tables.
 static inline bool sph_is_codebook_kind(int kind) { return kind == SPH_KIND_CB13 || kind == SPH_KIND_CB13Q4; }
@@ -88,6 +107,8 @@ static inline int sph_c_halves(int kind) { return kind == SPH_KIND_CB13Q4 ? 1 : 
 // Bytes of the lookup tables kept in the blob: nibble kinds hold T_lo and T_hi (8 bytes per entry,
 // 2^D * 16 entries each); codebook kinds hold the codebook as 16-byte entries.
 static inline uint64_t sph_table_bytes(int kind, int dir_bits) {
+  if (kind == SPH_KIND_V4) return 64 * 8;
+  if (kind == SPH_KIND_V16) return 0;
   if (sph_is_codebook_kind(kind)) return (uint64_t)16 << dir_bits;
   return (uint64_t)2 * 8 * 16 << dir_bits;
 }

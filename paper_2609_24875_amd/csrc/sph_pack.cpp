@@ -16,8 +16,8 @@ static bool f16_sign(uint16_t b) { return (b >> 15) != 0; }
 
 int sph_host_check_format(const sph_format* fmt) {
   if (!fmt) return SPH_ERR_NULL;
-  if (fmt->vec_dim != SPH_VEC || fmt->group_size != SPH_GROUP) return SPH_ERR_UNSUPPORTED_FORMAT;
-  if (sph_kind_of(fmt->dir_bits, fmt->radius_bits) == SPH_KIND_NONE) return SPH_ERR_UNSUPPORTED_FORMAT;
+  if (fmt->group_size != SPH_GROUP) return SPH_ERR_UNSUPPORTED_FORMAT;
+  if (sph_kind_of_fmt(fmt->vec_dim, fmt->dir_bits, fmt->radius_bits) == SPH_KIND_NONE) return SPH_ERR_UNSUPPORTED_FORMAT;
   return SPH_OK;
 }
 
@@ -34,11 +34,27 @@ int sph_host_layout(const sph_format* fmt, int64_t n, int64_t k, uint64_t off[8]
   if (st) return st;
   st = sph_host_check_shape(n, k);
   if (st) return st;
-  const int kind = sph_kind_of(fmt->dir_bits, fmt->radius_bits);
+  const int kind = sph_kind_of_fmt(fmt->vec_dim, fmt->dir_bits, fmt->radius_bits);
   const uint64_t nt = (uint64_t)((n + SPH_TILE_ROWS - 1) / SPH_TILE_ROWS);
   const uint64_t nv = (uint64_t)(k / SPH_VEC), ng = (uint64_t)(k / SPH_GROUP);
   uint64_t p = 0;
   for (int i = 0; i < 8; ++i) off[i] = 0;
+  if (sph_is_rowvec_kind(kind)) {
+    const uint64_t nvd = (uint64_t)(k / fmt->vec_dim), fb = kind == SPH_KIND_V4 ? 1 : 4;
+    off[SPH_OFF_A] = p;
+    p = align_up(p + (uint64_t)n * nvd * fb, SPH_ALIGN);
+    off[SPH_OFF_B] = p;
+    p = align_up(p + (uint64_t)n * ng * 4, SPH_ALIGN);
+    off[SPH_OFF_PARAMS] = p;
+    p = align_up(p + (uint64_t)n * ng * 4, SPH_ALIGN);
+    off[SPH_OFF_TABLES] = p;
+    p = align_up(p + sph_table_bytes(kind, fmt->dir_bits), SPH_ALIGN);
+    off[SPH_OFF_CODEBOOK] = p;
+    p = align_up(p + ((uint64_t)fmt->vec_dim * 2 << fmt->dir_bits), SPH_ALIGN);
+    off[SPH_OFF_C] = p;
+    *total = p;
+    return SPH_OK;
+  }
   off[SPH_OFF_A] = p;
   p = align_up(p + nt * nv * 4 * sph_a_dwords(kind), SPH_ALIGN);
   off[SPH_OFF_B] = p;
@@ -59,17 +75,59 @@ int sph_host_check_codes(const sph_format* fmt, int64_t n, int64_t k, const uint
                          const uint16_t* dir_idx, const uint8_t* radius_code, const uint16_t* gmin,
                          const uint16_t* gstep, const uint16_t* codebook) {
   if (!signs || !dir_idx || !radius_code || !gmin || !gstep || !codebook) return SPH_ERR_NULL;
-  const int64_t nvec = n * (k / SPH_VEC), ngrp = n * (k / SPH_GROUP);
+  const int vec = fmt->vec_dim;
+  const int64_t nvec = n * (k / vec), ngrp = n * (k / SPH_GROUP);
   const uint32_t dmax = 1u << fmt->dir_bits, qmax = 1u << fmt->radius_bits;
   for (int64_t i = 0; i < nvec; ++i)
     if (dir_idx[i] >= dmax || radius_code[i] >= qmax) return SPH_ERR_CODE_RANGE;
+  if (vec == 4)
+    for (int64_t i = 0; i < nvec; ++i)
+      if (signs[i] >= 16) return SPH_ERR_CODE_RANGE;
   for (int64_t i = 0; i < ngrp; ++i) {
     if (!f16_finite(gmin[i])) return SPH_ERR_BAD_VALUE;
     if (!f16_finite(gstep[i]) || f16_sign(gstep[i])) return SPH_ERR_BAD_VALUE;
   }
-  for (int64_t i = 0; i < ((int64_t)SPH_VEC << fmt->dir_bits); ++i)
+  for (int64_t i = 0; i < ((int64_t)vec << fmt->dir_bits); ++i)
     if (!f16_finite(codebook[i]) || f16_sign(codebook[i])) return SPH_ERR_BAD_VALUE;
   return SPH_OK;
+}
+
+// Row-planar packing of the 4-D and 16-D formats (see sph_layout.h). For 16-D vectors the sign
+// array holds one little-endian uint16 per vector.
+static void pack_rowvec(const sph_format* fmt, int kind, int64_t n, int64_t k, const uint8_t* signs,
+                        const uint16_t* dir_idx, const uint8_t* radius_code, const uint16_t* gmin,
+                        const uint16_t* gstep, const uint16_t* codebook, const uint64_t off[8], uint8_t* blob) {
+  const int vec = fmt->vec_dim;
+  const int64_t nvd = k / vec, ng = k / SPH_GROUP, vpg = SPH_GROUP / vec;
+  uint32_t* B = (uint32_t*)(blob + off[SPH_OFF_B]);
+  uint32_t* P = (uint32_t*)(blob + off[SPH_OFF_PARAMS]);
+  const uint16_t* s16 = (const uint16_t*)signs;
+  for (int64_t row = 0; row < n; ++row) {
+    for (int64_t g = 0; g < ng; ++g) {
+      uint32_t b = 0;
+      for (int64_t v = 0; v < vpg; ++v) {
+        const int64_t i = row * nvd + g * vpg + v;
+        const uint32_t q = radius_code[i], z = dir_idx[i];
+        if (kind == SPH_KIND_V4) {
+          blob[off[SPH_OFF_A] + i] = (uint8_t)((signs[i] & 15) | (z << 4) | ((q & 3) << 6));
+          b |= ((q >> 2) & 1) << v;
+        } else {
+          ((uint32_t*)(blob + off[SPH_OFF_A]))[i] = (uint32_t)s16[i] | (z << 16) | ((q & 3) << 30);
+          b |= ((q >> 2) & 15) << (4 * v);
+        }
+      }
+      B[row * ng + g] = b;
+      P[row * ng + g] = (uint32_t)gmin[row * ng + g] | ((uint32_t)gstep[row * ng + g] << 16);
+    }
+  }
+  const uint32_t entries = 1u << fmt->dir_bits;
+  if (kind == SPH_KIND_V4) {
+    uint16_t* T = (uint16_t*)(blob + off[SPH_OFF_TABLES]);
+    for (uint32_t z = 0; z < entries; ++z)
+      for (uint32_t s = 0; s < 16; ++s)
+        for (int j = 0; j < 4; ++j) T[((z << 4) | s) * 4 + j] = codebook[z * 4 + j] ^ (((s >> j) & 1) ? 0x8000 : 0);
+  }
+  std::memcpy(blob + off[SPH_OFF_CODEBOOK], codebook, sizeof(uint16_t) * vec * entries);
 }
 
 // One row's code, or zeros for a padding row.
@@ -81,7 +139,11 @@ void sph_host_pack(const sph_format* fmt, int64_t n, int64_t k, const uint8_t* s
                    const uint16_t* dir_idx, const uint8_t* radius_code, const uint16_t* gmin,
                    const uint16_t* gstep, const uint16_t* codebook, const uint64_t off[8],
                    uint8_t* blob) {
-  const int kind = sph_kind_of(fmt->dir_bits, fmt->radius_bits);
+  const int kind = sph_kind_of_fmt(fmt->vec_dim, fmt->dir_bits, fmt->radius_bits);
+  if (sph_is_rowvec_kind(kind)) {
+    pack_rowvec(fmt, kind, n, k, signs, dir_idx, radius_code, gmin, gstep, codebook, off, blob);
+    return;
+  }
   const int D = fmt->dir_bits;
   const int64_t nt = (n + SPH_TILE_ROWS - 1) / SPH_TILE_ROWS, nv = k / SPH_VEC, ng = k / SPH_GROUP;
   const int adw = sph_a_dwords(kind), bdw = sph_b_dwords(kind);

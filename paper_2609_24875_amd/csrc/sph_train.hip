@@ -276,9 +276,11 @@ bool launch_ok(const void* fn, dim3 grid, dim3 block, hipStream_t s, A... args) 
 
 bool dir_bits_ok(int32_t d) { return d >= 1 && d <= 13; }
 
+// The fine-tuning kernels handle 8-D vectors (the 4-D and 16-D formats are decode-only).
 int check_fq(const sph_format* fmt, int64_t n, int64_t k) {
   int st = sph_host_check_format(fmt);
   if (st) return st;
+  if (fmt->vec_dim != SPH_VEC) return SPH_ERR_UNSUPPORTED_FORMAT;
   return sph_host_check_shape(n, k);
 }
 

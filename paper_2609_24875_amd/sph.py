@@ -115,17 +115,17 @@ def make_format(dir_bits: int, radius_bits: int, vec_dim: int = 8, group_size: i
     return CFormat(vec_dim, dir_bits, radius_bits, group_size)
 
 
-def format_supported(dir_bits: int, radius_bits: int) -> bool:
-    return bool(load_library().sph_format_supported(ctypes.byref(make_format(dir_bits, radius_bits))))
+def format_supported(dir_bits: int, radius_bits: int, vec_dim: int = 8) -> bool:
+    return bool(load_library().sph_format_supported(ctypes.byref(make_format(dir_bits, radius_bits, vec_dim))))
 
 
 def status_str(status: int) -> str:
     return load_library().sph_status_str(status).decode()
 
 
-def packed_bytes(dir_bits: int, radius_bits: int, n: int, k: int) -> int:
+def packed_bytes(dir_bits: int, radius_bits: int, n: int, k: int, vec_dim: int = 8) -> int:
     out = ctypes.c_size_t(0)
-    _check(load_library().sph_packed_bytes(ctypes.byref(make_format(dir_bits, radius_bits)),
+    _check(load_library().sph_packed_bytes(ctypes.byref(make_format(dir_bits, radius_bits, vec_dim)),
                                            n, k, ctypes.byref(out)), "sph_packed_bytes")
     return out.value
 
@@ -150,6 +150,7 @@ class SphWeights:
     dir_bits: int
     radius_bits: int
     workspaces: dict = field(default_factory=dict)
+    vec_dim: int = 8
 
     @property
     def nbytes(self) -> int:
@@ -157,21 +158,21 @@ class SphWeights:
 
 
 def pack(dir_bits: int, radius_bits: int, codes: dict, codebook, device="cuda", stream=None,
-         buffer=None) -> SphWeights:
+         buffer=None, vec_dim: int = 8) -> SphWeights:
     """Pack logical codes (see ``synth``) into a device buffer (allocated unless ``buffer`` is
-    given) with sph_pack_weights."""
+    given) with sph_pack_weights. ``vec_dim`` 4, 8 or 16; 16-D signs are uint16 per vector."""
     import torch
     lib = load_library()
-    signs = _host(codes["signs"], np.uint8)
+    signs = _host(codes["signs"], np.uint8 if vec_dim <= 8 else np.uint16)
     n, nv = signs.shape
-    k = nv * 8
+    k = nv * vec_dim
     dirs = _host(codes["dir"], np.uint16)
     q = _host(codes["q"], np.uint8)
     gmin = _host(codes["gmin"], np.uint16)
     gstep = _host(codes["gstep"], np.uint16)
     cb = _host(codebook, np.uint16)
-    fmt = make_format(dir_bits, radius_bits)
-    need = packed_bytes(dir_bits, radius_bits, n, k)
+    fmt = make_format(dir_bits, radius_bits, vec_dim)
+    need = packed_bytes(dir_bits, radius_bits, n, k, vec_dim)
     if buffer is None:
         buffer = torch.empty(need, dtype=torch.uint8, device=device)
     w = CWeights()
@@ -180,7 +181,7 @@ def pack(dir_bits: int, radius_bits: int, codes: dict, codebook, device="cuda", 
                               buffer.data_ptr(), buffer.numel(), _stream_handle(stream),
                               ctypes.byref(w))
     _check(st, "sph_pack_weights")
-    return SphWeights(w, buffer, n, k, dir_bits, radius_bits)
+    return SphWeights(w, buffer, n, k, dir_bits, radius_bits, vec_dim=vec_dim)
 
 
 def workspace_bytes(w: SphWeights, m: int) -> int:
@@ -256,15 +257,17 @@ def unpack(w: SphWeights, stream=None) -> dict:
     """Logical codes read back through the kernels' field extraction (sph_unpack)."""
     import torch
     dev = w.buffer.device
-    nv = w.k // 8
-    s = torch.empty((w.n, nv), dtype=torch.uint8, device=dev)
+    nv = w.k // w.vec_dim
+    s = torch.empty((w.n, nv), dtype=torch.uint8 if w.vec_dim <= 8 else torch.int16, device=dev)
     d = torch.empty((w.n, nv), dtype=torch.int16, device=dev)
     q = torch.empty((w.n, nv), dtype=torch.uint8, device=dev)
     st = load_library().sph_unpack(ctypes.byref(w.desc), s.data_ptr(), d.data_ptr(), q.data_ptr(),
                                    _stream_handle(stream))
     _check(st, "sph_unpack")
     torch.cuda.synchronize(dev)
-    return {"signs": s.cpu().numpy(), "dir": d.cpu().numpy().view(np.uint16), "q": q.cpu().numpy()}
+    sg = s.cpu().numpy()
+    return {"signs": sg if w.vec_dim <= 8 else sg.view(np.uint16), "dir": d.cpu().numpy().view(np.uint16),
+            "q": q.cpu().numpy()}
 
 
 def _dev_f32_matrix(w):

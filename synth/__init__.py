@@ -42,7 +42,16 @@ FORMATS = {
     "W2_63": (6, 3),    # bit-allocation splits of the W2 budget: 8 sign + 6 direction + 3 radius,
     "W2_72": (7, 2),    # 8 + 7 + 2,
     "W2_82": (8, 2),    # 8 + 8 + 2
+    "V4": (2, 3),       # 4-D vectors: 4 sign + 2-bit direction + 3-bit radius (2.25 bpw payload)
+    "V16": (14, 6),     # 16-D vectors: 16 sign + 14-bit direction + 6-bit radius (2.25 bpw payload)
 }
+
+# Vector size of each format (8 unless listed).
+FORMAT_DIM = {"V4": 4, "V16": 16}
+
+
+def fmt_dim(fmt: str) -> int:
+    return FORMAT_DIM.get(fmt, VEC)
 
 
 def rng(*key: int) -> np.random.Generator:
@@ -60,11 +69,13 @@ def random_codebook(dir_bits: int, g: np.random.Generator, dim: int = VEC) -> np
     return f16_bits(a)
 
 
-def uniform_codes(n: int, k: int, dir_bits: int, radius_bits: int, g: np.random.Generator) -> dict:
-    """Independent uniform signs, direction indices and radius levels."""
-    nv = k // VEC
+def uniform_codes(n: int, k: int, dir_bits: int, radius_bits: int, g: np.random.Generator,
+                  dim: int = VEC) -> dict:
+    """Independent uniform signs, direction indices and radius levels (signs are one byte per
+    vector for 4-D and 8-D vectors, 16 bits for 16-D)."""
+    nv = k // dim
     return {
-        "signs": g.integers(0, 256, (n, nv), dtype=np.uint8),
+        "signs": g.integers(0, 1 << dim, (n, nv)).astype(np.uint8 if dim <= 8 else np.uint16),
         "dir": g.integers(0, 1 << dir_bits, (n, nv), dtype=np.uint16),
         "q": g.integers(0, 1 << radius_bits, (n, nv), dtype=np.uint8),
     }

@@ -235,3 +235,46 @@ def test_training_entry_points_validate_before_any_hip_call():
                                        64 * 16 * 32 - 1, None) == 6
     assert lib.sph_fake_quant_backward(ctypes.byref(f), 16, 128, P, P, P, P, P, P, 128, P, P, P, P, None,
                                        1 << 20, None) == 1
+
+
+@needs_lib
+def test_vector_size_variants_supported_and_sized():
+    assert pkg.format_supported(2, 3, 4) and pkg.format_supported(14, 6, 16)
+    assert not pkg.format_supported(6, 4, 4) and not pkg.format_supported(13, 3, 16)
+    assert not pkg.format_supported(2, 3, 8) and not pkg.format_supported(2, 3, 2)
+    n, k = 4096, 4096
+    # 4-D: one byte per vector, one dword of high radius bits and one of parameters per group
+    got = pkg.packed_bytes(2, 3, n, k, 4)
+    base = n * k // 4 + n * (k // 128) * 8 + 64 * 8 + 4 * 4 * 2
+    assert base <= got <= base + 5 * 256
+    # 16-D: one dword per vector, two dwords per group, the 512 KiB codebook
+    got = pkg.packed_bytes(14, 6, n, k, 16)
+    base = n * k // 16 * 4 + n * (k // 128) * 8 + (1 << 14) * 16 * 2
+    assert base <= got <= base + 5 * 256
+    # payload 2.25 bits per weight plus 0.25 of fp16 group parameters, besides the codebook
+    assert (got - (1 << 14) * 32) * 8 / (n * k) <= 2.5 + 1e-3
+
+
+@needs_lib
+def test_vector_size_pack_validation():
+    g = synth.rng(9)
+    codes = synth.uniform_codes(16, 128, 2, 3, g, dim=4)
+    codes["gmin"], codes["gstep"] = synth.row_scale_group_params(16, 128, 3, g)
+    cb = synth.random_codebook(2, g, dim=4)
+    lib = pkg.load_library()
+
+    def st(c, fmt=B.make_format(2, 3, 4)):
+        arrs = [np.ascontiguousarray(c[key]) for key in ("signs", "dir", "q", "gmin", "gstep")]
+        w = B.CWeights()
+        return lib.sph_pack_weights(ctypes.byref(fmt), 16, 128, *[a.ctypes.data for a in arrs], cb.ctypes.data,
+                                    0x10000, 1 << 30, None, ctypes.byref(w))
+    bad = dict(codes, signs=codes["signs"].copy())
+    bad["signs"][2, 3] = 16                     # only 4 sign bits
+    assert st(bad) == 4
+    bad = dict(codes, q=codes["q"].copy())
+    bad["q"][0, 0] = 8
+    assert st(bad) == 4
+    enc = ctypes.c_int
+    f4 = B.make_format(2, 3, 4)
+    assert lib.sph_encode(ctypes.byref(f4), 16, 128, 0x10000, 128, 0x20000, 0x30000, 0x40000, 0x50000,
+                          0x60000, 0x70000, None) == 3     # the encoder is 8-D only

@@ -235,3 +235,66 @@ def test_prefill_gemm_full_size_sampled_rows(fmt):
         rows[0], rows[-1] = 0, n - 1
         ref = O.gemm_rows(codes, cb, x, rows)
         assert O.rel_err(y[:, rows], ref) <= TOL
+
+
+# ------------------------------------------------------------------ 4-D and 16-D vectors (Tab. 7)
+
+DIM_FMTS = ["V4", "V16"]
+
+
+def dim_case(fmt, n, k, seed):
+    D, V = synth.FORMATS[fmt]
+    dim = synth.fmt_dim(fmt)
+    g = synth.rng(seed, n, k, dim, synth.STREAM_CODES)
+    codes = synth.uniform_codes(n, k, D, V, g, dim=dim)
+    codes["gmin"], codes["gstep"] = synth.row_scale_group_params(n, k, V, g)
+    cb = synth.random_codebook(D, synth.rng(seed, n, k, dim, synth.STREAM_CODEBOOK), dim=dim)
+    return D, V, dim, codes, cb
+
+
+@pytest.mark.parametrize("fmt", DIM_FMTS)
+def test_vector_size_unpack_bit_exact(fmt):
+    D, V, dim, codes, cb = dim_case(fmt, 87, 640, 11)
+    w = pkg.pack(D, V, codes, cb, device=DEV, vec_dim=dim)
+    back = pkg.unpack(w)
+    for key in ("signs", "dir", "q"):
+        assert np.array_equal(back[key], codes[key]), key
+
+
+@pytest.mark.parametrize("fmt", DIM_FMTS)
+@pytest.mark.parametrize("n,k", [(87, 640), (16, 128), (1, 256), (300, 8192), (40, 4224)])
+def test_vector_size_gemv_parity(fmt, n, k):
+    D, V, dim, codes, cb = dim_case(fmt, n, k, 12)
+    w = pkg.pack(D, V, codes, cb, device=DEV, vec_dim=dim)
+    x = synth.activations(1, k, synth.rng(12, n, k, synth.STREAM_X))
+    y = pkg.gemv(w, to_dev_f16(x)[0]).cpu().numpy()
+    ref = O.gemv(codes, cb, x)
+    if n >= 16:
+        assert O.rel_err(y, ref) <= TOL
+    bound = apriori_bound(codes, cb, x)[0]
+    assert np.all(np.abs(y - ref) <= k * 2.0**-23 * bound + 1e-30)
+
+
+@pytest.mark.parametrize("fmt", DIM_FMTS)
+@pytest.mark.parametrize("m", [2, 5, 17, 32, 100])
+def test_vector_size_batched_parity(fmt, m):
+    n, k = 75, 1152
+    D, V, dim, codes, cb = dim_case(fmt, n, k, 13)
+    w = pkg.pack(D, V, codes, cb, device=DEV, vec_dim=dim)
+    x = synth.activations(m, k, synth.rng(13, m, k, synth.STREAM_X))
+    y = pkg.gemm(w, to_dev_f16(x)).cpu().numpy()
+    ref = O.gemm(codes, cb, x)
+    assert O.rel_err(y, ref) <= TOL
+    assert np.all(np.abs(y - ref) <= f16_weight_bound(codes, cb, x, k) + 1e-30)
+
+
+@pytest.mark.parametrize("fmt", DIM_FMTS)
+def test_vector_size_full_size_sampled(fmt):
+    n, k = 12288, 4096
+    D, V, dim, codes, cb = dim_case(fmt, n, k, 14)
+    w = pkg.pack(D, V, codes, cb, device=DEV, vec_dim=dim)
+    x = synth.activations(1, k, synth.rng(14, synth.STREAM_X))
+    y = pkg.gemv(w, to_dev_f16(x)[0]).cpu().numpy()
+    rows = np.unique(np.concatenate([[0, n - 1], np.random.default_rng(14).integers(0, n, 48)]))
+    ref = O.gemm_rows(codes, cb, x, rows)[0]
+    assert O.rel_err(y[rows], ref) <= TOL

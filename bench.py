@@ -40,9 +40,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source and compile flags the counters were taken with: any change to
 # the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "b3f9d293118efa124a69f58f85369bd75c1b84e6d54510059e8bf329389ce343": {
-        "7168x5120-m1": 11943949, "5120x5120-m1": 9339802,
-        "51200x5120-m1": 82789648, "5120x25600-m1": 42926722},
+    "df175ada93870fab40128b4c006d5d46b34608495db4ab444c6235968bc8feb7": {
+        "7168x5120-m1": 11941472, "5120x5120-m1": 9351031,
+        "51200x5120-m1": 82781975, "5120x25600-m1": 42898406},
 }
 
 
@@ -498,6 +498,8 @@ def main():
 
 def kernel_label(fmt, m):
     """The decode kernel variant the library picks for this format and batch."""
+    if fmt in synth.FORMAT_DIM:
+        return f"k_gemm_rowvec<{fmt},MB={min(32, 1 << (m - 1).bit_length()) if m > 1 else 1}> (one wave per row)"
     if m == 1:
         return f"k_gemm_valu<{fmt},M=1> (vector ALU)"
     if m <= 8:

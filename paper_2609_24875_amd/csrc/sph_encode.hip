@@ -18,6 +18,7 @@
 //                (integer LDS atomics per block, integer sums across blocks, so the order of
 //                arrival does not matter), renormalisation.
 #include <hip/hip_runtime.h>
+#include <limits.h>
 #include <math.h>
 #include <stdint.h>
 
@@ -178,6 +179,175 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncArgs a) {
       if ((threadIdx.x & 15) == 0) {
         a.gmin[i >> 4] = lo16;
         a.gstep[i >> 4] = st16;
+      }
+    }
+  }
+}
+
+// Matrix-core direction search for the 2^13-entry codebook (exact in fp16). A unit direction d is
+// split as d_hi = fp16(d), d_lo = fp16(d - d_hi); with K = 16 = (c, c) . (d_hi, d_lo) one
+// v_mfma_f32_16x16x16_f16 scores 16 entries against 16 vectors with exact products and fp32
+// sums. |score - c.d| <= 2^-22 + 8 * 2^-24 (the split) + 16 * 2^-24 * 2 (fp32 sums) < delta =
+// 3e-6 (the matrix cores keep fp16 subnormal inputs, which the split produces for coordinates
+// below 2^-14). The fp64 argmax e* then has score >= s(e*) - delta >= best score - 2 delta:
+// every entry within kMxSlack (> 2 delta, with margin) of the best score is a candidate. Pass 1 finds each vector's best score; pass 2 rescores, and evaluates the fp64
+// cosine (the same FMA chain as the vector-ALU search, in ascending entry order) only for the
+// candidates. The result equals the full fp64 scan's. Lane layout: vector j = lane % 16 of each 16-vector block
+// (one radius group), entries 4 * (lane / 16) + e of each 16-entry block; the four lanes of a
+// vector are combined at the end (larger cosine, then lower index).
+constexpr int kMxWaves = 8;
+constexpr int kMxNB = 4;                                   // 16-vector blocks per wave
+constexpr int kMxVecPerWg = kMxWaves * kMxNB * 16;         // 512
+constexpr int kMxMaxEntries = 8192;
+constexpr float kMxSlack = 2e-5f;
+
+typedef _Float16 h4v __attribute__((ext_vector_type(4)));
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+// A operand of lane (j, qd) for entry block e0: coordinates 4 * (qd & 1) .. + 3 of entry e0 + j
+// (k 8..15 repeat k 0..7), one 8-byte LDS read.
+__device__ __forceinline__ h4v mx_a_operand(const uint4* cbl, int e0, int j, int qd) {
+  return __builtin_bit_cast(h4v, ((const uint2*)cbl)[(e0 + j) * 2 + (qd & 1)]);
+}
+
+// Scores of non-negative vectors are compared through their bit patterns as signed integers:
+// for non-negative floats the order is the same, and integer max needs no NaN canonicalisation.
+__device__ __forceinline__ int fbits(float x) { return __builtin_bit_cast(int, x); }
+__device__ __forceinline__ int max4bits(const f4v acc) {
+  return max(max(fbits(acc[0]), fbits(acc[1])), max(fbits(acc[2]), fbits(acc[3])));
+}
+
+__global__ __launch_bounds__(64 * kMxWaves) void k_encode_mx(EncArgs a, int64_t nchunks) {
+  __shared__ uint4 cbl[kMxMaxEntries];   // the fp16 codebook, 16 bytes per entry (2^13 entries)
+  for (int t = threadIdx.x; t < kMxMaxEntries; t += 64 * kMxWaves) cbl[t] = ((const uint4*)a.cb)[t];
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = lane & 15, qd = lane >> 4;
+  for (int64_t ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
+    const int64_t v0 = ch * kMxVecPerWg + (int64_t)wave * (kMxNB * 16);
+    double d[kMxNB][8];
+    h4v bop[kMxNB];
+    bool ok[kMxNB];
+#pragma unroll
+    for (int nb = 0; nb < kMxNB; ++nb) {
+      const int64_t i = v0 + nb * 16 + j;
+      ok[nb] = i < a.nvec;
+      double av[8];
+      uint32_t neg;
+      if (ok[nb]) {
+        decompose(a.w, a.ldw, a.nv, i, av, d[nb], neg);
+      } else {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) d[nb][t] = 0.0;
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const double x = d[nb][4 * (qd & 1) + t];
+        const _Float16 hi = (_Float16)(float)x;
+        bop[nb][t] = qd < 2 ? hi : (_Float16)(float)(x - (double)hi);
+      }
+    }
+    // pass 1: the best matrix-core score of every vector (scores of the non-negative entries and
+    // directions are >= 0 up to rounding; only a zero vector has its best at 0)
+    int mx[kMxNB];
+#pragma unroll
+    for (int nb = 0; nb < kMxNB; ++nb) mx[nb] = INT_MIN;
+#pragma unroll 4
+    for (int e0 = 0; e0 < kMxMaxEntries; e0 += 16) {
+      const h4v aop = mx_a_operand(cbl, e0, j, qd);
+#pragma unroll
+      for (int nb = 0; nb < kMxNB; ++nb) {
+        const f4v acc = __builtin_amdgcn_mfma_f32_16x16x16f16(aop, bop[nb], f4v{0.0f, 0.0f, 0.0f, 0.0f}, 0, 0, 0);
+        mx[nb] = max(mx[nb], max4bits(acc));
+      }
+    }
+    int thr[kMxNB];
+#pragma unroll
+    for (int nb = 0; nb < kMxNB; ++nb) {
+      int v = max(mx[nb], __shfl_xor(mx[nb], 16, 64));
+      v = max(v, __shfl_xor(v, 32, 64));
+      const float t = __builtin_bit_cast(float, v) - kMxSlack;
+      // a threshold below 0 (a zero vector) takes every entry; vectors past the end take none
+      thr[nb] = !ok[nb] ? INT_MAX : t < 0.0f ? INT_MIN : fbits(t);
+    }
+    // pass 2: fp64 cosines of the candidates, ascending entry order per lane
+    double best[kMxNB];
+    int bz[kMxNB];
+#pragma unroll
+    for (int nb = 0; nb < kMxNB; ++nb) {
+      best[nb] = -INFINITY;
+      bz[nb] = kMxMaxEntries;
+    }
+#pragma unroll 2
+    for (int e0 = 0; e0 < kMxMaxEntries; e0 += 16) {
+      const h4v aop = mx_a_operand(cbl, e0, j, qd);
+#pragma unroll
+      for (int nb = 0; nb < kMxNB; ++nb) {
+        const f4v acc = __builtin_amdgcn_mfma_f32_16x16x16f16(aop, bop[nb], f4v{0.0f, 0.0f, 0.0f, 0.0f}, 0, 0, 0);
+        if (max4bits(acc) >= thr[nb]) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (fbits(acc[e]) >= thr[nb]) {
+              const int ent = e0 + 4 * qd + e;
+              const uint4 ce = cbl[ent];
+              const uint32_t cw[4] = {ce.x, ce.y, ce.z, ce.w};
+              double c[8];
+#pragma unroll
+              for (int t = 0; t < 8; ++t) c[t] = h2d((uint16_t)(cw[t / 2] >> (16 * (t & 1))));
+              double sc = d[nb][0] * c[0];
+#pragma unroll
+              for (int t = 1; t < 8; ++t) sc = fma(d[nb][t], c[t], sc);
+              if (sc > best[nb]) {
+                best[nb] = sc;
+                bz[nb] = ent;
+              }
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int nb = 0; nb < kMxNB; ++nb) {
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        const double ob = __shfl_xor(best[nb], o, 64);
+        const int oz = __shfl_xor(bz[nb], o, 64);
+        if (ob > best[nb] || (ob == best[nb] && oz < bz[nb])) {
+          best[nb] = ob;
+          bz[nb] = oz;
+        }
+      }
+      if (bz[nb] >= a.ncb) bz[nb] = 0;   // no candidate (non-finite input): any valid index
+    }
+    // Eq. 6 and 7 as in k_encode; the four lanes of a vector agree, the first writes
+#pragma unroll
+    for (int nb = 0; nb < kMxNB; ++nb) {
+      const int64_t i = v0 + nb * 16 + j;
+      double av[8] = {0, 0, 0, 0, 0, 0, 0, 0}, dd[8];
+      uint32_t neg = 0;
+      if (ok[nb]) decompose(a.w, a.ldw, a.nv, i, av, dd, neg);
+      double c[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) c[t] = h2d(a.cb[(int64_t)bz[nb] * 8 + t]);
+      const double rt = dot8_pairwise(av, c);
+      double lo = rt, hi = rt;
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        lo = fmin(lo, __shfl_xor(lo, o, 16));
+        hi = fmax(hi, __shfl_xor(hi, o, 16));
+      }
+      const uint16_t lo16 = d2h(lo), st16 = d2h((hi - lo) / (double)a.vmax);
+      const double lod = h2d(lo16), std_ = h2d(st16);
+      int q = 0;
+      if (std_ > 0.0) q = (int)fmin(fmax(rint((rt - lod) / std_), 0.0), (double)a.vmax);
+      if (ok[nb] && qd == 0) {
+        a.signs[i] = (uint8_t)neg;
+        a.dir[i] = (uint16_t)bz[nb];
+        a.q[i] = (uint8_t)q;
+        if (j == 0) {
+          a.gmin[i >> 4] = lo16;
+          a.gstep[i >> 4] = st16;
+        }
       }
     }
   }
@@ -578,6 +748,17 @@ sph_status sph_encode(const sph_format* fmt, int64_t n, int64_t k, const float* 
   a.q = d_radius_code;
   a.gmin = d_group_min;
   a.gstep = d_group_step;
+  if (a.ncb == kMxMaxEntries) {
+    // the 2^13-entry codebook: matrix-core search, one 128 KiB codebook copy per CU
+    const int64_t nchunks = (a.nvec + kMxVecPerWg - 1) / kMxVecPerWg;
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      cus = 256;
+    const int64_t grid = std::min<int64_t>(nchunks, cus);
+    if (!launch_ok((const void*)k_encode_mx, dim3((unsigned)grid), dim3(64 * kMxWaves), (hipStream_t)stream, a, nchunks))
+      return SPH_ERR_HIP;
+    return SPH_OK;
+  }
   const int64_t grid = (a.nvec + kThreads * kVpt - 1) / (kThreads * kVpt);
   if (!launch_ok((const void*)k_encode, dim3((unsigned)grid), dim3(kThreads), (hipStream_t)stream, a))
     return SPH_ERR_HIP;

@@ -155,8 +155,9 @@ FP64_PEAK_TFS = 78.6   # MI355X fp64 vector peak
 def encode_main(args):
     """Encoder benchmark: a step is sph_encode of one 12288x4096 fp32 matrix (the 8B-class
     gate/up shape) plus sph_kmeans_codebook on it with the paper's 65,536 samples and 20
-    iterations. The dominant kernel is the Eq. 5 nearest-direction search inside the encoder,
-    bound by the fp64 vector ALUs: 2^D cosines of 8 terms (8 multiplies + 7 adds) per vector."""
+    iterations. The dominant kernel is the Eq. 5 nearest-direction search inside the encoder:
+    for small codebooks 2^D fp64 cosines of 8 terms (8 multiplies + 7 adds) per vector on the
+    vector ALUs, for the 2^13-entry codebook two matrix-core passes of 16-deep fp16 products."""
     import torch
 
     import paper_2609_24875_amd as pkg
@@ -194,7 +195,11 @@ def encode_main(args):
     enc_ms = timed(enc, args.steps)
     km_ms = timed(km, max(1, args.steps // 4))
     nvec = n * k // 8
-    flops = nvec * (1 << D) * 15
+    # 2^13 entries: the search runs on the matrix cores (two passes of 16-deep fp16 products per
+    # entry and vector, hi/lo split of the direction); smaller codebooks: fp64 cosines on the ALUs
+    mfma = D == 13
+    flops = nvec * (1 << D) * (2 * 16 * 2 if mfma else 15)
+    peak = MFMA_F16_PEAK_TFS if mfma else FP64_PEAK_TFS
     out = {
         "metric": "device encoder: weights encoded per second (Eq. 3, 5-7) and k-means codebook time",
         "value": round(n * k / (enc_ms / 1e3) / 1e9, 3),
@@ -208,9 +213,10 @@ def encode_main(args):
         "config": {"workload": f"encode-{fmt}-{n}x{k}", "format": f"{fmt} (8 sign + {D} direction + "
                    f"{V} radius bits)", "kmeans_samples": ns, "kmeans_iters": iters,
                    "encode_ms": round(enc_ms, 4), "kmeans_ms": round(km_ms, 4)},
-        "roofline": {"kernel": f"k_encode {fmt} {n}x{k}", "bound": "alu",
-                     "achieved": round(flops / (enc_ms / 1e3) / 1e12, 2), "peak": FP64_PEAK_TFS,
-                     "unit": "TFLOP/s", "frac": round(flops / (enc_ms / 1e3) / 1e12 / FP64_PEAK_TFS, 4),
+        "roofline": {"kernel": f"{'k_encode_mx' if mfma else 'k_encode'} {fmt} {n}x{k}",
+                     "bound": "mfma" if mfma else "alu",
+                     "achieved": round(flops / (enc_ms / 1e3) / 1e12, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(flops / (enc_ms / 1e3) / 1e12 / peak, 4),
                      "traffic": None, "flops_per_launch": flops},
     }
     if not args.no_cpu_baseline:

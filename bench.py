@@ -510,8 +510,8 @@ def kernel_label(fmt, m):
         return f"k_gemm_valu<{fmt},M=1> (vector ALU)"
     if m <= 8:
         return f"k_gemm_valu<{fmt},M={4 if m <= 4 else 8}> (4x4x4 MFMA blocks)"
-    if m <= 32:
-        return f"k_gemm_valu<{fmt},M={16 if m <= 16 else 32}> (16x16x32 MFMA tiles)"
+    if m <= 16:
+        return f"k_gemm_valu<{fmt},M=16> (16x16x32 MFMA tiles)"
     return f"k_gemm_prefill<{fmt}> (16x16x32 MFMA, LDS-staged activations)"
 
 

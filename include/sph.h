@@ -109,9 +109,11 @@ sph_status sph_gemv(const sph_weights* w, const void* d_x, void* d_y, sph_dtype 
                     void* d_ws, size_t ws_bytes, void* stream);
 
 /* Y = X W^T for 1 <= m <= 32 activation rows: d_x is device fp16[m][ldx] (ldx >= k), d_y is
- * device [m][ldy] of y_dtype (ldy >= n). Batches up to 8 run on the vector ALUs with exact fp16
- * products and fp32 accumulation; batches 9..32 round each decoded weight once to fp16 and run
- * on the matrix cores (MFMA) with fp32 accumulation. Asynchronous on `stream`. */
+ * device [m][ldy] of y_dtype (ldy >= n). Batch 1 runs on the vector ALUs with exact fp16 products
+ * and fp32 accumulation; batches 2..32 round each decoded weight once to fp16 and run on the
+ * matrix cores (MFMA: 4x4x4 blocks up to 8, 16x16x32 tiles up to 16, above that the prefill
+ * kernel of sph_gemm with 32 activation rows staged in LDS) with fp32 accumulation.
+ * Asynchronous on `stream`. */
 sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y,
                           int64_t ldy, sph_dtype y_dtype, void* d_ws, size_t ws_bytes,
                           void* stream);
@@ -128,9 +130,9 @@ sph_status sph_gemm(const sph_weights* w, const void* d_x, int64_t m, int64_t ld
 
 /* Device workspace needed by sph_gemv (m = 1), sph_gemm_small or sph_gemm for this matrix and
  * batch (1 <= m <= 65536) on the current device (0 when the call needs none; d_ws may then be
- * NULL). For m <= 32 the workspace holds split-K partial sums and one arrival counter per 16-row
- * tile: it must be 256-byte aligned and zero-filled before its first use, every call leaves it
- * zero-filled again. For m > 32 it holds fp32 partial outputs and needs no initial contents.
+ * NULL). It holds split-K partial sums (and, for m <= 16, one arrival counter per 16-row tile):
+ * it must be 256-byte aligned and zero-filled before its first use, and every call leaves it
+ * zero-filled again (above m = 32 it needs no initial contents, but is still left zero-filled).
  * Calls that may run concurrently must not share one. */
 sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes);
 

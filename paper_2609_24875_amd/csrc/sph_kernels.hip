@@ -1099,14 +1099,18 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
   }
 }
 
-// y[b][row] = sum over the K ranges, in range order, of the prefill partials.
+// y[b][row] = sum over the K ranges, in range order, of the prefill partials, which are cleared.
 __global__ void __launch_bounds__(256) k_prefill_reduce(KArgs a) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t npad = (int64_t)a.nt * 16;
   if (t >= (int64_t)a.m * a.n) return;
   const int b = (int)(t / a.n), row = (int)(t % a.n);
   float s = 0.0f;
-  for (int z = 0; z < a.ks; ++z) s += a.ws_part[((int64_t)z * a.m + b) * npad + row];
+  for (int z = 0; z < a.ks; ++z) {
+    float* p = a.ws_part + ((int64_t)z * a.m + b) * npad + row;
+    s += *p;
+    *p = 0.0f;   // the workspace is left zero-filled, as the batch 1..32 calls promise
+  }
   store_y(a, b, row, s);
 }
 
@@ -1309,6 +1313,7 @@ const void* pick(int D, int V, int M) {
 
 template <int KIND, int D>
 const void* prefill_fn_mc(int mc) {
+  if (mc == 32) return (const void*)k_gemm_prefill<KIND, D, 32>;
   if constexpr (IS_CB<KIND>) {
     return (const void*)k_gemm_prefill<KIND, D, 64>;
   } else {
@@ -1317,8 +1322,9 @@ const void* prefill_fn_mc(int mc) {
   }
 }
 
-// Batch rows per workgroup: 128 for the nibble kinds at batches above 64, else 64.
+// Batch rows per workgroup: 32 for batches 17..32, 128 for the nibble kinds above 64, else 64.
 int prefill_mc(int D, int V, int64_t m) {
+  if (m <= 32) return 32;
   return (sph_is_codebook_kind(sph_kind_of(D, V)) || m <= 64) ? 64 : 128;
 }
 
@@ -1461,6 +1467,39 @@ Launch plan(const sph_weights* w, int m) {
   return L;
 }
 
+// The prefill kernel (and its split-K reduction) for a validated call with m > 16.
+sph_status launch_prefill(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y, int64_t ldy,
+                          sph_dtype y_dtype, void* d_ws, size_t ws_bytes, hipStream_t s) {
+  const PrefillPlan P = prefill_plan(w, m);
+  const void* fn = prefill_fn(w->fmt.dir_bits, w->fmt.radius_bits, P.mc);
+  if (!fn) return SPH_ERR_UNSUPPORTED_FORMAT;
+  if (P.ws_bytes > 0) {
+    if (!d_ws) return SPH_ERR_NULL;
+    if (ws_bytes < P.ws_bytes) return SPH_ERR_BUFFER_TOO_SMALL;
+    if ((uintptr_t)d_ws % 256 != 0) return SPH_ERR_SHAPE;
+  }
+  KArgs a = make_args(w);
+  a.x = (const uint16_t*)d_x;
+  a.ldx = ldx;
+  a.y = d_y;
+  a.ldy = ldy;
+  a.y_f16 = (y_dtype == SPH_F16);
+  a.m = (int)m;
+  a.ks = P.ks;
+  a.ws_part = (float*)d_ws;
+  void* kargs[] = {&a};
+  if (hipLaunchKernel(fn, dim3(P.gx, P.gy, P.ks), dim3(PF_THREADS), kargs, 0, s) != hipSuccess) return SPH_ERR_HIP;
+  if (hipGetLastError() != hipSuccess) return SPH_ERR_HIP;
+  if (P.ks > 1) {
+    const int64_t total = (int64_t)m * w->n;
+    if (hipLaunchKernel((const void*)k_prefill_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), kargs, 0, s) !=
+        hipSuccess)
+      return SPH_ERR_HIP;
+    if (hipGetLastError() != hipSuccess) return SPH_ERR_HIP;
+  }
+  return SPH_OK;
+}
+
 bool valid_desc(const sph_weights* w) {
   if (!w || w->magic != SPH_MAGIC || w->layout_version != SPH_LAYOUT_VERSION || !w->d_base) return false;
   if (sph_host_check_format(&w->fmt) != SPH_OK || sph_host_check_shape(w->n, w->k) != SPH_OK) return false;
@@ -1551,7 +1590,7 @@ sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes) {
     *bytes = 0;
     return SPH_OK;
   }
-  *bytes = m <= 32 ? plan(w, (int)m).ws_bytes : prefill_plan(w, m).ws_bytes;
+  *bytes = m <= 16 ? plan(w, (int)m).ws_bytes : prefill_plan(w, m).ws_bytes;
   return SPH_OK;
 }
 
@@ -1575,35 +1614,7 @@ sph_status sph_gemm(const sph_weights* w, const void* d_x, int64_t m, int64_t ld
     }
     return SPH_OK;
   }
-  const PrefillPlan P = prefill_plan(w, m);
-  const void* fn = prefill_fn(w->fmt.dir_bits, w->fmt.radius_bits, P.mc);
-  if (!fn) return SPH_ERR_UNSUPPORTED_FORMAT;
-  if (P.ws_bytes > 0) {
-    if (!d_ws) return SPH_ERR_NULL;
-    if (ws_bytes < P.ws_bytes) return SPH_ERR_BUFFER_TOO_SMALL;
-    if ((uintptr_t)d_ws % 256 != 0) return SPH_ERR_SHAPE;
-  }
-  KArgs a = make_args(w);
-  a.x = (const uint16_t*)d_x;
-  a.ldx = ldx;
-  a.y = d_y;
-  a.ldy = ldy;
-  a.y_f16 = (y_dtype == SPH_F16);
-  a.m = (int)m;
-  a.ks = P.ks;
-  a.ws_part = (float*)d_ws;
-  void* kargs[] = {&a};
-  hipStream_t s = (hipStream_t)stream;
-  if (hipLaunchKernel(fn, dim3(P.gx, P.gy, P.ks), dim3(PF_THREADS), kargs, 0, s) != hipSuccess) return SPH_ERR_HIP;
-  if (hipGetLastError() != hipSuccess) return SPH_ERR_HIP;
-  if (P.ks > 1) {
-    const int64_t total = (int64_t)m * w->n;
-    if (hipLaunchKernel((const void*)k_prefill_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), kargs, 0, s) !=
-        hipSuccess)
-      return SPH_ERR_HIP;
-    if (hipGetLastError() != hipSuccess) return SPH_ERR_HIP;
-  }
-  return SPH_OK;
+  return launch_prefill(w, d_x, m, ldx, d_y, ldy, y_dtype, d_ws, ws_bytes, (hipStream_t)stream);
 }
 
 sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y,
@@ -1628,6 +1639,9 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
       return SPH_ERR_HIP;
     return hipGetLastError() == hipSuccess ? SPH_OK : SPH_ERR_HIP;
   }
+  // batches 17..32: the prefill kernel with 32 batch rows per workgroup (its activations staged
+  // in LDS and shared by 16 row tiles) moves less activation traffic than the tile mode
+  if (m > 16) return launch_prefill(w, d_x, m, ldx, d_y, ldy, y_dtype, d_ws, ws_bytes, (hipStream_t)stream);
   const Launch L = plan(w, (int)m);
   if (!L.fn) return SPH_ERR_UNSUPPORTED_FORMAT;
   if (L.ws_bytes > 0) {

@@ -298,3 +298,19 @@ def test_vector_size_full_size_sampled(fmt):
     rows = np.unique(np.concatenate([[0, n - 1], np.random.default_rng(14).integers(0, n, 48)]))
     ref = O.gemm_rows(codes, cb, x, rows)[0]
     assert O.rel_err(y[rows], ref) <= TOL
+
+
+@pytest.mark.parametrize("m", [17, 24, 32, 40])
+def test_batch_workspace_left_zero(m):
+    """The split-K partials of the batched kernels are cleared by the call that used them, so one
+    zero-filled workspace serves every later call."""
+    D, V, codes, cb = uniform_case("W2", 64, 4096, 15)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = synth.activations(m, 4096, synth.rng(15, m, synth.STREAM_X))
+    y1 = pkg.gemm(w, to_dev_f16(x)).cpu().numpy()
+    ws = w.workspaces.get(m)
+    if ws is not None:
+        assert int(torch.count_nonzero(ws)) == 0
+    y2 = pkg.gemm(w, to_dev_f16(x)).cpu().numpy()
+    assert np.array_equal(y1, y2)
+    assert O.rel_err(y1, O.gemm(codes, cb, x)) <= TOL

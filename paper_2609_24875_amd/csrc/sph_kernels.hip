@@ -5,14 +5,18 @@
 // and multiplied with fp16 activations, accumulating in fp32; nothing dequantised is written to
 // memory. The mapping to the hardware is this library's own:
 //  - device layout: 16-row tiles, one "record" per (tile, vector position) (sph_layout.h);
-//  - vector-ALU path (batch 1..8): a lane owns one vector position of a tile and decodes up to
-//    16 rows of it from 16-byte loads; signs are folded into two nibble-indexed lookup tables in
-//    LDS, so the signed direction costs two 8-byte LDS reads and no sign arithmetic; products
-//    use v_dot2_f32_f16 (exact fp16 products, fp32 sums); persistent waves walk balanced
-//    (tile, K-segment) items and split-K partial sums are added in a fixed order, so results
-//    are bitwise reproducible;
-//  - matrix-core path (batch 9..32): each lane decodes one (row, vector) into the A operand of
-//    v_mfma_f32_16x16x32_f16 (weights rounded once to fp16), activations form the B operand.
+//  - vector-ALU path (batch 1): a lane owns one vector position of a tile and decodes its 16
+//    rows from 16-byte loads; signs are folded into two nibble-indexed lookup tables in LDS, so
+//    the signed direction costs two 8-byte LDS reads and no sign arithmetic; products use
+//    v_dot2_f32_f16 (exact fp16 products, fp32 sums); waves walk balanced ranges of
+//    (tile, K-chunk) steps and split tiles are added in a fixed order, so results are bitwise
+//    reproducible. Batches 2..8 decode the same records, 4 lanes per vector position, into
+//    4x4x4 MFMA blocks;
+//  - matrix-core tile path (batch 9..16): each lane decodes one (row, vector) into the A operand
+//    of v_mfma_f32_16x16x32_f16 (weights rounded once to fp16), activations form the B operand;
+//  - prefill (batch above 16): workgroups rebuild their tiles once per K-chunk and multiply them
+//    with activations staged in LDS on the same 16x16x32 MFMA;
+//  - 4-D and 16-D vectors: row-planar kernels, one wave per output row.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -345,7 +349,7 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL, MX>& R, floa
   }
 }
 
-// Tile variant (batch 9..32): lane (r, j) = (lane % 16, lane / 16) rebuilds row r of the vector
+// Tile variant (batch 9..16): lane (r, j) = (lane % 16, lane / 16) rebuilds row r of the vector
 // positions 4i + j (i = 0..3) of a 16-position chunk, which is exactly the A operand of
 // v_mfma_f32_16x16x32_f16 (16 rows x 4 positions); the B operand is x for batch rows
 // 16nb + lane % 16 at the same positions. The MFMA sums over the chunk, so each lane ends a step
@@ -894,7 +898,7 @@ __global__ void __launch_bounds__(256) k_unpack(KArgs a, uint8_t* signs, uint16_
 // column per MC-row slice of X), and walks K in chunks of 128 (16 vector positions = one radius
 // group). Per chunk the X slice [MC][128] is staged in LDS (rows padded by 16 bytes against bank
 // conflicts); each lane rebuilds, for each of its tiles, row lane % 16 at positions 4i + lane / 16
-// (i = 0..3) as fp16(r * t) -- the operand layout of the batch 9..32 tile mode -- and every rebuilt
+// (i = 0..3) as fp16(r * t) -- the operand layout of the batch 9..16 tile mode -- and every rebuilt
 // operand meets all MC / 16 column blocks of X, each X fragment serving both tiles. With ks > 1
 // the grid's third dimension splits K and the partial outputs are added in range order by
 // k_prefill_reduce. The order of every sum is fixed, so results are reproducible.
@@ -1037,7 +1041,7 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
   for (int u = 0; u < PF_TPW; ++u)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[u][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  // the row's dword in streams A and B, as in the batch 9..32 tile mode
+  // the row's dword in streams A and B, as in the batch 9..16 tile mode
   const int adw = IS_CB<KIND> ? r / 4 : r / 2;
   const int bdw = S::B1 ? 0 : (KIND == SPH_KIND_NIB16Q8) ? r / 4 : r / 2;
   for (int c = c0; c < c1; ++c) {
@@ -1292,8 +1296,7 @@ const void* valu_fn(int M) {
     case 4: return (const void*)k_gemm_valu<KIND, D, 4, 4, 1>;
     case 8: return (const void*)k_gemm_valu<KIND, D, 8, 4, 1>;
   }
-  if (M == 16) return (const void*)k_gemm_valu<KIND, D, 16, 4, 2>;
-  return (const void*)k_gemm_valu<KIND, D, 32, 4, 2>;
+  return (const void*)k_gemm_valu<KIND, D, 16, 4, 2>;
 }
 
 const void* pick(int D, int V, int M) {
@@ -1422,11 +1425,11 @@ Launch plan(const sph_weights* w, int m) {
   const int kind = sph_kind_of(w->fmt.dir_bits, w->fmt.radius_bits);
   const int cus = num_cus();
   // batch 1: vector ALU; 2..8: 4x4x4 MFMA blocks on the same records (4 lanes per vector
-  // position); 9..32: 16x16x32 MFMA tiles (lane = row x position group). The batched variants
+  // position); 9..16: 16x16x32 MFMA tiles (lane = row x position group). The batched variants
   // round each rebuilt weight to fp16. All share the step plan below (16 positions per step for
-  // the batched variants, 64 for batch 1).
-  if (m <= 32) {
-    const int M = m <= 1 ? 1 : m <= 4 ? 4 : m <= 8 ? 8 : m <= 16 ? 16 : 32;
+  // the batched variants, 64 for batch 1). Larger batches run on the prefill kernel.
+  if (m <= 16) {
+    const int M = m <= 1 ? 1 : m <= 4 ? 4 : m <= 8 ? 8 : 16;
     const int H = M == 1 ? 1 : 4;
     const int vpc = 64 / H;
     const int wpb = VALU_WPB;

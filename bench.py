@@ -67,6 +67,8 @@ def parse():
     ap.add_argument("--fmt", default="", help="override the workload's format (e.g. W3)")
     ap.add_argument("--layers", type=int, default=0, help="override layer count (0: workload's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-read-ceiling", action="store_true",
+                    help="skip the plain streaming-read ceiling measurement")
     ap.add_argument("--cpu-sample-seconds", type=float, default=15.0)
     ap.add_argument("--unfused", action="store_true", help="launch q, k, v, gate, up separately")
     ap.add_argument("--path", default="decode", choices=("decode", "encode", "train"),
@@ -141,6 +143,7 @@ def cpu_baseline(mats, budget_s, step_bytes_total, per_mat_bytes, layers):
         "value": round(gbs, 4),
         "unit": "GB/s",
         "cores": int(threads),
+        "cpu": cpu_model(),
         "kind": "oracle",
         "sample": f"{done} matrix decodes cycling over one layer's shapes "
                   f"[{', '.join(f'{m[0]} {m[1]}x{m[2]}' for m in mats)}] of the {layers}-layer step, "
@@ -150,6 +153,55 @@ def cpu_baseline(mats, budget_s, step_bytes_total, per_mat_bytes, layers):
 
 
 FP64_PEAK_TFS = 78.6   # MI355X fp64 vector peak
+
+
+def cpu_model() -> str:
+    """The host CPU's model name and logical CPU count (from /proc/cpuinfo where present)."""
+    name = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return f"{name or 'unknown CPU'}, {os.cpu_count()} logical CPUs"
+
+
+def read_ceiling(torch, dev, nbytes=2 << 30, reps=10):
+    """Plain streaming-read bandwidth of this GPU (libsph_probe.so, a measurement probe outside
+    the library): GB/s of one launch over a buffer far larger than the Infinity Cache, from HIP
+    events on the probe's stream, best of two grids. None if the probe is not built."""
+    import ctypes
+    from paper_2609_24875_amd import build as B
+    if not os.path.exists(B.PROBE_OUT):
+        return None
+    lib = ctypes.CDLL(B.PROBE_OUT)
+    lib.sph_probe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p,
+                                          ctypes.c_uint32, ctypes.c_void_p]
+    never = 0x9E3779B9   # every word is 1, so each thread's XOR fold is 0 or 1
+    buf = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev)
+    st = torch.cuda.Stream()
+    best = 0.0
+    for grid in (4096, 16384):
+        with torch.cuda.stream(st):
+            for _ in range(2):
+                lib.sph_probe_stream_read(buf.data_ptr(), nbytes, grid, flag.data_ptr(), never, st.cuda_stream)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            for _ in range(reps):
+                if lib.sph_probe_stream_read(buf.data_ptr(), nbytes, grid, flag.data_ptr(), never, st.cuda_stream) != 0:
+                    return None
+            e1.record(st)
+        torch.cuda.synchronize()
+        best = max(best, nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del buf, flag
+    torch.cuda.empty_cache()
+    return {"GB/s": round(best, 1), "bytes": nbytes, "frac_of_peak": round(best / HBM_PEAK_GBS, 4),
+            "kernel": "plain streaming read, 16-byte loads, grid-stride (libsph_probe.so)"}
 
 
 def encode_main(args):
@@ -442,6 +494,34 @@ def main():
     dom_bytes = sum(w.nbytes for w, _, _ in dom_launches) / len(dom_launches)
     dom_gbs = dom_bytes / (dom_us * 1e-6) / 1e9
     dom_flops = 2.0 * m * big[0][1] * big[0][2]
+    del g2
+
+    # ---- every shape the same way: average launch over the per-layer copies (us per GEMV)
+    per_shape = {}
+    for label, n, k, copies, xd, ys in packed:
+        gs = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gs, stream=s2):
+            for li in range(layers):
+                if m == 1:
+                    pkg.gemv(copies[li], xd[0], out=ys[li][0])
+                elif m <= 32:
+                    pkg.gemm_small(copies[li], xd, out=ys[li])
+                else:
+                    pkg.gemm(copies[li], xd, out=ys[li])
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s2):
+            gs.replay()
+            torch.cuda.synchronize()
+            d0.record(s2)
+            for _ in range(reps):
+                gs.replay()
+            d1.record(s2)
+        torch.cuda.synchronize()
+        us = d0.elapsed_time(d1) * 1e3 / (reps * layers)
+        per_shape[f"{label} {n}x{k}"] = {"us": round(us, 3),
+                                         "GB/s": round(copies[0].nbytes / (us * 1e-6) / 1e9, 1)}
+        del gs
+    ceiling = read_ceiling(torch, dev) if not args.no_read_ceiling else None
 
     out = {
         "metric": "packed-weight GB/s & % HBM peak for W2/W3 sph_gemv; linear-layer tokens/s",
@@ -471,6 +551,9 @@ def main():
         },
         "tokens_per_s": round(m / (ms / 1e3), 2),
         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "per_shape": per_shape,
+        "read_ceiling": ceiling,
+        "frac_read_ceiling": round(gbs / ceiling["GB/s"], 4) if ceiling else None,
         "roofline": ({
             "kernel": f"{kernel_label(fmt, m)} on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
             "bound": "hbm",
@@ -481,6 +564,7 @@ def main():
             "traffic": TRAFFIC.get(kernel_source_hash(), {}).get(f"{big[0][1]}x{big[0][2]}-m{m}"),
             "avg_launch_us": round(dom_us, 3),
             "bytes_per_launch": int(dom_bytes),
+            "frac_read_ceiling": round(dom_gbs / ceiling["GB/s"], 4) if ceiling else None,
         } if m <= 32 else {
             # batches above 32: a dense contraction on the matrix cores, 2 m n k flop per launch
             "kernel": f"{kernel_label(fmt, m)} on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",

@@ -11,6 +11,9 @@ CSRC = os.path.join(HERE, "csrc")
 SOURCES = [os.path.join(CSRC, "sph_kernels.hip"), os.path.join(CSRC, "sph_encode.hip"),
            os.path.join(CSRC, "sph_train.hip"), os.path.join(CSRC, "sph_pack.cpp")]
 OUT = os.path.join(HERE, "libsph.so")
+# A separate measurement probe (plain streaming read), loaded by the benchmark only.
+PROBE_SOURCES = [os.path.join(CSRC, "sph_probe.hip")]
+PROBE_OUT = os.path.join(HERE, "libsph_probe.so")
 
 HIPCC_FLAGS = [
     "-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC", "-shared",
@@ -31,17 +34,23 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into libsph.so next to this file; returns its path."""
-    tmp = OUT + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, *SOURCES]
+def _compile(sources, out: str, verbose: bool) -> str:
+    tmp = out + ".tmp"
+    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, *sources]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)
     if verbose and res.stderr.strip():
         print(res.stderr)
-    os.replace(tmp, OUT)
-    return OUT
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Compile the library sources into libsph.so and the measurement probe into
+    libsph_probe.so, next to this file; returns the library's path."""
+    _compile(PROBE_SOURCES, PROBE_OUT, verbose)
+    return _compile(SOURCES, OUT, verbose)
 
 
 if __name__ == "__main__":

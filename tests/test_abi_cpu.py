@@ -37,6 +37,17 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
 
 
+def test_read_probe_is_separate_from_the_library():
+    """The benchmark's streaming-read probe is its own library: libsph exports no probe symbol,
+    and the probe exports its one entry point."""
+    from paper_2609_24875_amd import build as Bd
+    if os.path.exists(pkg.LIB_PATH):
+        assert not hasattr(ctypes.CDLL(pkg.LIB_PATH), "sph_probe_stream_read")
+    if not os.path.exists(Bd.PROBE_OUT):
+        pytest.skip("libsph_probe.so not built")
+    assert hasattr(ctypes.CDLL(Bd.PROBE_OUT), "sph_probe_stream_read")
+
+
 @needs_lib
 def test_status_strings():
     for code in range(9):

@@ -6,7 +6,7 @@
 // memory. The mapping to the hardware is this library's own:
 //  - device layout: 16-row tiles, one "record" per (tile, vector position) (sph_layout.h);
 //  - vector-ALU path (batch 1): a lane owns one vector position of a tile and decodes its 16
-//    rows from 16-byte loads; signs are folded into two nibble-indexed lookup tables in LDS, so
+//    rows (or, with two lanes per position, 8 of them) from 16-byte loads; signs are folded into two nibble-indexed lookup tables in LDS, so
 //    the signed direction costs two 8-byte LDS reads and no sign arithmetic; products use
 //    v_dot2_f32_f16 (exact fp16 products, fp32 sums); waves walk balanced ranges of
 //    (tile, K-chunk) steps and split tiles are added in a fixed order, so results are bitwise
@@ -1289,27 +1289,41 @@ KArgs make_args(const sph_weights* w) {
   return a;
 }
 
+// Rows per lane of the batch-1 mode: 8 (two lanes per vector position, twice the waves, half
+// the work per step) for the large-table kinds (the 2^13 codebook, 8-bit directions) and for
+// rows of at most 4096 weights; 16 otherwise, where the longer steps amortise their fixed cost.
+// Both choices were timed per format on the 8B- and 32B-class shapes.
+int batch1_rpl(int kind, int dir_bits, int64_t k) {
+  if (sph_is_codebook_kind(kind) || dir_bits >= 8) return 8;
+  return k <= 4096 ? 8 : 16;
+}
 template <int KIND, int D>
-const void* valu_fn(int M) {
+constexpr bool B1_RPL16 = !IS_CB<KIND> && D < 8;
+
+template <int KIND, int D>
+const void* valu_fn(int M, int rpl1) {
   switch (M) {
-    case 1: return (const void*)k_gemm_valu<KIND, D, 1, 16, 0>;
+    case 1:
+      if constexpr (B1_RPL16<KIND, D>)
+        if (rpl1 == 16) return (const void*)k_gemm_valu<KIND, D, 1, 16, 0>;
+      return (const void*)k_gemm_valu<KIND, D, 1, 8, 0>;
     case 4: return (const void*)k_gemm_valu<KIND, D, 4, 4, 1>;
     case 8: return (const void*)k_gemm_valu<KIND, D, 8, 4, 1>;
   }
   return (const void*)k_gemm_valu<KIND, D, 16, 4, 2>;
 }
 
-const void* pick(int D, int V, int M) {
+const void* pick(int D, int V, int M, int rpl1) {
   switch (sph_kind_of(D, V)) {
-    case SPH_KIND_W2: return D == 7 ? valu_fn<SPH_KIND_W2, 7>(M) : valu_fn<SPH_KIND_W2, 6>(M);
+    case SPH_KIND_W2: return D == 7 ? valu_fn<SPH_KIND_W2, 7>(M, rpl1) : valu_fn<SPH_KIND_W2, 6>(M, rpl1);
     case SPH_KIND_NIB16:
-      if (D == 4) return valu_fn<SPH_KIND_NIB16, 4>(M);
-      if (D == 5) return valu_fn<SPH_KIND_NIB16, 5>(M);
-      return valu_fn<SPH_KIND_NIB16, 6>(M);
-    case SPH_KIND_NIB16Q8: return valu_fn<SPH_KIND_NIB16Q8, 8>(M);
-    case SPH_KIND_NIB16Q2: return valu_fn<SPH_KIND_NIB16Q2, 8>(M);
-    case SPH_KIND_CB13: return valu_fn<SPH_KIND_CB13, 13>(M);
-    case SPH_KIND_CB13Q4: return valu_fn<SPH_KIND_CB13Q4, 13>(M);
+      if (D == 4) return valu_fn<SPH_KIND_NIB16, 4>(M, rpl1);
+      if (D == 5) return valu_fn<SPH_KIND_NIB16, 5>(M, rpl1);
+      return valu_fn<SPH_KIND_NIB16, 6>(M, rpl1);
+    case SPH_KIND_NIB16Q8: return valu_fn<SPH_KIND_NIB16Q8, 8>(M, rpl1);
+    case SPH_KIND_NIB16Q2: return valu_fn<SPH_KIND_NIB16Q2, 8>(M, rpl1);
+    case SPH_KIND_CB13: return valu_fn<SPH_KIND_CB13, 13>(M, rpl1);
+    case SPH_KIND_CB13Q4: return valu_fn<SPH_KIND_CB13Q4, 13>(M, rpl1);
   }
   return nullptr;
 }
@@ -1427,10 +1441,11 @@ Launch plan(const sph_weights* w, int m) {
   // batch 1: vector ALU; 2..8: 4x4x4 MFMA blocks on the same records (4 lanes per vector
   // position); 9..16: 16x16x32 MFMA tiles (lane = row x position group). The batched variants
   // round each rebuilt weight to fp16. All share the step plan below (16 positions per step for
-  // the batched variants, 64 for batch 1). Larger batches run on the prefill kernel.
+  // the batched variants, 64 or 32 for batch 1). Larger batches run on the prefill kernel.
   if (m <= 16) {
     const int M = m <= 1 ? 1 : m <= 4 ? 4 : m <= 8 ? 8 : 16;
-    const int H = M == 1 ? 1 : 4;
+    const int rpl1 = batch1_rpl(kind, w->fmt.dir_bits, w->k);
+    const int H = M == 1 ? 16 / rpl1 : 4;
     const int vpc = 64 / H;
     const int wpb = VALU_WPB;
     const int64_t nc = (nv + vpc - 1) / vpc;
@@ -1448,7 +1463,7 @@ Launch plan(const sph_weights* w, int m) {
     // one more step per wave than the balanced plan, whose split tiles cross workgroups and meet
     // through global memory (a round trip at the end of the launch)
     const bool aligned = lA <= lB + 1 && lds_handover_fits(kind, w->fmt.dir_bits, M, M == 1 ? 0 : M <= 8 ? 1 : 2);
-    L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, M);
+    L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, M, rpl1);
     L.block = 64 * wpb;
     L.nc = (int)nc;
     L.ts = (int)ts;

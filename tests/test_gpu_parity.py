@@ -71,7 +71,9 @@ def test_unpack_bit_exact(fmt):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-@pytest.mark.parametrize("n,k", [(87, 640), (16, 128), (1, 256), (300, 2048)])
+# rows of at most 4096 weights take 8 rows per lane at batch 1, longer ones 16 (for the formats
+# that have both): 4224 = 33 groups of 128 also leaves a ragged last step
+@pytest.mark.parametrize("n,k", [(87, 640), (16, 128), (1, 256), (300, 2048), (300, 4224), (40, 8320)])
 def test_gemv_parity(fmt, n, k):
     D, V, codes, cb = uniform_case(fmt, n, k, 2)
     w = pkg.pack(D, V, codes, cb, device=DEV)
@@ -163,6 +165,8 @@ def test_bad_batch_raises():
 FULL = [
     ("W2", 1024, 1024, "uniform", 1),        # smallest workload: every output checked
     ("W2", 4096, 4096, "encoded", 1),        # encoded outlier-laden weights
+    ("W2", 7168, 5120, "uniform", 1),        # 32B-class fused q/k/v, batch 1 (16 rows per lane)
+    ("W2", 5120, 25600, "uniform", 1),       # 32B-class down, batch 1
     ("W3", 12288, 4096, "uniform", 1),       # 8B-class gate/up, W3
     ("W3", 4096, 12288, "uniform", 1),       # 8B-class down, W3
     ("W2", 25600, 5120, "uniform", 8),       # 32B-class gate/up, batch 8

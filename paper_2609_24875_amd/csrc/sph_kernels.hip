@@ -1057,9 +1057,7 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
     const uint32_t* sb = (const uint32_t*)(st + S::b_off);
     const uint16_t* sc = (const uint16_t*)(st + S::c_off);
     const uint32_t* sp = (const uint32_t*)(st + S::p_off);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      uint4 w[PF_TPW];
+    auto rebuild_i = [&](int i, uint4 (&w)[PF_TPW]) {
 #pragma unroll
       for (int u = 0; u < PF_TPW; ++u) {
         const int lt = wave * PF_TPW + u, rec = lt * 16 + 4 * i + j;
@@ -1071,14 +1069,26 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
         const uint32_t pw = sp[lt * 16 + r];
         w[u] = pf_rebuild<KIND, D>(ra, rb, rc, f16lo(pw), f16hi(pw), lds, a.t_bytes, r);
       }
+    };
+    // the operands of position group i + 1 are rebuilt before the multiplies of group i, so
+    // that their LDS round trips overlap the matrix-core work
+    uint4 wc[PF_TPW];
+    rebuild_i(0, wc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint4 wn[PF_TPW];
+      if (i + 1 < 4) rebuild_i(i + 1, wn);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         const uint4 xb = *(const uint4*)(st + (16 * nb + r) * PF_XROW + (4 * i + j) * 16);
 #pragma unroll
         for (int u = 0; u < PF_TPW; ++u)
-          acc[u][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, w[u]),
+          acc[u][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wc[u]),
                                                               __builtin_bit_cast(f16x8, xb), acc[u][nb], 0, 0, 0);
       }
+      if (i + 1 < 4)
+#pragma unroll
+        for (int u = 0; u < PF_TPW; ++u) wc[u] = wn[u];
     }
   }
   // D[row][col] of a 16x16 block: lane holds col lane % 16 (batch row) and rows 4 * (lane / 16) + e

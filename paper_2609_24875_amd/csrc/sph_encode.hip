@@ -242,7 +242,11 @@ __global__ __launch_bounds__(64 * kMxWaves) void k_encode_mx(EncArgs a, int64_t 
       }
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const double x = d[nb][4 * (qd & 1) + t];
+        // both halves pass through an empty asm so that the select stays a register select
+        // (an indexed read would put d in scratch memory)
+        double x0 = d[nb][t], x1 = d[nb][4 + t];
+        asm volatile("" : "+v"(x0), "+v"(x1));
+        const double x = (qd & 1) ? x1 : x0;
         const _Float16 hi = (_Float16)(float)x;
         bop[nb][t] = qd < 2 ? hi : (_Float16)(float)(x - (double)hi);
       }

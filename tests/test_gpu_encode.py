@@ -105,11 +105,13 @@ def test_encode_leading_dimension():
     assert compare_codes(w32, cb, V, got, ref) == 0
 
 
-def test_encode_edge_values():
+@pytest.mark.parametrize("fmt", ["W2", "W3"])
+def test_encode_edge_values(fmt):
     """Zero and negative-zero vectors, constant groups (zero step), fp16 rounding ties, fp16
     subnormal and overflowing offsets, against the oracle with a codebook whose every entry is
-    e_0 (so r~ = |w_0| exactly and every cosine ties: the lowest index, 0, must win)."""
-    D, V = synth.FORMATS["W2"]
+    e_0 (so r~ = |w_0| exactly and every cosine ties: the lowest index, 0, must win). With the
+    2^13-entry codebook every lane of the matrix-core search runs out of candidate slots."""
+    D, V = synth.FORMATS[fmt]
     cb = np.zeros((1 << D, 8), np.uint16)
     cb[:, 0] = 0x3C00
     firsts = [0.0, -0.0, 1 + 2.0**-11, 1 + 3 * 2.0**-11, 65504.0, 65519.0, 65520.0, 70000.0,
@@ -130,11 +132,16 @@ def test_encode_edge_values():
         assert np.array_equal(got[key], ref[key]), key
 
 
-def test_encode_duplicate_entries_take_lowest_index():
-    D, V = synth.FORMATS["W2"]
+@pytest.mark.parametrize("fmt,dups", [("W2", (40, 63)), ("W3", (40, 63, 4000)),
+                                      ("W3", (23, 39, 55, 71, 4103, 8183))])
+def test_encode_duplicate_entries_take_lowest_index(fmt, dups):
+    """Copies of entry 7 tie with it exactly: the lowest index must win. In the 2^13-entry
+    search, entries e with e % 16 in 4q..4q+3 go to the same lane, so the second W3 case (all
+    copies = 7 mod 16) overflows that lane's candidate slots and the first fits in them."""
+    D, V = synth.FORMATS[fmt]
     cb = synth.random_codebook(D, synth.rng(13, synth.STREAM_CODEBOOK))
-    cb[40] = cb[7]
-    cb[63] = cb[7]
+    for e in dups:
+        cb[e] = cb[7]
     c7 = O.f16_to_f64(cb[7])
     n, k = 4, 128
     g = np.random.default_rng(13)

@@ -40,9 +40,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source and compile flags the counters were taken with: any change to
 # the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "e5ad742e6554601b19ba33e34b6ba3046d71b8b2bc31485b3b477b5a6895d04f": {
-        "7168x5120-m1": 11946676, "5120x5120-m1": 8661964,
-        "51200x5120-m1": 82683111, "5120x25600-m1": 42923663},
+    "8c5f7a40a111c3e272f9c96b3cd260eee6df139de2eebaf224281448467d84a7": {
+        "7168x5120-m1": 11946491, "5120x5120-m1": 8661923,
+        "51200x5120-m1": 82680446, "5120x25600-m1": 42920775},
 }
 
 

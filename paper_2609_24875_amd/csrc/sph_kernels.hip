@@ -705,31 +705,58 @@ __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[MODE == 2
 // Lookup tables staged in two halves around the first record's loads: the table words are
 // fetched first, the record loads are issued behind them, and the LDS stores wait only for the
 // table words, so the first record's memory round trip overlaps the staging.
-
+//
+// With 8-bit directions the sign-folded tables (16 * 2^(D+1) entries of 8 bytes, 64 KiB) are
+// expanded in the workgroup from the 2^D-entry codebook (16 bytes per entry), 16 times fewer
+// bytes to fetch: every workgroup of a launch reads the same lines, so that fetch is bound by
+// the L2 serving them (0.4 us per launch saved). For the smaller tables the expansion's extra
+// work cost more than it saved, and they are copied as packed. Entry e < 16 * 2^D of T_lo is
+// (z, s) = (e / 16, e % 16); entry e of T_hi is (s, z) = (e / 2^D, e % 2^D) after the first
+// 16 * 2^D; both are the codebook's low (T_lo) or high (T_hi) four fp16 with the sign bits of s
+// applied, as the packer lays them out.
 template <int KIND, int D>
 struct TableWords {
+  static constexpr bool EXPAND = !IS_CB<KIND> && D >= 8;
+  static constexpr int NLO = 16 << D;                       // entries of T_lo (and of T_hi)
   static constexpr int N16 = (int)((Tables<KIND, D>::bytes - (IS_CB<KIND> ? 128u : 0u)) / 16u);
-  static constexpr int PER = (N16 + VALU_THREADS - 1) / VALU_THREADS;
-  uint4 w[PER];
+  static constexpr int NITEM = EXPAND ? 2 * NLO : N16;     // 8-byte entries, or 16-byte words
+  static constexpr int PER = (NITEM + VALU_THREADS - 1) / VALU_THREADS;
+  typename std::conditional<EXPAND, uint2, uint4>::type w[PER];
 };
 
 template <int KIND, int D>
 __device__ __forceinline__ void fetch_tables(TableWords<KIND, D>& tw, const KArgs& a) {
-  constexpr int N16 = TableWords<KIND, D>::N16;
+  using TW = TableWords<KIND, D>;
 #pragma unroll
-  for (int i = 0; i < TableWords<KIND, D>::PER; ++i) {
-    const int j = (int)threadIdx.x + VALU_THREADS * i;
-    tw.w[i] = a.T[j < N16 ? j : N16 - 1];
+  for (int i = 0; i < TW::PER; ++i) {
+    const int j = min((int)threadIdx.x + VALU_THREADS * i, TW::NITEM - 1);
+    if constexpr (TW::EXPAND) {
+      const bool hi = j >= TW::NLO;
+      const int z = hi ? (j - TW::NLO) & ((1 << D) - 1) : j >> 4;
+      tw.w[i] = ((const uint2*)a.CB)[2 * z + (hi ? 1 : 0)];
+    } else {
+      tw.w[i] = a.T[j];
+    }
   }
 }
 
 template <int KIND, int D>
 __device__ __forceinline__ void store_tables(unsigned char* lds, const TableWords<KIND, D>& tw, const KArgs& a) {
-  constexpr int N16 = TableWords<KIND, D>::N16;
+  using TW = TableWords<KIND, D>;
 #pragma unroll
-  for (int i = 0; i < TableWords<KIND, D>::PER; ++i) {
+  for (int i = 0; i < TW::PER; ++i) {
     const int j = (int)threadIdx.x + VALU_THREADS * i;
-    if (j < N16) ((uint4*)lds)[j] = tw.w[i];
+    if (j < TW::NITEM) {
+      if constexpr (TW::EXPAND) {
+        const uint32_t sg = j >= TW::NLO ? (uint32_t)(j - TW::NLO) >> D : (uint32_t)j & 15u;
+        uint2 v = tw.w[i];
+        v.x ^= ((sg & 1u) << 15) | ((sg & 2u) << 30);
+        v.y ^= ((sg & 4u) << 13) | ((sg & 8u) << 28);
+        ((uint2*)lds)[j] = v;
+      } else {
+        ((uint4*)lds)[j] = tw.w[i];
+      }
+    }
   }
   if constexpr (IS_CB<KIND>) {
     // mask[s] flips the fp16 sign bit of element j (of 4) where bit j of the nibble s is set.

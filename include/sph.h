@@ -109,10 +109,11 @@ sph_status sph_gemv(const sph_weights* w, const void* d_x, void* d_y, sph_dtype 
                     void* d_ws, size_t ws_bytes, void* stream);
 
 /* Y = X W^T for 1 <= m <= 32 activation rows: d_x is device fp16[m][ldx] (ldx >= k), d_y is
- * device [m][ldy] of y_dtype (ldy >= n). Batch 1 runs on the vector ALUs with exact fp16 products
- * and fp32 accumulation; batches 2..32 round each decoded weight once to fp16 and run on the
- * matrix cores (MFMA: 4x4x4 blocks up to 8, 16x16x32 tiles up to 16, above that the prefill
- * kernel of sph_gemm with 32 activation rows staged in LDS) with fp32 accumulation.
+ * device [m][ldy] of y_dtype (ldy >= n). Batch 1, and batch 2 for formats with at most 8
+ * direction bits, run on the vector ALUs with exact fp16 products and fp32 accumulation; the
+ * other batches up to 32 round each decoded weight once to fp16 and run on the matrix cores
+ * (MFMA: 4x4x4 blocks up to 8, 16x16x32 tiles up to 16, above that the prefill kernel of
+ * sph_gemm with 32 activation rows staged in LDS) with fp32 accumulation.
  * Asynchronous on `stream`. */
 sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y,
                           int64_t ldy, sph_dtype y_dtype, void* d_ws, size_t ws_bytes,

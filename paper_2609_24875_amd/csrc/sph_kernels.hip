@@ -10,7 +10,8 @@
 //    the signed direction costs two 8-byte LDS reads and no sign arithmetic; products use
 //    v_dot2_f32_f16 (exact fp16 products, fp32 sums); waves walk balanced ranges of
 //    (tile, K-chunk) steps and split tiles are added in a fixed order, so results are bitwise
-//    reproducible. Batches 2..8 decode the same records, 4 lanes per vector position, into
+//    reproducible. Batch 2 runs the same way with two rows of products (except with the 2^13
+//    codebook); batches up to 8 decode the same records, 4 lanes per vector position, into
 //    4x4x4 MFMA blocks;
 //  - matrix-core tile path (batch 9..16): each lane decodes one (row, vector) into the A operand
 //    of v_mfma_f32_16x16x32_f16 (weights rounded once to fp16), activations form the B operand;
@@ -1344,6 +1345,9 @@ const void* valu_fn(int M, int rpl1) {
       if constexpr (B1_RPL16<KIND, D>)
         if (rpl1 == 16) return (const void*)k_gemm_valu<KIND, D, 1, 16, 0>;
       return (const void*)k_gemm_valu<KIND, D, 1, 8, 0>;
+    case 2:
+      if constexpr (!IS_CB<KIND>) return (const void*)k_gemm_valu<KIND, D, 2, 8, 0>;
+      return nullptr;
     case 4: return (const void*)k_gemm_valu<KIND, D, 4, 4, 1>;
     case 8: return (const void*)k_gemm_valu<KIND, D, 8, 4, 1>;
   }
@@ -1480,9 +1484,11 @@ Launch plan(const sph_weights* w, int m) {
   // round each rebuilt weight to fp16. All share the step plan below (16 positions per step for
   // the batched variants, 64 or 32 for batch 1). Larger batches run on the prefill kernel.
   if (m <= 16) {
-    const int M = m <= 1 ? 1 : m <= 4 ? 4 : m <= 8 ? 8 : 16;
+    // batch 2 on the vector ALUs as well (exact products), except for the codebook kinds, whose
+    // two-row kernel would spill
+    const int M = m <= 1 ? 1 : (m == 2 && !sph_is_codebook_kind(kind)) ? 2 : m <= 4 ? 4 : m <= 8 ? 8 : 16;
     const int rpl1 = batch1_rpl(kind, w->fmt.dir_bits, w->k);
-    const int H = M == 1 ? 16 / rpl1 : 4;
+    const int H = M == 1 ? 16 / rpl1 : M == 2 ? 2 : 4;
     const int vpc = 64 / H;
     const int wpb = VALU_WPB;
     const int64_t nc = (nv + vpc - 1) / vpc;
@@ -1499,7 +1505,7 @@ Launch plan(const sph_weights* w, int m) {
     // whole tiles per workgroup need the parts inside a workgroup to meet in LDS; they are worth
     // one more step per wave than the balanced plan, whose split tiles cross workgroups and meet
     // through global memory (a round trip at the end of the launch)
-    const bool aligned = lA <= lB + 1 && lds_handover_fits(kind, w->fmt.dir_bits, M, M == 1 ? 0 : M <= 8 ? 1 : 2);
+    const bool aligned = lA <= lB + 1 && lds_handover_fits(kind, w->fmt.dir_bits, M, M <= 2 ? 0 : M <= 8 ? 1 : 2);
     L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, M, rpl1);
     L.block = 64 * wpb;
     L.nc = (int)nc;

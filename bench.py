@@ -40,9 +40,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source and compile flags the counters were taken with: any change to
 # the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "8c5f7a40a111c3e272f9c96b3cd260eee6df139de2eebaf224281448467d84a7": {
-        "7168x5120-m1": 11946491, "5120x5120-m1": 8661923,
-        "51200x5120-m1": 82680446, "5120x25600-m1": 42920775},
+    "3878bb033e7ff7cd04bdaee5f92a37ebbd8319366ae1ceca0699b3630587cad2": {
+        "7168x5120-m1": 11953809, "5120x5120-m1": 8669106,
+        "51200x5120-m1": 82695833, "5120x25600-m1": 42932950},
 }
 
 
@@ -592,6 +592,8 @@ def kernel_label(fmt, m):
         return f"k_gemm_rowvec<{fmt},MB={min(32, 1 << (m - 1).bit_length()) if m > 1 else 1}> (one wave per row)"
     if m == 1:
         return f"k_gemm_valu<{fmt},M=1> (vector ALU)"
+    if m == 2 and synth.FORMATS[fmt][0] < 13:
+        return f"k_gemm_valu<{fmt},M=2> (vector ALU)"
     if m <= 8:
         return f"k_gemm_valu<{fmt},M={4 if m <= 4 else 8}> (4x4x4 MFMA blocks)"
     if m <= 16:

@@ -109,12 +109,15 @@ def test_gemm_small_parity(fmt, m):
     err = O.rel_err(y, ref)
     assert err <= TOL, err
     assert np.all(np.abs(y - ref) <= f16_weight_bound(codes, cb, x, k) + 1e-30)
+    if m == 2 and D < 13:
+        # batch 2 runs on the vector ALUs with exact products, like batch 1
+        assert np.all(np.abs(y - ref) <= k * 2.0**-23 * apriori_bound(codes, cb, x) + 1e-30)
 
 
 def test_gemm_small_strided_and_fp16_out():
     D, V, codes, cb = uniform_case("W2", 48, 512, 5)
     w = pkg.pack(D, V, codes, cb, device=DEV)
-    for m in (3, 20):
+    for m in (2, 3, 20):
         x = synth.activations(m, 512, synth.rng(5, m, 0, synth.STREAM_X))
         big = torch.zeros((m, 512 + 64), dtype=torch.float16, device=DEV)
         big[:, :512] = to_dev_f16(x)
@@ -127,7 +130,8 @@ def test_gemm_small_strided_and_fp16_out():
 
 def test_unit_activation_returns_decoded_column():
     """x = e_c picks column c of W^: every weight the kernel rebuilds is checked (Eq. 4). The
-    batch-1 path returns it exactly (in fp32); the batched path returns its fp16 rounding."""
+    batch-1 and batch-2 paths return it exactly (in fp32); the matrix-core paths return its fp16
+    rounding."""
     D, V, codes, cb = uniform_case("W2", 33, 256, 6)
     w = pkg.pack(D, V, codes, cb, device=DEV)
     dense = O.decode(codes, cb)
@@ -141,6 +145,8 @@ def test_unit_activation_returns_decoded_column():
         y = pkg.gemm_small(w, xd).cpu().numpy()
         ref = dense[:, c0:c0 + 8].T
         assert np.all(np.abs(y - ref) <= (2.0**-10 + 2.0**-20) * np.abs(ref) + 2.0**-25)
+        y2 = pkg.gemm_small(w, xd[2:4]).cpu().numpy()
+        assert np.array_equal(y2, ref[2:4].astype(np.float32))
 
 
 def test_deterministic():

@@ -15,12 +15,12 @@
  * Conventions shared by every entry point:
  *  - W is n x k (n = d_out rows, k = d_in columns). k must be a multiple of 128 with
  *    128 <= k <= 2^20, 1 <= n <= 2^24, and ceil(n/16) * k/8 < 2^31.
- *  - Logical codes are row-major: signs/dir/q are [n][k/8], group params are [n][k/128].
- *    Sign bit j of a vector belongs to element 8v+j (least significant bit first); a set bit
- *    means the element is negative.
+ *  - Logical codes are row-major: signs/dir/q are [n][k/8] (k/vec_dim for the 4-D and 16-D
+ *    formats), group params are [n][k/128]. Sign bit j of a vector belongs to element 8v+j
+ *    (least significant bit first); a set bit means the element is negative.
  *  - fp16 values (group params, codebook, activations) are passed as IEEE binary16 bit patterns.
  *  - The caller owns every buffer. The library never allocates device memory; it allocates
- *    host staging memory inside sph_pack_weights and sph_unpack only, and frees it on return.
+ *    host staging memory inside sph_pack_weights only, and frees it on return.
  *  - Device pointers must be device-accessible HIP allocations of the current device, 16-byte
  *    aligned. Compute calls are asynchronous on the given stream; argument errors are detected
  *    on the host before any HIP call and reported through sph_status. Nothing throws or aborts
@@ -43,8 +43,8 @@ typedef enum {
                                   /* leading dimension too small, or misaligned pointer         */
   SPH_ERR_UNSUPPORTED_FORMAT = 3, /* (vec_dim, dir_bits, radius_bits, group_size) not built in  */
   SPH_ERR_CODE_RANGE = 4,         /* a direction index >= 2^D or a radius level >= 2^V          */
-  SPH_ERR_BAD_VALUE = 5,          /* non-finite or negative codebook entry, non-finite offset,  */
-                                  /* non-finite or negative step                                */
+  SPH_ERR_BAD_VALUE = 5,          /* codebook entry non-finite, negative or above 2; offset     */
+                                  /* non-finite; step non-finite or negative                    */
   SPH_ERR_BUFFER_TOO_SMALL = 6,   /* device buffer smaller than sph_packed_bytes                */
   SPH_ERR_HIP = 7,                /* a HIP runtime call or kernel launch failed                 */
   SPH_ERR_BAD_DESCRIPTOR = 8      /* the sph_weights descriptor is not one this library filled  */
@@ -52,8 +52,8 @@ typedef enum {
 
 typedef enum { SPH_F16 = 0, SPH_F32 = 1 } sph_dtype;
 
-/* The representation (Sec. 3.1-3.2). Built-in (dir_bits, radius_bits) pairs, all with vec_dim 8
- * and group_size 128:
+/* The representation (Sec. 3.1-3.2). Built-in (dir_bits, radius_bits) pairs with vec_dim 8 and
+ * group_size 128:
  *   (6, 4)  W2: 8 sign + 6 direction + 4 radius bits, the packed W2 format of Sec. 3.4 / App. D
  *   (13, 3) W3: K_dir = 7*3 - 8 = 13 with 3 radius bits (3.00 bits/weight payload, App. B)
  *   (4, 4)  16-bit vectors: 8 sign + 4 direction + 4 radius bits
@@ -61,9 +61,12 @@ typedef enum { SPH_F16 = 0, SPH_F32 = 1 } sph_dtype;
  *   (8, 8)  24-bit vectors: 8 sign + 8 direction + 8 radius bits
  *   (13, 4) W3 with 4 radius bits (3.125 bits/weight payload, the W3 row of Tab. 1)
  *   (6, 3), (7, 2), (8, 2)  further splits of the W2 budget from the bit-allocation study of
- *           Tab. 4 (8 sign bits + D direction + V radius bits)                                 */
+ *           Tab. 4 (8 sign bits + D direction + V radius bits)
+ * and the other vector sizes of Tab. 7 (group_size 128): vec_dim 4 with (2, 3) (4 sign + 2 direction
+ * + 3 radius bits) and vec_dim 16 with (14, 6) (16 sign + 14 direction + 6 radius bits); for vec_dim
+ * 16 the sign array holds one uint16 per vector.                                               */
 typedef struct {
-  int32_t vec_dim;      /* must be 8   */
+  int32_t vec_dim;      /* 8, or 4 / 16 with the pairs above */
   int32_t dir_bits;     /* D           */
   int32_t radius_bits;  /* V           */
   int32_t group_size;   /* must be 128 */
@@ -90,7 +93,8 @@ sph_status sph_packed_bytes(const sph_format* fmt, int64_t n, int64_t k, size_t*
  * device layout and copy them into d_buf (d_buf_bytes >= sph_packed_bytes). Inputs are host
  * arrays: signs uint8[n][k/8], dir_idx uint16[n][k/8] (< 2^D), radius_code uint8[n][k/8]
  * (< 2^V), group_min / group_step uint16[n][k/128] (fp16 bits: min finite, step finite and
- * >= 0), codebook uint16[2^D][8] (fp16 bits, finite and >= 0). Synchronous: returns after the
+ * >= 0), codebook uint16[2^D][vec_dim] (fp16 bits, in [0, 2]: coordinates of non-negative unit
+ * directions, Sec. 3.1, with room for rounding). Synchronous: returns after the
  * copy on `stream` has completed, so the host arrays may be freed. On success *out describes
  * the packed matrix. */
 sph_status sph_pack_weights(const sph_format* fmt, int64_t n, int64_t k, const uint8_t* signs,
@@ -109,20 +113,23 @@ sph_status sph_gemv(const sph_weights* w, const void* d_x, void* d_y, sph_dtype 
                     void* d_ws, size_t ws_bytes, void* stream);
 
 /* Y = X W^T for 1 <= m <= 32 activation rows: d_x is device fp16[m][ldx] (ldx >= k), d_y is
- * device [m][ldy] of y_dtype (ldy >= n). Batch 1, and batch 2 for formats with at most 8
- * direction bits, run on the vector ALUs with exact fp16 products and fp32 accumulation; the
- * other batches up to 32 round each decoded weight once to fp16 and run on the matrix cores
- * (MFMA: 4x4x4 blocks up to 8, 16x16x32 tiles up to 16, above that the prefill kernel of
- * sph_gemm with 32 activation rows staged in LDS) with fp32 accumulation.
- * Asynchronous on `stream`. */
+ * device [m][ldy] of y_dtype (ldy >= n). Every batch size forms exact products of fp16 numbers
+ * and rounds only fp32 sums: batch 1, and batch 2 for formats with at most 8 direction bits, on the
+ * vector ALUs (signed direction times activations, then times the fp32 radius); batches 3..8 on
+ * 4x4x4 MFMA blocks, one vector per block, each block's sum times the fp32 radius; batches 9..32
+ * on 16x16x32 MFMA tiles with Eq. 7 factored over each 128-weight group, offset * sum <t, x> +
+ * step * sum q <t, x>, where t (the signed direction) and q * t (split exactly into two fp16
+ * numbers) are the operands (9..16 inside the step plan, 17..32 in the prefill kernel of sph_gemm
+ * with 32 activation rows staged in LDS). Asynchronous on `stream`. */
 sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y,
                           int64_t ldy, sph_dtype y_dtype, void* d_ws, size_t ws_bytes,
                           void* stream);
 
 /* Y = X W^T for any batch 1 <= m <= 65536 (prefill and large batches): m <= 32 is sph_gemm_small;
- * larger batches run on the matrix cores (16x16x32 fp16 MFMA, fp32 accumulation) with each
- * weight rebuilt as fp16(r * t) once per 64- or 128-row slice of X (128 for the nibble formats,
- * 64 for D = 13) and per 128-column chunk of K. Same argument rules as sph_gemm_small. When the
+ * larger batches run on the matrix cores (16x16x32 fp16 MFMA, fp32 accumulation) with the
+ * factored exact-product arithmetic of sph_gemm_small's batches above 8, each weight's operands
+ * rebuilt once per 64-row slice of X and per 128-column chunk of K. Same argument rules as
+ * sph_gemm_small. When the
  * grid would not cover the chip, K is split and fp32 partial outputs go through the workspace
  * (sph_workspace_bytes(w, m); for m > 32 it needs no zero-fill) and are added in a fixed order,
  * so repeated calls give bitwise identical results. Asynchronous on `stream`. */
@@ -131,18 +138,24 @@ sph_status sph_gemm(const sph_weights* w, const void* d_x, int64_t m, int64_t ld
 
 /* Device workspace needed by sph_gemv (m = 1), sph_gemm_small or sph_gemm for this matrix and
  * batch (1 <= m <= 65536) on the current device (0 when the call needs none; d_ws may then be
- * NULL). It holds split-K partial sums (and, for m <= 16, one arrival counter per 16-row tile):
- * it must be 256-byte aligned and zero-filled before its first use, and every call leaves it
- * zero-filled again (above m = 32 it needs no initial contents, but is still left zero-filled).
- * Calls that may run concurrently must not share one. */
+ * NULL). For m <= 16 it holds the partial sums of 16-row tiles whose K range is split between
+ * workgroups (a 64-bit slot per part and value: fp32 sum and a valid flag) and one 32-bit arrival
+ * counter per tile; above m = 16 it holds fp32 partial outputs of a K split. It must be 256-byte
+ * aligned and zero-filled before its first use, and every call leaves it zero-filled again (above
+ * m = 32 it needs no initial contents, but is still left zero-filled). Calls that may run
+ * concurrently must not share one. No call waits for another workgroup to make progress, so calls
+ * on other streams may occupy any part of the GPU meanwhile. */
 sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes);
 
 /* Read the packed matrix back as logical codes, on the device, with the same bit extraction the
- * compute kernels use: d_signs uint8[n][k/8], d_dir_idx uint16[n][k/8], d_radius_code
- * uint8[n][k/8] are caller-owned device arrays. For the table-lookup formats the sign bits and
- * the direction are recovered from the two lookup indices each row uses; a mismatch between the
+ * compute kernels use: d_signs uint8[n][k/vec_dim] (uint16 for vec_dim 16), d_dir_idx
+ * uint16[n][k/vec_dim], d_radius_code uint8[n][k/vec_dim] are caller-owned DEVICE arrays, written
+ * asynchronously on `stream`; the caller copies them to the host and synchronizes. (A host-array,
+ * synchronous form would need device staging memory, and the library never allocates device
+ * memory; the Python binding does the copy.) For the table-lookup formats the sign bits and the
+ * direction are recovered from the two lookup indices each row uses; a mismatch between the
  * direction seen through the low and the high table is reported by setting the direction to
- * 0xFFFF. Asynchronous on `stream`. Intended for bit-exactness tests. */
+ * 0xFFFF. Intended for bit-exactness tests. */
 sph_status sph_unpack(const sph_weights* w, uint8_t* d_signs, uint16_t* d_dir_idx,
                       uint8_t* d_radius_code, void* stream);
 

@@ -61,6 +61,7 @@ struct KArgs {
   int pmax;           // slot parts per tile
   int ts;
   uint64_t* ws_slot;  // [nt][pmax][M][16] tagged partial sums of split tiles, zero between calls
+  uint32_t* ws_cnt;   // [nt] arrivals at each split tile, zero between calls
   // prefill path (batch > 32): K split into ks ranges; with ks > 1 each range writes fp32 partial
   // outputs [ks][m][nt * 16] to ws_part and a second kernel adds them in range order
   int ks;
@@ -125,14 +126,30 @@ __device__ __forceinline__ float f16lo(uint32_t u) { return (float)__builtin_bit
 __device__ __forceinline__ float f16hi(uint32_t u) { return (float)__builtin_bit_cast(f16, (uint16_t)(u >> 16)); }
 __device__ __forceinline__ f16x2 as_h2(uint32_t u) { return __builtin_bit_cast(f16x2, u); }
 
-// r * t for the 8 fp16 values of t, each rounded once to fp16 (v_fma_mix writes one half each).
+// q * t for the 8 fp16 values of a signed direction t and a level q < 2^8, split exactly into two
+// fp16 words, hi = fp16(q * t) and lo = q * t - hi. The product has at most 11 + 8 significant bits
+// and is a multiple of t's unit in the last place, so the rounding residual is at most 2^7 such
+// units and fits an fp16 significand exactly; the fused multiply-add returns it without rounding.
+// |q * t| <= 255 * 2 because the packer admits codebook entries of at most 2, so nothing overflows.
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t scale_h2(uint32_t t, float r) {
-  const f32x2 p = {fmaf(f16lo(t), r, 0.0f), fmaf(f16hi(t), r, 0.0f)};   // products rounded to fp32
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(p, f16x2));
+__device__ __forceinline__ void qt_split(uint4 t, uint32_t q, uint4& hi, uint4& lo) {
+  const f16 qh = (f16)(float)q;
+  const f16x2 qq = {qh, qh};
+  const f16x2 h0 = as_h2(t.x) * qq, h1 = as_h2(t.y) * qq, h2 = as_h2(t.z) * qq, h3 = as_h2(t.w) * qq;
+  const f16x2 l0 = __builtin_elementwise_fma(as_h2(t.x), qq, -h0);
+  const f16x2 l1 = __builtin_elementwise_fma(as_h2(t.y), qq, -h1);
+  const f16x2 l2 = __builtin_elementwise_fma(as_h2(t.z), qq, -h2);
+  const f16x2 l3 = __builtin_elementwise_fma(as_h2(t.w), qq, -h3);
+  hi = make_uint4(__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1), __builtin_bit_cast(uint32_t, h2),
+                  __builtin_bit_cast(uint32_t, h3));
+  lo = make_uint4(__builtin_bit_cast(uint32_t, l0), __builtin_bit_cast(uint32_t, l1), __builtin_bit_cast(uint32_t, l2),
+                  __builtin_bit_cast(uint32_t, l3));
 }
-__device__ __forceinline__ uint4 scale_dir(uint4 t, float r) {
-  return make_uint4(scale_h2(t.x, r), scale_h2(t.y, r), scale_h2(t.z, r), scale_h2(t.w, r));
+
+// Value of lane E of this lane's quad (lanes 4i..4i+3), by a DPP quad permutation.
+template <int E>
+__device__ __forceinline__ float quad_bcast(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), E * 0x55, 0xF, 0xF, false));
 }
 
 __device__ __forceinline__ float dot8(uint4 t, const uint32_t (&x)[4]) {
@@ -198,11 +215,12 @@ struct Tables {
   static constexpr uint32_t bytes = IS_CB<KIND> ? ((16u << D) + 128u) : (256u << D);
 };
 
-// Whether the split-tile parts of one workgroup's waves fit in LDS next to the lookup table (else
-// they go through the global workspace, and the plan keeps to balanced ranges). Host and device.
+// Whether the split-tile slots and counters of one workgroup's waves fit in LDS next to the lookup
+// table and the parameter staging (else they go through the global workspace, and the plan keeps
+// to balanced ranges). Host and device.
 __host__ __device__ constexpr bool lds_handover_fits(int kind, int D, int M, int mode) {
-  return ((kind == SPH_KIND_CB13 || kind == SPH_KIND_CB13Q4) ? ((16u << D) + 128u) : (256u << D)) + 16u * M * 16u * 8u +
-             (mode == 2 ? 0u : 16u * 256u) <= 160u * 1024u;
+  return ((kind == SPH_KIND_CB13 || kind == SPH_KIND_CB13Q4) ? ((16u << D) + 128u) : (256u << D)) +
+             (16u * 2u * M * 16u * 4u + 16u * 4u) + (mode == 2 ? 0u : 16u * 256u) <= 160u * 1024u;
 }
 
 // MX selects the matrix-core variant (batch 2..16): the lane's rows are rebuilt as in the vector
@@ -325,21 +343,24 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL, MX>& R, floa
       const int r = j * RB + i;
       const float rh = fmaf(qf[j & 1][i], f16hi(pp[r]), f16lo(pp[r]));
       if constexpr (MX) {
-        // w = fp16(r * t), one rounding per weight. Block v of the MFMA is this lane's vector
-        // position; its row lane % 4 is the lane's row 4 * (lane % 4) + r, and its column
-        // lane % 4 is batch row 4g + lane % 4, so lane (v, j) accumulates rows 4e + r (e = 0..3,
-        // in acc[4g + r][e]) of batch row 4g + j.
-        const uint4 w = scale_dir(tt[j & 1][i], rh);
-        const uint2 wlo = make_uint2(w.x, w.y), whi = make_uint2(w.z, w.w);
+        // Exact products, as in the vector-ALU path: block v of the MFMA is this lane's vector
+        // position, its row lane % 4 the quad lane's row 4 * (lane % 4) + r (rebuilt there as the
+        // signed direction t, exact in fp16) and its column lane % 4 batch row 4g + lane % 4. So
+        // lane (v, j) receives D[e] = <t, x> of row 4e + r and batch row 4g + j: fp16 products
+        // summed in fp32 over the vector's 8 elements. Each is scaled in fp32 by that row's radius,
+        // which lane e of the quad computed, and added to acc[4g + r][e].
+        const uint4 t = tt[j & 1][i];
+        const float re[4] = {quad_bcast<0>(rh), quad_bcast<1>(rh), quad_bcast<2>(rh), quad_bcast<3>(rh)};
+        const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int g = 0; g < M / 4; ++g) {
-          f32x4 d = {acc[4 * g + r][0], acc[4 * g + r][1], acc[4 * g + r][2], acc[4 * g + r][3]};
-          d = __builtin_amdgcn_mfma_f32_4x4x4f16(__builtin_bit_cast(f16x4, wlo),
-                                                  __builtin_bit_cast(f16x4, make_uint2(R.xv[g][0], R.xv[g][1])), d, 0, 0, 0);
-          d = __builtin_amdgcn_mfma_f32_4x4x4f16(__builtin_bit_cast(f16x4, whi),
+          f32x4 d = __builtin_amdgcn_mfma_f32_4x4x4f16(__builtin_bit_cast(f16x4, make_uint2(t.x, t.y)),
+                                                        __builtin_bit_cast(f16x4, make_uint2(R.xv[g][0], R.xv[g][1])), z, 0,
+                                                        0, 0);
+          d = __builtin_amdgcn_mfma_f32_4x4x4f16(__builtin_bit_cast(f16x4, make_uint2(t.z, t.w)),
                                                   __builtin_bit_cast(f16x4, make_uint2(R.xv[g][2], R.xv[g][3])), d, 0, 0, 0);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) acc[4 * g + r][e] = d[e];
+          for (int e = 0; e < 4; ++e) acc[4 * g + r][e] = fmaf(re[e], d[e], acc[4 * g + r][e]);
         }
       } else {
 #pragma unroll
@@ -353,16 +374,19 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL, MX>& R, floa
 // Tile variant (batch 9..16): lane (r, j) = (lane % 16, lane / 16) rebuilds row r of the vector
 // positions 4i + j (i = 0..3) of a 16-position chunk, which is exactly the A operand of
 // v_mfma_f32_16x16x32_f16 (16 rows x 4 positions); the B operand is x for batch rows
-// 16nb + lane % 16 at the same positions. The MFMA sums over the chunk, so each lane ends a step
-// with finished sums for (batch 16nb + lane % 16, rows 4 * (lane / 16) + e) and no lane reduction
-// is needed. One record dword (and one aux dword) per position and lane: 128 contiguous bytes
-// per load over the wave.
+// 16nb + lane % 16 at the same positions. A chunk is one radius group, so Eq. 7 factors over it:
+// sum_v r^_v <t_v, x_v> = offset * sum_v <t_v, x_v> + step * sum_v q_v <t_v, x_v>. The MFMA forms
+// both sums with exact fp16 operands -- the signed directions t, and q * t split exactly into two
+// fp16 words -- so every product is exact and only fp32 sums round; each lane then ends a step
+// with both sums for (batch 16nb + lane % 16, rows 4 * (lane / 16) + e) and folds them into its
+// accumulators with those rows' offset and step. No lane reduction is needed. One record dword
+// (and one aux dword) per position and lane: 128 contiguous bytes per load over the wave.
 template <int KIND, int NB>
 struct RecT {
   uint32_t ra[4];
   uint32_t rb[4];
   uint32_t rc[4];         // stream C words (codebook kind with 4 radius bits)
-  uint32_t pw;            // (min, step) of this lane's row in the chunk's group
+  uint4 pw;               // (offset, step) of rows 4 * (lane / 16) + e of the chunk's group
   uint32_t xv[NB * 4][4]; // x[16nb + lane % 16] at position 4i + j, index nb * 4 + i
   bool pok;
 };
@@ -386,9 +410,9 @@ __device__ __forceinline__ void load_rec_t(RecT<KIND, NB>& R, const KArgs& a, in
     if constexpr (KIND == SPH_KIND_CB13Q4) R.rc[i] = a.C[rec];
     else R.rc[i] = 0;
   }
-  // one 128-weight group per chunk: (min, step) of row r
+  // one 128-weight group per chunk: (offset, step) of the rows this lane's sums belong to
   const int pg = min(c, a.ng - 1);
-  R.pw = a.P[((int64_t)t * a.ng + pg) * 16 + r];
+  R.pw = *(const uint4*)(a.P + ((int64_t)t * a.ng + pg) * 16 + 4 * j);
   R.pok = c < a.ng;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
@@ -405,8 +429,6 @@ template <int KIND, int D, int NB>
 __device__ __forceinline__ void compute_rec_t(const RecT<KIND, NB>& R, float (&acc)[NB][4], const unsigned char* lds,
                                               uint32_t mask_off, int lane) {
   const int r = lane & 15;
-  const uint32_t pw = R.pok ? R.pw : 0u;
-  const float lo = f16lo(pw), st = f16hi(pw);
   uint4 tt[4];
   uint32_t q[4];
 #pragma unroll
@@ -425,19 +447,28 @@ __device__ __forceinline__ void compute_rec_t(const RecT<KIND, NB>& R, float (&a
       tt[i] = signed_dir_nib<KIND, D>(lds, l, hh);
     }
   }
+  f32x4 s0[NB], s1[NB];   // sum <t, x> and sum q <t, x> over the chunk
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) s0[nb] = s1[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const uint4 w = scale_dir(tt[i], fmaf((float)q[i], st, lo));   // fp16(r * t), one rounding
+    uint4 hi, lo;
+    qt_split(tt[i], q[i], hi, lo);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const uint32_t* xq = R.xv[nb * 4 + i];
-      f32x4 d = {acc[nb][0], acc[nb][1], acc[nb][2], acc[nb][3]};
-      d = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, w),
-                                                 __builtin_bit_cast(f16x8, make_uint4(xq[0], xq[1], xq[2], xq[3])), d, 0, 0, 0);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[nb][e] = d[e];
+      const f16x8 xb = __builtin_bit_cast(f16x8, make_uint4(xq[0], xq[1], xq[2], xq[3]));
+      s0[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, tt[i]), xb, s0[nb], 0, 0, 0);
+      s1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, hi), xb, s1[nb], 0, 0, 0);
+      s1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, lo), xb, s1[nb], 0, 0, 0);
     }
   }
+  const uint4 pw = R.pok ? R.pw : make_uint4(0u, 0u, 0u, 0u);
+  const uint32_t pe[4] = {pw.x, pw.y, pw.z, pw.w};
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[nb][e] = fmaf(f16hi(pe[e]), s1[nb][e], fmaf(f16lo(pe[e]), s0[nb][e], acc[nb][e]));
 }
 
 // Step dispatch over the three variants (MODE 0: vector ALU, 1: 4x4x4 blocks, 2: 16x16x32 tiles).
@@ -498,14 +529,6 @@ __device__ __forceinline__ void wave_reduce(float (&v)[NVAL], int lane) {
   }
 }
 
-// Split-K slots: one 64-bit word per (tile, segment, batch row, tile row) holding the fp32
-// partial sum in the low half and a valid flag in the high half, written and read with
-// device-coherent (agent-scope) atomics so that a single load sees value and flag together.
-__device__ __forceinline__ void slot_store(uint64_t* p, float v) {
-  __hip_atomic_store(p, (uint64_t)__builtin_bit_cast(uint32_t, v) | (1ull << 32), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-}
-
 // n steps cut into `parts` contiguous pieces, the first n % parts of them one step longer: the
 // start of piece i, and the piece holding step x. 32-bit arithmetic only (the kernel computes
 // these in its prologue, before its first loads).
@@ -545,9 +568,59 @@ __device__ __forceinline__ int wave_of_step(const KArgs& a, int s) {
   return __builtin_amdgcn_readfirstlane(b * VALU_WPB + piece_of(n, min(VALU_WPB, n), s - s0));
 }
 
-// Slot words of the other parts of a split tile, fetched by the wave holding chunk 0 before it
-// computes its last step, so that their round trip overlaps that computation: lane l reads slot
-// index l % NIDX of parts 1 + l / NIDX + PPI * j, j < JB.
+// ------------------------------------------------------------------------------------------
+// Split tiles. A tile whose steps fall into the ranges of several waves has one part per wave: part
+// 0 (holding chunk 0) ends its wave's range, parts 1 .. np-1 start the ranges of the following
+// waves. Every part reduces its sums across lanes, puts them in a slot, and then counts its arrival
+// on the tile's counter; the part that arrives last adds part 0 to the sum of parts 1 .. np-1
+// (formed by the lanes in a fixed order, see gather_parts) and stores y. No wave waits for another
+// one to make progress: whichever part arrives last finds every other part's slot written. The
+// sum does not depend on which part arrives last, so results are bitwise reproducible.
+//
+// Tiles whose parts all lie in one workgroup meet in LDS (a slot per wave and role, a counter per
+// wave holding a part 0). The others meet in the global workspace: a 64-bit slot per value, the
+// fp32 sum in the low half and a valid flag in the high half, and a 32-bit counter per tile, all
+// written and read with device-coherent (agent-scope) atomics and no fences. A counter can show a
+// part as arrived while its slot stores, issued before the arrival, are still in flight; the last
+// arriver then re-reads that slot until the store lands -- a wait for a store already issued, not
+// for another wave. The last arriver clears the slots and the counter it used, so the workspace is
+// zero again after every call.
+// ------------------------------------------------------------------------------------------
+__device__ __forceinline__ void slot_store(uint64_t* p, float v) {
+  __hip_atomic_store(p, (uint64_t)__builtin_bit_cast(uint32_t, v) | (1ull << 32), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t slot_load(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// A global slot word whose store was issued before its part's arrival was counted: re-read until
+// the store has landed. The bound (about 100 ms on the 100 MHz real-time counter, far beyond any
+// memory latency) is never expected to run out; if it did, the sum is marked invalid (NaN).
+__device__ __forceinline__ float landed(uint64_t w, const uint64_t* p, bool& ok) {
+  if ((w >> 32) == 0) {
+    const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + 10000000ull;
+    do {
+      __builtin_amdgcn_s_sleep(1);
+      w = slot_load(p);
+    } while ((w >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline);
+    ok = ok && (w >> 32) != 0;
+  }
+  return __builtin_bit_cast(float, (uint32_t)w);
+}
+
+// LDS meeting place of the split tiles inside a workgroup: per wave a slot for a later part it
+// holds (role 0) and one for a part 0 (role 1), and the arrival counter of the tile whose part 0
+// it holds (each wave holds at most one later part, its first, and one part 0, its last).
+template <int M>
+struct WgHo {
+  float slot[VALU_WPB][2][M * 16];
+  uint32_t cnt[VALU_WPB];
+};
+
+// Global slot words of parts 1 + l / NIDX + PPI * j (j < JB) at index l % NIDX (+ 64 k) for lane
+// l, and the tile's counter: fetched by the wave holding part 0 before its last step, so that
+// their round trip overlaps that step.
 template <int M>
 struct SlotPre {
   static constexpr int NIDX = M * 16;
@@ -555,152 +628,214 @@ struct SlotPre {
   static constexpr int IPP = NIDX <= 64 ? 1 : NIDX / 64;   // load instructions per part
   static constexpr int JB = IPP >= 4 ? 1 : 4 / IPP;        // parts per lane loaded together
   uint64_t w[JB][IPP];
+  uint32_t cnt;
 };
 
-// Parts held by waves of the same workgroup are handed over through LDS instead (see emit_part);
-// only the parts of other workgroups are fetched here.
-template <int M, bool LDS_HO = true>
-__device__ __forceinline__ void fetch_parts(SlotPre<M>& P, const KArgs& a, int t, int np, int j0, int g, int lane) {
+template <int M>
+__device__ __forceinline__ void fetch_parts(SlotPre<M>& P, const KArgs& a, int t, int np, int j0, int lane) {
   using S = SlotPre<M>;
   const uint64_t* slots = a.ws_slot + (int64_t)t * a.pmax * S::NIDX;
   const int loff = (S::NIDX >= 64) ? 0 : lane / S::NIDX;
 #pragma unroll
   for (int j = 0; j < S::JB; ++j) {
     const int p = min(1 + loff + S::PPI * (j0 + j), np - 1);
-    const bool same_wg = LDS_HO && (g + p) / VALU_WPB == g / VALU_WPB;
 #pragma unroll
-    for (int k = 0; k < S::IPP; ++k)
-      P.w[j][k] = same_wg ? 0ull
-                          : __hip_atomic_load(slots + (int64_t)p * S::NIDX + (lane % S::NIDX) + 64 * k,
-                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int k = 0; k < S::IPP; ++k) P.w[j][k] = slot_load(slots + (int64_t)p * S::NIDX + (lane % S::NIDX) + 64 * k);
+  }
+  P.cnt = __hip_atomic_load(a.ws_cnt + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Slot index (batch row * 16 + tile row) of value i of this lane after the wave reduction: vector
+// variant, value b * RPL + r is batch row b, tile row h * RPL + r; 4x4x4 blocks, value 16g + 4r + e
+// is batch row 4g + h, tile row 4e + r (see compute_rec); tiles, value 4nb + e is batch row
+// 16nb + lane % 16, tile row 4 * (lane / 16) + e (see compute_rec_t).
+template <int M, int RPL, int MODE>
+struct PartIdx {
+  static constexpr int H = 16 / RPL;
+  static constexpr int AR = MODE == 2 ? M / 16 : M;
+  static constexpr int NVAL = AR * RPL, N4 = MODE == 2 ? NVAL : NVAL / 4;
+  int idx[N4];
+  bool writer;   // one writer lane per h in each 16-lane row; the tile variant's sums are per lane
+  __device__ __forceinline__ explicit PartIdx(int lane) {
+    const int h = lane % H;
+    writer = MODE == 2 || (lane & 15) < H;
+    const int base = MODE == 2 ? 0 : ((lane >> 5) & 1) * (NVAL / 2) + ((lane >> 4) & 1) * N4;
+#pragma unroll
+    for (int i = 0; i < N4; ++i) {
+      const int f = base + i;
+      if constexpr (MODE == 2) idx[i] = (16 * (f / 4) + (lane & 15)) * 16 + 4 * (lane >> 4) + f % 4;
+      else if constexpr (MODE == 1) idx[i] = ((f / 16) * 4 + h) * 16 + 4 * (f % 4) + (f / 4) % 4;
+      else idx[i] = (f / RPL) * 16 + h * RPL + f % RPL;
+    }
+  }
+};
+
+template <int M, int RPL, int MODE>
+__device__ __forceinline__ void store_part(const KArgs& a, int t, const PartIdx<M, RPL, MODE>& I,
+                                           const float (&v)[PartIdx<M, RPL, MODE>::N4], bool ok) {
+  if (!I.writer) return;
+#pragma unroll
+  for (int i = 0; i < PartIdx<M, RPL, MODE>::N4; ++i) {
+    const int b = I.idx[i] / 16, grow = t * 16 + I.idx[i] % 16;
+    if (b < a.m && grow < a.n) store_y(a, b, grow, ok ? v[i] : __builtin_nanf(""));
   }
 }
 
-// Finish the part [ca, cb) of tile t computed by wave g: reduce across lanes, then store y
-// (whole tile), hand the part over (ca > 0; only the first part of a range can be one), or, as
-// the part holding chunk 0 of a split tile (only possible when MAY_WAIT; np parts in all), add the
-// other parts in chunk order and store y. The waits are bounded by a
-// deadline on the constant 100 MHz real-time counter (about 50 ms, thousands of times a whole
-// launch); a wait that runs out (not expected) stores NaN rather than hanging.
-template <int M, int RPL, bool MAY_WAIT, int MODE = 0, bool LDS_HO = true>
-__device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[MODE == 2 ? M / 16 : M][RPL], int t, int ca,
-                                          int cb, int g, int lane, int h, const SlotPre<M>& pre, bool have_pre,
-                                          uint64_t* wg_slots, int np) {
-  int gr;
-  constexpr int H = 16 / RPL;
-  constexpr int AR = MODE == 2 ? M / 16 : M;
-  constexpr int NVAL = AR * RPL, N4 = MODE == 2 ? NVAL : NVAL / 4;
-  float vals[NVAL];
+// Finish split tile t as its last arriving part (p_self; own values in `vals`, used when it is
+// part 0): y = part 0 + (sum of parts 1 .. np-1). Lane l adds, in increasing part order, slot
+// index l % NIDX (+ 64 k) of parts 1 + l / NIDX + PPI * j; the lanes holding one slot index are
+// then added by a fixed exchange tree; the writer lanes add that to part 0. GLOBAL: the parts are
+// in the workspace (the first batch possibly prefetched in `pre`), which is cleared afterwards.
+template <int M, int RPL, int MODE, bool GLOBAL>
+__device__ __forceinline__ void finish_tile(const KArgs& a, int t, int np, int gr, int p_self,
+                                         const float (&vals)[PartIdx<M, RPL, MODE>::N4], const SlotPre<M>* pre,
+                                         const WgHo<M>* ho, int lane) {
+  using S = SlotPre<M>;
+  using I = PartIdx<M, RPL, MODE>;
+  constexpr int NIDX = S::NIDX, PPI = S::PPI, IPP = S::IPP, JB = S::JB;
+  const I ix(lane);
+  const uint64_t* slots = GLOBAL ? a.ws_slot + (int64_t)t * a.pmax * NIDX : nullptr;
+  bool ok = true;
+  float ps[IPP];
 #pragma unroll
-  for (int b = 0; b < AR; ++b)
+  for (int k = 0; k < IPP; ++k) ps[k] = 0.0f;
+  const int loff = (NIDX >= 64) ? 0 : lane / NIDX;
+  for (int j0 = 0; 1 + PPI * j0 < np; j0 += JB) {
+    S P;
+    if constexpr (GLOBAL) {
+      if (j0 == 0 && pre) P = *pre;
+      else fetch_parts<M>(P, a, t, np, j0, lane);
+    }
+#pragma unroll
+    for (int j = 0; j < JB; ++j) {
+      const int p = 1 + loff + PPI * (j0 + j);
+      if (p < np) {
+#pragma unroll
+        for (int k = 0; k < IPP; ++k) {
+          const int si = (lane % NIDX) + 64 * k;
+          if constexpr (GLOBAL) ps[k] += landed(P.w[j][k], slots + (int64_t)p * NIDX + si, ok);
+          else ps[k] += ho->slot[(gr + p) % VALU_WPB][0][si];
+        }
+      }
+    }
+  }
+  // lanes l and l ^ NIDX, ... hold the same slot index: add them, larger distances first
+  if constexpr (NIDX <= 16) ps[0] += __shfl_xor(ps[0], 32);
+  if constexpr (NIDX <= 16) ps[0] += __shfl_xor(ps[0], 16);
+  if constexpr (NIDX == 32) ps[0] += __shfl_xor(ps[0], 32);
+  float tot[I::N4];
+#pragma unroll
+  for (int i = 0; i < I::N4; ++i) {
+    const int src = ix.idx[i] % 64, k = ix.idx[i] / 64;
+    float other = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < IPP; ++kk) {
+      const float v = __shfl(ps[kk], src);
+      if (kk == k) other = v;
+    }
+    float base = vals[i];
+    if (p_self != 0) {
+      if constexpr (GLOBAL) base = landed(slot_load(slots + ix.idx[i]), slots + ix.idx[i], ok);
+      else base = ho->slot[gr % VALU_WPB][1][ix.idx[i]];
+    }
+    tot[i] = base + other;
+  }
+  store_part<M, RPL, MODE>(a, t, ix, tot, __all(ok));
+  if constexpr (GLOBAL) {
+    // every part has arrived and been read: clear the slots and the counter for the next call
+    for (int p = 0; p < np; ++p)
+#pragma unroll
+      for (int k = 0; k < (NIDX + 63) / 64; ++k)
+        if (lane + 64 * k < NIDX)
+          __hip_atomic_store((uint64_t*)slots + (int64_t)p * NIDX + lane + 64 * k, 0ull, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0) __hip_atomic_store(a.ws_cnt + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Count a part's arrival at a tile meeting in the workspace (its slot written before), and finish
+// the tile if it arrived last.
+template <int M, int RPL, int MODE>
+__device__ __forceinline__ void arrive_global(const KArgs& a, int t, int np, int gr, int p,
+                                              const float (&v4)[PartIdx<M, RPL, MODE>::N4], const WgHo<M>* ho,
+                                              int lane) {
+  uint32_t old = 0;
+  if (lane == 0)
+    old = __hip_atomic_fetch_add(a.ws_cnt + t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (__builtin_amdgcn_readfirstlane(old) + 1 == (uint32_t)np) finish_tile<M, RPL, MODE, true>(a, t, np, gr, p, v4, nullptr, ho, lane);
+}
+
+// A part handed over inside the step loop (a range's first part), to be followed up after the
+// loop: a tile that met in LDS and whose last part it was (finish it), or a tile meeting in the
+// workspace (count the arrival -- its slot is written already -- and finish the tile if it was the
+// last). All wave-uniform, so the loop carries no vector register for it: a count returned by an
+// atomic inside the loop would make the compiler wait for it there, draining the records in flight.
+struct Pending {
+  int t = -1, np = 0, p = 0;
+  bool lds = false;
+};
+
+// Finish the part [ca, cb) of tile t computed by wave g: reduce across lanes, then store y (whole
+// tile) or hand the part over as described above. FINAL: the range's last part, after which the
+// wave has no loads in flight, so it counts its arrival and finishes the tile straight away if it
+// arrived last; otherwise the follow-up is left in `pend`.
+template <int M, int RPL, int MODE, bool LDS_HO, bool FINAL>
+__device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[MODE == 2 ? M / 16 : M][RPL], int t, int ca,
+                                          int cb, int g, int lane, const SlotPre<M>& pre, bool have_pre, WgHo<M>* ho,
+                                          Pending& pend) {
+  using I = PartIdx<M, RPL, MODE>;
+  constexpr int H = 16 / RPL;
+  float vals[I::NVAL];
+#pragma unroll
+  for (int b = 0; b < I::AR; ++b)
 #pragma unroll
     for (int r = 0; r < RPL; ++r) {
       vals[b * RPL + r] = acc[b][r];
       acc[b][r] = 0.0f;
     }
-  if constexpr (MODE != 2) wave_reduce<NVAL, H>(vals, lane);
-  // one writer lane per h in each 16-lane row; the tile variant's sums are already per lane
-  const bool writer = MODE == 2 || (lane & 15) < H;
-  const int base = MODE == 2 ? 0 : ((lane >> 5) & 1) * (NVAL / 2) + ((lane >> 4) & 1) * N4;
-  int idx[N4];                               // slot index b*16 + row of value i
+  if constexpr (MODE != 2) wave_reduce<I::NVAL, H>(vals, lane);
+  const I ix(lane);
+  float v4[I::N4];
 #pragma unroll
-  for (int i = 0; i < N4; ++i) {
-    const int f = base + i;
-    // vector variant: value b * RPL + r is batch row b, tile row h * RPL + r; 4x4x4 blocks: value
-    // 16g + 4r + e is batch row 4g + h, tile row 4e + r (see compute_rec); tiles: value 4nb + e
-    // is batch row 16nb + lane % 16, tile row 4 * (lane / 16) + e (see compute_rec_t)
-    if constexpr (MODE == 2) idx[i] = (16 * (f / 4) + (lane & 15)) * 16 + 4 * (lane >> 4) + f % 4;
-    else if constexpr (MODE == 1) idx[i] = ((f / 16) * 4 + h) * 16 + 4 * (f % 4) + (f / 4) % 4;
-    else idx[i] = (f / RPL) * 16 + h * RPL + f % RPL;
+  for (int i = 0; i < I::N4; ++i) v4[i] = vals[i];
+  if (ca == 0 && cb == a.nc) {
+    store_part<M, RPL, MODE>(a, t, ix, v4, true);
+    return;
   }
-  if (ca > 0) {
-    gr = wave_of_step(a, t * a.nc);            // the wave holding chunk 0 of this tile
-    if (!writer) return;
-    if (LDS_HO && gr / VALU_WPB == g / VALU_WPB) {
-      // same workgroup: this wave's LDS slot (a wave hands over at most one part per launch)
-      uint64_t* slot = wg_slots + (g % VALU_WPB) * (M * 16);
+  const int gr = wave_of_step(a, t * a.nc);
+  const int np = wave_of_step(a, t * a.nc + a.nc - 1) - gr + 1;
+  const int p = g - gr;
+  if (LDS_HO && gr / VALU_WPB == (gr + np - 1) / VALU_WPB) {
+    float* mine = ho->slot[g % VALU_WPB][p == 0 ? 1 : 0];
+    if (ix.writer)
 #pragma unroll
-      for (int i = 0; i < N4; ++i)
-        __hip_atomic_store(slot + idx[i], (uint64_t)__builtin_bit_cast(uint32_t, vals[i]) | (1ull << 32),
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    } else {
-      uint64_t* slot = a.ws_slot + ((int64_t)t * a.pmax + (g - gr)) * (M * 16);
-#pragma unroll
-      for (int i = 0; i < N4; ++i) slot_store(slot + idx[i], vals[i]);
+      for (int i = 0; i < I::N4; ++i) mine[ix.idx[i]] = v4[i];
+    // the slot writes have reached LDS before the arrival is counted (lgkmcnt(0), other counters
+    // left alone)
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    uint32_t old = 0;
+    if (lane == 0)
+      old = __hip_atomic_fetch_add(&ho->cnt[gr % VALU_WPB], 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (__builtin_amdgcn_readfirstlane(old) + 1 == (uint32_t)np) {
+      if constexpr (FINAL) finish_tile<M, RPL, MODE, false>(a, t, np, gr, p, v4, nullptr, ho, lane);
+      else pend = Pending{t, np, p, true};
     }
     return;
   }
-  bool ok = true;
-  if (MAY_WAIT && cb < a.nc) {
-    // All 64 lanes fetch the other parts (the first batch normally prefetched, see SlotPre). Each
-    // lane adds its parts in increasing j, the lanes holding one slot index are then added by a
-    // fixed exchange tree, and the writer lanes add the result to their own part: a fixed order,
-    // independent of timing.
-    using S = SlotPre<M>;
-    constexpr int NIDX = S::NIDX, PPI = S::PPI, IPP = S::IPP, JB = S::JB;
-    uint64_t* slots = a.ws_slot + (int64_t)t * a.pmax * NIDX;
-    const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + 5000000ull;
-    float ps[IPP];
-#pragma unroll
-    for (int k = 0; k < IPP; ++k) ps[k] = 0.0f;
-    const int loff = (NIDX >= 64) ? 0 : lane / NIDX;
-    for (int j0 = 0; 1 + loff + PPI * j0 < np; j0 += JB) {
-      S P = pre;
-      if (j0 > 0 || !have_pre) fetch_parts<M, LDS_HO>(P, a, t, np, j0, g, lane);
-#pragma unroll
-      for (int j = 0; j < JB; ++j) {
-        const int p = 1 + loff + PPI * (j0 + j);
-        if (p < np) {
-          const bool same_wg = LDS_HO && (g + p) / VALU_WPB == g / VALU_WPB;
-#pragma unroll
-          for (int k = 0; k < IPP; ++k) {
-            const int si = (lane % NIDX) + 64 * k;
-            uint64_t w = P.w[j][k];
-            if (same_wg) {
-              uint64_t* q = wg_slots + ((g + p) % VALU_WPB) * NIDX + si;
-              w = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-              while ((w >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline) {
-                __builtin_amdgcn_s_sleep(1);
-                w = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-              }
-            } else {
-              uint64_t* q = slots + (int64_t)p * NIDX + si;
-              while ((w >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline) {
-                __builtin_amdgcn_s_sleep(2);
-                w = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-              }
-              __hip_atomic_store(q, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            ok = ok && (w >> 32) != 0;
-            ps[k] += __builtin_bit_cast(float, (uint32_t)w);
-          }
-        }
-      }
+  if constexpr (FINAL) {
+    if (p == 0 && have_pre && __builtin_amdgcn_readfirstlane(pre.cnt) + 1 == (uint32_t)np) {
+      // every later part has arrived: finish with the prefetched slots, no arrival of our own
+      finish_tile<M, RPL, MODE, true>(a, t, np, gr, 0, v4, &pre, ho, lane);
+      return;
     }
-    // lanes l and l ^ NIDX, ... hold the same slot index: add them, larger distances first
-    if constexpr (NIDX <= 16) ps[0] += __shfl_xor(ps[0], 32);
-    if constexpr (NIDX <= 16) ps[0] += __shfl_xor(ps[0], 16);
-    if constexpr (NIDX == 32) ps[0] += __shfl_xor(ps[0], 32);
-    const bool all_ok = __all(ok);
-#pragma unroll
-    for (int i = 0; i < N4; ++i) {
-      const int src = idx[i] % 64, k = idx[i] / 64;
-      float other = 0.0f;
-#pragma unroll
-      for (int kk = 0; kk < IPP; ++kk) {
-        const float v = __shfl(ps[kk], src);
-        if (kk == k) other = v;
-      }
-      vals[i] += other;
-    }
-    ok = all_ok;
   }
-  if (!writer) return;
+  uint64_t* slot = a.ws_slot + ((int64_t)t * a.pmax + p) * (M * 16);
+  if (ix.writer)
 #pragma unroll
-  for (int i = 0; i < N4; ++i) {
-    const int b = idx[i] / 16, grow = t * 16 + idx[i] % 16;
-    if (b < a.m && grow < a.n) store_y(a, b, grow, ok ? vals[i] : __builtin_nanf(""));
-  }
+    for (int i = 0; i < I::N4; ++i) slot_store(slot + ix.idx[i], v4[i]);
+  if constexpr (FINAL) arrive_global<M, RPL, MODE>(a, t, np, gr, p, v4, ho, lane);
+  else pend = Pending{t, np, p, false};
 }
 
 // Lookup tables staged in two halves around the first record's loads: the table words are
@@ -772,9 +907,7 @@ __device__ __forceinline__ void store_tables(unsigned char* lds, const TableWord
 }
 
 // The kernel: tables and the first record are fetched together, then each wave walks its range
-// of steps through a ring of record buffers (see below). Finishing a tile part never waits on
-// memory except in the part holding chunk 0 of a split tile, which is the last thing its wave
-// does.
+// of steps through a ring of record buffers (see below). No wave ever waits for another one.
 template <int KIND, int D, int M, int RPL, int MODE = 0>
 __global__ void __launch_bounds__(VALU_THREADS)
 __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(KArgs a) {
@@ -785,7 +918,8 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   static_assert(LDS_HO || MODE == 2, "only the tile variant may hand over through the workspace alone");
   __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes];
   __shared__ __align__(16) uint32_t pstage_all[MODE == 2 ? 1 : VALU_WPB * 64];
-  __shared__ uint64_t wg_slots[LDS_HO ? VALU_WPB * M * 16 : 1];
+  __shared__ __align__(16) unsigned char ho_raw[LDS_HO ? sizeof(WgHo<M>) : 4];
+  WgHo<M>* ho = (WgHo<M>*)ho_raw;
   constexpr int H = 16 / RPL;
   const int lane = threadIdx.x & 63;
   // wave-uniform by construction; readfirstlane keeps the schedule in SGPRs
@@ -818,7 +952,7 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   S::load(r0, a, t0, c0, h, vloc, lane);
   store_tables<KIND, D>(lds, tw, a);
   if constexpr (LDS_HO)
-    for (int i = threadIdx.x; i < VALU_WPB * M * 16; i += VALU_THREADS) wg_slots[i] = 0;
+    if (threadIdx.x < VALU_WPB) ho->cnt[threadIdx.x] = 0u;
   const uint32_t mask_off = a.t_bytes;
   __syncthreads();
   if (!active) return;                       // no barrier follows
@@ -834,12 +968,13 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   // computed. The loop runs over pairs of steps, one per buffer, with a single exit at the
   // bottom (an early exit would give the compiler a path back to the loop head with loads still
   // pending, and it would wait for them). The range's last step is peeled off: the tile parts
-  // that end inside the loop are whole tiles or later parts of split tiles, which only store,
-  // and the last part, which may be the part holding chunk 0 of a split tile, is finished after
-  // it, with the slots of the other parts fetched before the last step is computed.
+  // that end inside the loop are whole tiles or the range's first part, and the last part, which
+  // may be part 0 of a split tile, is finished after it, with the workspace slots of the other
+  // parts fetched before the last step is computed.
   const int nsteps = s_end - s_begin;
   const int npairs = (nsteps - 1) >> 1;
   SlotPre<M> pre;                            // filled only before the last step (see below)
+  Pending pend;
   int t = t0, c = c0;                        // position of step 2i
   for (int i = 0; i < npairs; ++i) {
     int t1 = t, c1 = c + 1;
@@ -849,7 +984,7 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
     }
     S::load(r1, a, t1, c1, h, vloc, lane);
     S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c1 == 0) emit_part<M, RPL, false, MODE, LDS_HO>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
+    if (c1 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, pre, false, ho, pend);
     int t2 = t1, c2 = c1 + 1;
     if (c2 == a.nc) {
       ++t2;
@@ -857,7 +992,7 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
     }
     S::load(r0, a, t2, c2, h, vloc, lane);   // step 2i + 2 <= nsteps - 1 exists
     S::compute(r1, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c2 == 0) emit_part<M, RPL, false, MODE, LDS_HO>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
+    if (c2 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, pre, false, ho, pend);
     t = t2;
     c = c2;
   }
@@ -871,16 +1006,30 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
     }
     S::load(r1, a, tf, cf, h, vloc, lane);
     S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (cf == 0) emit_part<M, RPL, false, MODE, LDS_HO>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, h, pre, false, wg_slots, 0);
+    if (cf == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, pre, false, ho, pend);
   }
   const int caf = tf == t0 ? c0 : 0;
-  const bool waits = caf == 0 && cf + 1 < a.nc;
-  const int np_final = waits ? wave_of_step(a, tf * a.nc + a.nc - 1) - g + 1 : 0;
-  if (waits) fetch_parts<M, LDS_HO>(pre, a, tf, np_final, 0, g, lane);
+  // part 0 of a tile that continues in another workgroup: prefetch the other parts' slots
+  bool have_pre = false;
+  if (caf == 0 && cf + 1 < a.nc) {
+    const int gl = wave_of_step(a, tf * a.nc + a.nc - 1);
+    if (!(LDS_HO && g / VALU_WPB == gl / VALU_WPB)) {
+      fetch_parts<M>(pre, a, tf, gl - g + 1, 0, lane);
+      have_pre = true;
+    }
+  }
   // one instance of the step code for the last step, whichever buffer holds it
   const typename S::R& rf = (nsteps - 2 * npairs == 2) ? r1 : r0;
   S::compute(rf, acc, lds, mask_off, pstage, lane, h, vloc);
-  emit_part<M, RPL, true, MODE, LDS_HO>(a, acc, tf, caf, cf + 1, g, lane, h, pre, waits, wg_slots, np_final);
+  emit_part<M, RPL, MODE, LDS_HO, true>(a, acc, tf, caf, cf + 1, g, lane, pre, have_pre, ho, pend);
+  // the follow-up of the range's first part, handed over inside the loop (its values are in its
+  // slot by now, so the ones passed here are not used)
+  if (pend.t >= 0) {
+    const float unused[PartIdx<M, RPL, MODE>::N4] = {};
+    const int gr = wave_of_step(a, pend.t * a.nc);
+    if (LDS_HO && pend.lds) finish_tile<M, RPL, MODE, false>(a, pend.t, pend.np, gr, pend.p, unused, nullptr, ho, lane);
+    else if (!pend.lds) arrive_global<M, RPL, MODE>(a, pend.t, pend.np, gr, pend.p, unused, ho, lane);
+  }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -919,15 +1068,17 @@ __global__ void __launch_bounds__(256) k_unpack(KArgs a, uint8_t* signs, uint16_
 }
 
 // ------------------------------------------------------------------------------------------
-// Prefill kernel (batch > 32): Y = X W^T on 16x16x32 MFMA tiles with the weights rebuilt once per
+// Prefill kernel (batch > 16): Y = X W^T on 16x16x32 MFMA tiles with the operands rebuilt once per
 // workgroup and k-chunk.
 //
 // A workgroup of PF_WAVES waves owns PF_TPW 16-row tiles per wave and MC batch rows (one grid
 // column per MC-row slice of X), and walks K in chunks of 128 (16 vector positions = one radius
 // group). Per chunk the X slice [MC][128] is staged in LDS (rows padded by 16 bytes against bank
 // conflicts); each lane rebuilds, for each of its tiles, row lane % 16 at positions 4i + lane / 16
-// (i = 0..3) as fp16(r * t) -- the operand layout of the batch 9..16 tile mode -- and every rebuilt
-// operand meets all MC / 16 column blocks of X, each X fragment serving both tiles. With ks > 1
+// (i = 0..3) as exact fp16 operands -- the signed direction t and the two halves of q * t, in the
+// operand layout of the batch 9..16 tile mode -- and every rebuilt operand meets all MC / 16
+// column blocks of X, each X fragment serving both tiles. Eq. 7 factors over the chunk's group:
+// the chunk adds offset * sum <t, x> + step * sum q <t, x> to each output. With ks > 1
 // the grid's third dimension splits K and the partial outputs are added in range order by
 // k_prefill_reduce. The order of every sum is fixed, so results are reproducible.
 // ------------------------------------------------------------------------------------------
@@ -966,25 +1117,32 @@ struct PfLds {
   static constexpr uint32_t bytes = x_off + nbuf * PfStage<KIND, MC>::bytes;
 };
 
+// One rebuilt MFMA operand of the prefill kernel: the signed direction t of row r at one position
+// (exact in fp16) and q * t split exactly into two fp16 words (see qt_split).
+struct PfOp {
+  uint4 t, hi, lo;
+};
+
 template <int KIND, int D>
-__device__ __forceinline__ uint4 pf_rebuild(const uint32_t ra, const uint32_t rb, const uint32_t rc, float lo,
-                                            float st, const unsigned char* lds, uint32_t mask_off, int r) {
-  uint4 tt;
+__device__ __forceinline__ PfOp pf_rebuild(const uint32_t ra, const uint32_t rb, const uint32_t rc,
+                                           const unsigned char* lds, uint32_t mask_off, int r) {
+  PfOp o;
   uint32_t q;
   if constexpr (IS_CB<KIND>) {
     uint32_t sg, z;
     decode_cb13(ra, r % 4, rb, r & 1, sg, z, q);
     if constexpr (KIND == SPH_KIND_CB13Q4) q |= ((rc >> r) & 1u) << 3;
-    tt = signed_dir_cb13(lds, mask_off, sg, z);
+    o.t = signed_dir_cb13(lds, mask_off, sg, z);
   } else {
     uint32_t l, hh, qx = 0;
     if constexpr (KIND == SPH_KIND_W2) qx = (rb >> (4 * (r / 2))) & 15u;
     if constexpr (KIND == SPH_KIND_NIB16Q2) qx = (rb >> (2 * r)) & 3u;
     if constexpr (KIND == SPH_KIND_NIB16Q8) qx = (rb >> (8 * (r % 4))) & 0xFFu;
     decode_nib<KIND, D>(ra, r & 1, qx, l, hh, q);
-    tt = signed_dir_nib<KIND, D>(lds, l, hh);
+    o.t = signed_dir_nib<KIND, D>(lds, l, hh);
   }
-  return scale_dir(tt, fmaf((float)q, st, lo));   // fp16(r * t), one rounding
+  qt_split(o.t, q, o.hi, o.lo);
+  return o;
 }
 
 // Load the PER 16-byte pieces of chunk c that this thread stages (X rows past the batch repeat
@@ -1085,7 +1243,7 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
     const uint32_t* sb = (const uint32_t*)(st + S::b_off);
     const uint16_t* sc = (const uint16_t*)(st + S::c_off);
     const uint32_t* sp = (const uint32_t*)(st + S::p_off);
-    auto rebuild_i = [&](int i, uint4 (&w)[PF_TPW]) {
+    auto rebuild_i = [&](int i, PfOp (&w)[PF_TPW]) {
 #pragma unroll
       for (int u = 0; u < PF_TPW; ++u) {
         const int lt = wave * PF_TPW + u, rec = lt * 16 + 4 * i + j;
@@ -1094,29 +1252,48 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
         if constexpr (S::BDW > 0) rb = sb[rec * S::BDW + bdw];
         uint32_t rc = 0u;
         if constexpr (S::CH > 0) rc = sc[rec];
-        const uint32_t pw = sp[lt * 16 + r];
-        w[u] = pf_rebuild<KIND, D>(ra, rb, rc, f16lo(pw), f16hi(pw), lds, a.t_bytes, r);
+        w[u] = pf_rebuild<KIND, D>(ra, rb, rc, lds, a.t_bytes, r);
       }
     };
-    // the operands of position group i + 1 are rebuilt before the multiplies of group i, so
-    // that their LDS round trips overlap the matrix-core work
-    uint4 wc[PF_TPW];
+    // A chunk is one radius group, so Eq. 7 factors over it: per (row, batch row) the chunk adds
+    // offset * sum <t, x> + step * sum q <t, x>, both sums formed by the MFMA from exact fp16
+    // operands. The operands of position group i + 1 are rebuilt before the multiplies of group i,
+    // so that their LDS round trips overlap the matrix-core work.
+    f32x4 s0[PF_TPW][NB], s1[PF_TPW][NB];
+#pragma unroll
+    for (int u = 0; u < PF_TPW; ++u)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) s0[u][nb] = s1[u][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    PfOp wc[PF_TPW];
     rebuild_i(0, wc);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      uint4 wn[PF_TPW];
+      PfOp wn[PF_TPW];
       if (i + 1 < 4) rebuild_i(i + 1, wn);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        const uint4 xb = *(const uint4*)(st + (16 * nb + r) * PF_XROW + (4 * i + j) * 16);
+        const f16x8 xb = __builtin_bit_cast(f16x8, *(const uint4*)(st + (16 * nb + r) * PF_XROW + (4 * i + j) * 16));
 #pragma unroll
-        for (int u = 0; u < PF_TPW; ++u)
-          acc[u][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wc[u]),
-                                                              __builtin_bit_cast(f16x8, xb), acc[u][nb], 0, 0, 0);
+        for (int u = 0; u < PF_TPW; ++u) {
+          s0[u][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wc[u].t), xb, s0[u][nb], 0, 0, 0);
+          s1[u][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wc[u].hi), xb, s1[u][nb], 0, 0, 0);
+          s1[u][nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, wc[u].lo), xb, s1[u][nb], 0, 0, 0);
+        }
       }
       if (i + 1 < 4)
 #pragma unroll
         for (int u = 0; u < PF_TPW; ++u) wc[u] = wn[u];
+    }
+    // fold the chunk's sums in with the offset and step of rows 4 * (lane / 16) + e
+#pragma unroll
+    for (int u = 0; u < PF_TPW; ++u) {
+      const uint4 pw = *(const uint4*)(sp + (wave * PF_TPW + u) * 16 + 4 * j);
+      const uint32_t pe[4] = {pw.x, pw.y, pw.z, pw.w};
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          acc[u][nb][e] = fmaf(f16hi(pe[e]), s1[u][nb][e], fmaf(f16lo(pe[e]), s0[u][nb][e], acc[u][nb][e]));
     }
   }
   // D[row][col] of a 16x16 block: lane holds col lane % 16 (batch row) and rows 4 * (lane / 16) + e
@@ -1164,8 +1341,8 @@ __global__ void __launch_bounds__(256) k_prefill_reduce(KArgs a) {
 // wave reduction. The 4-D signed directions come from a 64-entry sign-folded table in LDS; a 16-D
 // codebook entry is read from memory (the 512 KiB codebook stays in L2) and its signs applied by
 // XOR on the fp16 sign bits. Batch 1 forms exact fp16 products with fp32 sums and applies the
-// radius in fp32, as the 8-D vector-ALU mode does; larger batches rebuild the lane's 64 weights
-// once as fp16(r * t) and reuse them for every activation row.
+// radius in fp32, as the 8-D vector-ALU mode does; larger batches decode the lane's vectors once
+// and reuse them for every activation row with the same exact-product arithmetic.
 // ------------------------------------------------------------------------------------------
 constexpr int RV_WAVES = 4;
 
@@ -1236,29 +1413,36 @@ __global__ void __launch_bounds__(64 * RV_WAVES) k_gemm_rowvec(KArgs a) {
         acc[0] = fmaf(r, d, acc[0]);
       }
     } else {
-      uint32_t w[32];   // the lane's 64 weights as fp16(r * t)
+      // the lane's vectors once (signed directions exact in fp16, radii in fp32), then per batch
+      // row the exact-product dots of each vector, scaled by its radius in fp32
+      float rr[NVL];
+      uint32_t tw[NVL][TW];
 #pragma unroll
       for (int u = 0; u < NVL; ++u) {
-        float r;
         uint32_t t[8];
-        rv_vector<KIND>(a, tab, f, u, bw, vin, lo, st, r, t);
+        rv_vector<KIND>(a, tab, f, u, bw, vin, lo, st, rr[u], t);
 #pragma unroll
-        for (int i = 0; i < TW; ++i) w[u * TW + i] = scale_h2(t[i], r);
+        for (int i = 0; i < TW; ++i) tw[u][i] = t[i];
       }
 #pragma unroll
       for (int b = 0; b < MB; ++b) {
         if (b < a.m) {
           const uint4* xp = (const uint4*)(a.x + (int64_t)b * a.ldx + kw);
-          float d = 0.0f;
+          uint32_t xw[32];
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
             const uint4 xv = xp[i];
-            d = __builtin_amdgcn_fdot2(as_h2(w[4 * i]), as_h2(xv.x), d, false);
-            d = __builtin_amdgcn_fdot2(as_h2(w[4 * i + 1]), as_h2(xv.y), d, false);
-            d = __builtin_amdgcn_fdot2(as_h2(w[4 * i + 2]), as_h2(xv.z), d, false);
-            d = __builtin_amdgcn_fdot2(as_h2(w[4 * i + 3]), as_h2(xv.w), d, false);
+            xw[4 * i] = xv.x; xw[4 * i + 1] = xv.y; xw[4 * i + 2] = xv.z; xw[4 * i + 3] = xv.w;
           }
-          acc[b] += d;
+          float s = acc[b];
+#pragma unroll
+          for (int u = 0; u < NVL; ++u) {
+            float d = 0.0f;
+#pragma unroll
+            for (int i = 0; i < TW; ++i) d = __builtin_amdgcn_fdot2(as_h2(tw[u][i]), as_h2(xw[u * TW + i]), d, false);
+            s = fmaf(rr[u], d, s);
+          }
+          acc[b] = s;
         }
       }
     }
@@ -1307,6 +1491,7 @@ struct Launch {
   int grid;
   int nc, wg_tiles, wq, wr, pmax, ts;
   size_t ws_bytes;    // workspace the launch needs
+  size_t cnt_off;     // offset of the split-tile arrival counters in it
 };
 
 KArgs make_args(const sph_weights* w) {
@@ -1372,19 +1557,12 @@ const void* pick(int D, int V, int M, int rpl1) {
 template <int KIND, int D>
 const void* prefill_fn_mc(int mc) {
   if (mc == 32) return (const void*)k_gemm_prefill<KIND, D, 32>;
-  if constexpr (IS_CB<KIND>) {
-    return (const void*)k_gemm_prefill<KIND, D, 64>;
-  } else {
-    if (mc == 64) return (const void*)k_gemm_prefill<KIND, D, 64>;
-    return (const void*)k_gemm_prefill<KIND, D, 128>;
-  }
+  return (const void*)k_gemm_prefill<KIND, D, 64>;
 }
 
-// Batch rows per workgroup: 32 for batches 17..32, 128 for the nibble kinds above 64, else 64.
-int prefill_mc(int D, int V, int64_t m) {
-  if (m <= 32) return 32;
-  return (sph_is_codebook_kind(sph_kind_of(D, V)) || m <= 64) ? 64 : 128;
-}
+// Batch rows per workgroup: 32 for batches 17..32, else 64 (the two fp32 sums of the factored
+// product double the accumulators, which 128 rows would not leave room for).
+int prefill_mc(int, int, int64_t m) { return m <= 32 ? 32 : 64; }
 
 const void* prefill_fn(int D, int V, int mc) {
   switch (sph_kind_of(D, V)) {
@@ -1524,7 +1702,9 @@ Launch plan(const sph_weights* w, int m) {
       // nc / that + 2 ranges
       const int64_t lmin = std::max<int64_t>(1, ts / (gB * wpb));
       L.pmax = (int)(nc / lmin + 2);
-      L.ws_bytes = (size_t)nt * L.pmax * M * 16 * 8;
+      // tagged slots [nt][pmax][M][16], then one arrival counter per tile
+      L.cnt_off = ((size_t)nt * L.pmax * M * 16 * 8 + 255) / 256 * 256;
+      L.ws_bytes = L.cnt_off + ((size_t)nt * 4 + 255) / 256 * 256;
     }
   }
   return L;
@@ -1721,7 +1901,10 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
   a.wr = L.wr;
   a.pmax = L.pmax;
   a.ts = L.ts;
-  if (L.ws_bytes > 0) a.ws_slot = (uint64_t*)d_ws;
+  if (L.ws_bytes > 0) {
+    a.ws_slot = (uint64_t*)d_ws;
+    a.ws_cnt = (uint32_t*)((char*)d_ws + L.cnt_off);
+  }
   a.x = (const uint16_t*)d_x;
   a.ldx = ldx;
   a.y = d_y;

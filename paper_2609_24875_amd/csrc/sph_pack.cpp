@@ -87,8 +87,11 @@ int sph_host_check_codes(const sph_format* fmt, int64_t n, int64_t k, const uint
     if (!f16_finite(gmin[i])) return SPH_ERR_BAD_VALUE;
     if (!f16_finite(gstep[i]) || f16_sign(gstep[i])) return SPH_ERR_BAD_VALUE;
   }
+  // Codebook entries are coordinates of non-negative unit directions (Sec. 3.1), so they lie in
+  // [0, 1] up to rounding; entries above 2 (fp16 0x4000) are rejected. The bound keeps a level
+  // times an entry (at most 255 * 2) far inside the fp16 range of the matrix-core operands.
   for (int64_t i = 0; i < ((int64_t)vec << fmt->dir_bits); ++i)
-    if (!f16_finite(codebook[i]) || f16_sign(codebook[i])) return SPH_ERR_BAD_VALUE;
+    if (!f16_finite(codebook[i]) || f16_sign(codebook[i]) || codebook[i] > 0x4000) return SPH_ERR_BAD_VALUE;
   return SPH_OK;
 }
 

@@ -94,6 +94,44 @@ def row_scale_group_params(n: int, k: int, radius_bits: int, g: np.random.Genera
     return f16_bits(off), f16_bits(step)
 
 
+def varied_group_params(n: int, k: int, radius_bits: int, g: np.random.Generator):
+    """An independent (offset, step) pair for every group of every row, so that neighbouring
+    groups of one row never share parameters: offsets of either sign (about a quarter negative),
+    about one step in eight exactly zero, and magnitudes spread over eight binary orders
+    (2^-4 ... 2^3 times a U(0.5, 2) mantissa), all finite fp16."""
+    ng = k // GROUP
+    mag = g.uniform(0.5, 2.0, (n, ng)) * 2.0 ** g.integers(-4, 4, (n, ng))
+    off = np.where(g.random((n, ng)) < 0.25, -1.0, 1.0) * mag
+    step = g.uniform(0.5, 2.0, (n, ng)) * 2.0 ** g.integers(-4, 4, (n, ng)) / 2.0 ** radius_bits
+    step[g.random((n, ng)) < 0.125] = 0.0
+    return f16_bits(off), f16_bits(step)
+
+
+def extreme_group_params(n: int, k: int, radius_bits: int, g: np.random.Generator):
+    """Group parameters at the edges of fp16: rows cycle through three kinds.
+
+    * row % 3 == 0: radii beyond the fp16 range, offsets in [2^14, 2^15.9] and steps in
+      [2^10, 2^15], so min + q * step reaches far past 65504;
+    * row % 3 == 1: radii among the fp16 subnormals and smallest normals (offsets and steps in
+      [2^-24, 2^-13]);
+    * row % 3 == 2: huge and ordinary groups alternating inside the row.
+    """
+    ng = k // GROUP
+    big_off = 2.0 ** g.uniform(14.0, 15.9, (n, ng))
+    big_step = 2.0 ** g.uniform(10.0, 15.0, (n, ng))
+    tiny_off = 2.0 ** g.uniform(-24.0, -13.0, (n, ng))
+    tiny_step = 2.0 ** g.uniform(-24.0, -13.0, (n, ng))
+    mid_off = g.uniform(0.01, 0.1, (n, ng))
+    mid_step = g.uniform(0.001, 0.01, (n, ng))
+    kind = (np.arange(n) % 3)[:, None] * np.ones((1, ng), dtype=np.int64)
+    alt = (np.arange(ng) % 2)[None, :] == 0
+    use_big = (kind == 0) | ((kind == 2) & alt)
+    off = np.where(use_big, big_off, np.where(kind == 1, tiny_off, mid_off))
+    step = np.where(use_big, big_step, np.where(kind == 1, tiny_step, mid_step))
+    off = np.where(g.random((n, ng)) < 0.25, -off, off)
+    return f16_bits(off), f16_bits(step)
+
+
 def outlier_gaussian_weights(n: int, k: int, g: np.random.Generator, sigma: float = 0.02,
                              p: float = 1e-3, scale: float = 20.0, nu: float = 3.0) -> np.ndarray:
     """N(0, sigma^2) weights; each entry is replaced with probability p by scale*sigma*t_nu."""

@@ -134,6 +134,11 @@ def test_pack_validation_errors():
     bcb = cb.copy()
     bcb[2, 3] = 0x8000 | bcb[2, 3]             # negative entry
     assert _pack_status(codes, bcb) == 5
+    bcb = cb.copy()
+    bcb[1, 0] = 0x4001                         # just above 2: not a unit direction's coordinate
+    assert _pack_status(codes, bcb) == 5
+    bcb[1, 0] = 0x4000                         # exactly 2 passes validation (then the size check)
+    assert _pack_status(codes, bcb, nbytes=100) == 6
     assert _pack_status(codes, cb, nbytes=100) == 6
     assert _pack_status(codes, cb, buf=0x10001) == 2
     assert _pack_status(codes, cb, buf=0) == 1

@@ -1761,7 +1761,20 @@ sph_status launch(const Launch& L, const KArgs& a, hipStream_t s) {
   return SPH_OK;
 }
 
+// Argument checks of sph_gemm_small (host only, before any HIP call).
+sph_status check_small_args(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, const void* d_y,
+                            int64_t ldy, sph_dtype y_dtype) {
+  if (!w || !d_x || !d_y) return SPH_ERR_NULL;
+  if (!valid_desc(w)) return SPH_ERR_BAD_DESCRIPTOR;
+  if (m < 1 || m > 32) return SPH_ERR_SHAPE;
+  if (ldx < w->k || ldy < w->n || ldx % 8 != 0) return SPH_ERR_SHAPE;
+  if (y_dtype != SPH_F16 && y_dtype != SPH_F32) return SPH_ERR_SHAPE;
+  if ((uintptr_t)d_x % 16 != 0 || (uintptr_t)d_y % 4 != 0) return SPH_ERR_SHAPE;
+  return SPH_OK;
+}
+
 }  // namespace
+
 
 // ------------------------------------------------------------------------------------------
 // C ABI
@@ -1862,12 +1875,8 @@ sph_status sph_gemm(const sph_weights* w, const void* d_x, int64_t m, int64_t ld
 
 sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y,
                           int64_t ldy, sph_dtype y_dtype, void* d_ws, size_t ws_bytes, void* stream) {
-  if (!w || !d_x || !d_y) return SPH_ERR_NULL;
-  if (!valid_desc(w)) return SPH_ERR_BAD_DESCRIPTOR;
-  if (m < 1 || m > 32) return SPH_ERR_SHAPE;
-  if (ldx < w->k || ldy < w->n || ldx % 8 != 0) return SPH_ERR_SHAPE;
-  if (y_dtype != SPH_F16 && y_dtype != SPH_F32) return SPH_ERR_SHAPE;
-  if ((uintptr_t)d_x % 16 != 0 || (uintptr_t)d_y % 4 != 0) return SPH_ERR_SHAPE;
+  const sph_status st = check_small_args(w, d_x, m, ldx, d_y, ldy, y_dtype);
+  if (st != SPH_OK) return st;
   if (sph_is_rowvec_kind(fmt_kind(w))) {
     KArgs a = make_args(w);
     a.x = (const uint16_t*)d_x;

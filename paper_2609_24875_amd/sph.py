@@ -191,46 +191,79 @@ def workspace_bytes(w: SphWeights, m: int) -> int:
     return out.value
 
 
-def _workspace(w: SphWeights, m: int, device):
-    """Zero-filled workspace for (w, m), allocated once and kept with the weights (the library
-    leaves it zero-filled after every call)."""
+def _workspace(w: SphWeights, m: int, device, stream=None):
+    """Zero-filled workspace for (w, m) on one stream, allocated once and kept with the weights
+    (the library leaves it zero-filled after every call). Calls on different streams may run
+    concurrently, so each stream gets its own."""
     import torch
     nb = workspace_bytes(w, m)
     if nb == 0:
         return None, 0
-    ws = w.workspaces.get(m)
+    key = (m, _stream_handle(stream))
+    ws = w.workspaces.get(key)
     if ws is None or ws.numel() < nb:
         ws = torch.zeros(nb, dtype=torch.uint8, device=device)
-        w.workspaces[m] = ws
+        w.workspaces[key] = ws
     return ws, nb
+
+
+def _check_x(w: SphWeights, x, batched: bool):
+    """x must be a device fp16 tensor on the weights' device with k columns, contiguous along k:
+    [k] for gemv, [m][k] (any row stride) for the batched calls."""
+    import torch
+    if not isinstance(x, torch.Tensor) or x.dtype != torch.float16:
+        raise TypeError("x must be a torch.float16 tensor")
+    if x.device != w.buffer.device:
+        raise ValueError(f"x is on {x.device}, the weights on {w.buffer.device}")
+    if x.dim() != (2 if batched else 1) or x.shape[-1] != w.k or (x.numel() > 0 and x.stride(-1) != 1):
+        raise ValueError(f"x must be {'[m][' if batched else '['}{w.k}] with unit stride along k, "
+                         f"got shape {tuple(x.shape)} and strides {tuple(x.stride())}")
+
+
+def _out(w: SphWeights, x, m: int, out, out_dtype, batched: bool):
+    """The output tensor: a new one, or ``out`` checked to be fp16 or fp32 on x's device, [n] for
+    gemv or [m][n] (any row stride) for the batched calls, contiguous along n."""
+    import torch
+    if out is None:
+        shape = (m, w.n) if batched else (w.n,)
+        return torch.empty(shape, dtype=out_dtype or torch.float32, device=x.device)
+    if out.dtype not in (torch.float16, torch.float32):
+        raise TypeError("out must be torch.float16 or torch.float32")
+    if out_dtype is not None and out.dtype != out_dtype:
+        raise TypeError("out_dtype differs from out.dtype")
+    if out.device != x.device:
+        raise ValueError(f"out is on {out.device}, x on {x.device}")
+    want = (m, w.n) if batched else (w.n,)
+    if tuple(out.shape) != want or out.stride(-1) != 1:
+        raise ValueError(f"out must have shape {want} with unit stride along n, got "
+                         f"{tuple(out.shape)} and strides {tuple(out.stride())}")
+    return out
+
+
+def _dtype_code(t) -> int:
+    import torch
+    return SPH_F16 if t.dtype == torch.float16 else SPH_F32
 
 
 def gemv(w: SphWeights, x, out=None, out_dtype=None, stream=None):
     """y = W^ x for a device fp16 vector x[k] (sph_gemv)."""
-    import torch
-    out_dtype = out_dtype or torch.float32
-    if out is None:
-        out = torch.empty(w.n, dtype=out_dtype, device=x.device)
-    ws, nb = _workspace(w, 1, x.device)
-    st = load_library().sph_gemv(ctypes.byref(w.desc), x.data_ptr(), out.data_ptr(),
-                                 SPH_F16 if out.dtype == torch.float16 else SPH_F32,
-                                 ws.data_ptr() if ws is not None else None, nb,
-                                 _stream_handle(stream))
+    _check_x(w, x, batched=False)
+    out = _out(w, x, 1, out, out_dtype, batched=False)
+    ws, nb = _workspace(w, 1, x.device, stream)
+    st = load_library().sph_gemv(ctypes.byref(w.desc), x.data_ptr(), out.data_ptr(), _dtype_code(out),
+                                 ws.data_ptr() if ws is not None else None, nb, _stream_handle(stream))
     _check(st, "sph_gemv")
     return out
 
 
 def gemm_small(w: SphWeights, x, out=None, out_dtype=None, stream=None):
     """Y = X W^T for device fp16 X[m][k], 1 <= m <= 32 (sph_gemm_small)."""
-    import torch
-    out_dtype = out_dtype or torch.float32
+    _check_x(w, x, batched=True)
     m = x.shape[0]
-    if out is None:
-        out = torch.empty((m, w.n), dtype=out_dtype, device=x.device)
-    ws, nb = _workspace(w, m, x.device)
+    out = _out(w, x, m, out, out_dtype, batched=True)
+    ws, nb = _workspace(w, m, x.device, stream)
     st = load_library().sph_gemm_small(ctypes.byref(w.desc), x.data_ptr(), m, x.stride(0),
-                                       out.data_ptr(), out.stride(0),
-                                       SPH_F16 if out.dtype == torch.float16 else SPH_F32,
+                                       out.data_ptr(), out.stride(0), _dtype_code(out),
                                        ws.data_ptr() if ws is not None else None, nb,
                                        _stream_handle(stream))
     _check(st, "sph_gemm_small")
@@ -240,14 +273,12 @@ def gemm_small(w: SphWeights, x, out=None, out_dtype=None, stream=None):
 def gemm(w: SphWeights, x, out=None, out_dtype=None, stream=None):
     """Y = X W^T for device fp16 X[m][k], any 1 <= m <= 65536 (sph_gemm): the matrix-core prefill
     kernel above m = 32."""
-    import torch
-    out_dtype = out_dtype or torch.float32
+    _check_x(w, x, batched=True)
     m = x.shape[0]
-    if out is None:
-        out = torch.empty((m, w.n), dtype=out_dtype, device=x.device)
-    ws, nb = _workspace(w, m, x.device)
+    out = _out(w, x, m, out, out_dtype, batched=True)
+    ws, nb = _workspace(w, m, x.device, stream)
     st = load_library().sph_gemm(ctypes.byref(w.desc), x.data_ptr(), m, x.stride(0), out.data_ptr(),
-                                 out.stride(0), SPH_F16 if out.dtype == torch.float16 else SPH_F32,
+                                 out.stride(0), _dtype_code(out),
                                  ws.data_ptr() if ws is not None else None, nb, _stream_handle(stream))
     _check(st, "sph_gemm")
     return out

@@ -294,3 +294,4 @@ def test_vector_size_pack_validation():
     f4 = B.make_format(2, 3, 4)
     assert lib.sph_encode(ctypes.byref(f4), 16, 128, 0x10000, 128, 0x20000, 0x30000, 0x40000, 0x50000,
                           0x60000, 0x70000, None) == 3     # the encoder is 8-D only
+

@@ -174,6 +174,49 @@ def test_deterministic():
     assert torch.equal(a, b)
 
 
+def test_concurrent_streams():
+    """Two decode calls whose split tiles meet in the global workspace, launched back to back on
+    two streams so that their workgroups share the GPU, each with its own workspace: both match
+    the oracle and the results of the same calls made one after the other."""
+    cases = []
+    for i, (fmt, n, k) in enumerate((("W2", 5120, 25600), ("W3", 4096, 12288))):
+        D, V, codes, cb = uniform_case(fmt, n, k, 50 + i)
+        w = pkg.pack(D, V, codes, cb, device=DEV)
+        x = synth.activations(1, k, synth.rng(50 + i, synth.STREAM_X))
+        cases.append((w, codes, cb, x, to_dev_f16(x)[0]))
+    serial = [pkg.gemv(w, xd).cpu().numpy() for w, _, _, _, xd in cases]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [torch.empty(c[0].n, dtype=torch.float32, device=DEV) for c in cases]
+    torch.cuda.synchronize()
+    for _ in range(20):
+        for (w, _, _, _, xd), s, o in zip(cases, streams, outs):
+            with torch.cuda.stream(s):
+                pkg.gemv(w, xd, out=o, stream=s)
+    torch.cuda.synchronize()
+    for (w, codes, cb, x, _), o, ref_bits in zip(cases, outs, serial):
+        y = o.cpu().numpy()
+        assert np.array_equal(y, ref_bits)
+        assert O.rel_err(y, O.gemv(codes, cb, x)) <= TOL
+
+
+def test_bad_arguments_raise():
+    D, V, codes, cb = uniform_case("W2", 16, 128, 8)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = torch.zeros((2, 128), dtype=torch.float16, device=DEV)
+    with pytest.raises(TypeError):
+        pkg.gemm_small(w, x.float())                                  # fp32 activations
+    with pytest.raises(ValueError):
+        pkg.gemm_small(w, torch.zeros((2, 64), dtype=torch.float16, device=DEV))  # short rows
+    with pytest.raises(ValueError):
+        pkg.gemv(w, torch.zeros(256, dtype=torch.float16, device=DEV)[::2])        # strided x
+    with pytest.raises(TypeError):
+        pkg.gemm_small(w, x, out=torch.empty((2, 16), dtype=torch.bfloat16, device=DEV))
+    with pytest.raises(ValueError):
+        pkg.gemm_small(w, x, out=torch.empty((2, 8), dtype=torch.float32, device=DEV))
+    with pytest.raises(ValueError):
+        pkg.gemm_small(w, x, out=torch.empty((16, 2), dtype=torch.float32, device=DEV).t())
+
+
 def test_bad_batch_raises():
     D, V, codes, cb = uniform_case("W2", 16, 128, 8)
     w = pkg.pack(D, V, codes, cb, device=DEV)
@@ -474,9 +517,9 @@ def test_batch_workspace_left_zero(m):
     w = pkg.pack(D, V, codes, cb, device=DEV)
     x = synth.activations(m, 4096, synth.rng(15, m, synth.STREAM_X))
     y1 = pkg.gemm(w, to_dev_f16(x)).cpu().numpy()
-    ws = w.workspaces.get(m)
-    if ws is not None:
-        assert int(torch.count_nonzero(ws)) == 0
+    for (mm, _stream), ws in w.workspaces.items():
+        if mm == m:
+            assert int(torch.count_nonzero(ws)) == 0
     y2 = pkg.gemm(w, to_dev_f16(x)).cpu().numpy()
     assert np.array_equal(y1, y2)
     assert O.rel_err(y1, O.gemm(codes, cb, x)) <= TOL

@@ -136,6 +136,20 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
 sph_status sph_gemm(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y, int64_t ldy,
                     sph_dtype y_dtype, void* d_ws, size_t ws_bytes, void* stream);
 
+/* sph_gemm_small without a caller workspace, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid allocation). Same arguments,
+ * arithmetic, results (bitwise) and errors as sph_gemm_small, with d_ws/ws_bytes replaced by a
+ * fixed array of SPH_NOALLOC_SCRATCH_BYTES in device memory that the library's code object holds
+ * (one per GPU it runs on, kept until the process ends). A call whose sph_workspace_bytes exceeds
+ * that size returns SPH_ERR_BUFFER_TOO_SMALL before any HIP call. The first call on a device looks
+ * up the array's address and clears it with a kernel on `stream`; every call leaves it zero-filled
+ * again. Every call on one GPU shares that GPU's array: calls that may overlap on one GPU (other
+ * streams, other threads) race and must not be made. Allocates nothing, on the host or the device.
+ * Asynchronous on `stream`. */
+#define SPH_NOALLOC_SCRATCH_BYTES (16u << 20)
+sph_status sph_gemm_small_noalloc(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y,
+                                  int64_t ldy, sph_dtype y_dtype, void* stream);
+
 /* Device workspace needed by sph_gemv (m = 1), sph_gemm_small or sph_gemm for this matrix and
  * batch (1 <= m <= 65536) on the current device (0 when the call needs none; d_ws may then be
  * NULL). For m <= 16 it holds the partial sums of 16-row tiles whose K range is split between

@@ -23,6 +23,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include <type_traits>
 #include <cstring>
 #include <vector>
@@ -1775,6 +1776,51 @@ sph_status check_small_args(const sph_weights* w, const void* d_x, int64_t m, in
 
 }  // namespace
 
+// ------------------------------------------------------------------------------------------
+// Scratch memory of sph_gemm_small_noalloc: a fixed-size device array that takes the place of the
+// caller's workspace, for callers that cannot allocate. The loader gives every GPU that runs the
+// library its own copy, held until the process ends. Host code never passes the array's name to
+// a kernel (on the host it is a stand-in, not a device address): the device address of this GPU's
+// copy is looked up once per device and kept.
+// ------------------------------------------------------------------------------------------
+#define SPH_SCRATCH_BYTES ((size_t)SPH_NOALLOC_SCRATCH_BYTES)
+static __device__ __align__(256) unsigned char scratch[SPH_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch[kMaxDevices];
+std::mutex g_scratch_mu;
+
+__global__ void __launch_bounds__(256) k_zero16(uint4* p, size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (size_t)gridDim.x * 256)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+// The current device's copy of `scratch`: on the first call on a device, its address (with that
+// device current) and one clearing pass on `s` (a kernel, not a memset, so that it may be
+// captured into a graph); the calls that use it leave it zero-filled again.
+sph_status scratch_of_current_device(hipStream_t s, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return SPH_ERR_HIP;
+  void* p = g_scratch[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch[dev].load(std::memory_order_acquire);
+    if (!p) {
+      void* q = nullptr;
+      if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) return SPH_ERR_HIP;
+      hipLaunchKernelGGL(k_zero16, dim3(1024), dim3(256), 0, s, (uint4*)q, SPH_SCRATCH_BYTES / 16);
+      if (hipGetLastError() != hipSuccess) return SPH_ERR_HIP;
+      g_scratch[dev].store(q, std::memory_order_release);
+      p = q;
+    }
+  }
+  *out = p;
+  return SPH_OK;
+}
+
+}  // namespace
 
 // ------------------------------------------------------------------------------------------
 // C ABI
@@ -1927,6 +1973,21 @@ sph_status sph_gemv(const sph_weights* w, const void* d_x, void* d_y, sph_dtype 
                     size_t ws_bytes, void* stream) {
   if (!w) return SPH_ERR_NULL;
   return sph_gemm_small(w, d_x, 1, w->k, d_y, w->n, y_dtype, d_ws, ws_bytes, stream);
+}
+
+sph_status sph_gemm_small_noalloc(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y,
+                                  int64_t ldy, sph_dtype y_dtype, void* stream) {
+  sph_status st = check_small_args(w, d_x, m, ldx, d_y, ldy, y_dtype);
+  if (st != SPH_OK) return st;
+  size_t need = 0;
+  st = sph_workspace_bytes(w, m, &need);
+  if (st != SPH_OK) return st;
+  if (need > SPH_SCRATCH_BYTES) return SPH_ERR_BUFFER_TOO_SMALL;
+  if (need == 0) return sph_gemm_small(w, d_x, m, ldx, d_y, ldy, y_dtype, nullptr, 0, stream);
+  void* ws = nullptr;
+  st = scratch_of_current_device((hipStream_t)stream, &ws);
+  if (st != SPH_OK) return st;
+  return sph_gemm_small(w, d_x, m, ldx, d_y, ldy, y_dtype, ws, need, stream);
 }
 
 sph_status sph_unpack(const sph_weights* w, uint8_t* d_signs, uint16_t* d_dir_idx, uint8_t* d_radius_code,

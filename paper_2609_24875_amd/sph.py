@@ -24,8 +24,8 @@ STATUS = {
 }
 
 # Every symbol include/sph.h declares.
-EXPORTS = ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small", "sph_gemm",
-           "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
+EXPORTS = ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
+           "sph_gemm_small_noalloc", "sph_gemm", "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
            "sph_kmeans_codebook", "sph_angular_codebook", "sph_angular_codebook_backward",
            "sph_angular_logits", "sph_direction_groups", "sph_fake_quant_init_rho",
            "sph_fake_quant_forward", "sph_fake_quant_backward_workspace_bytes",
@@ -34,6 +34,10 @@ EXPORTS = ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
 FORMATS = {
     "W2": (6, 4), "W3": (13, 3), "W2_cfg": (4, 4), "W3_cfg": (8, 8), "W2_16": (6, 2),
 }
+
+
+# Size of the library's scratch array used by sph_gemm_small_noalloc (SPH_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 class SphLibraryMissing(RuntimeError):
@@ -76,6 +80,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sph_gemv.argtypes = [pw, P, P, I32, P, SZ, P]
     lib.sph_gemm_small.argtypes = [pw, P, I64, I64, P, I64, I32, P, SZ, P]
     lib.sph_gemm.argtypes = [pw, P, I64, I64, P, I64, I32, P, SZ, P]
+    lib.sph_gemm_small_noalloc.argtypes = [pw, P, I64, I64, P, I64, I32, P]
     lib.sph_workspace_bytes.argtypes = [pw, I64, ctypes.POINTER(SZ)]
     lib.sph_unpack.argtypes = [pw, P, P, P, P]
     lib.sph_encode.argtypes = [pf, I64, I64, P, I64, P, P, P, P, P, P, P]
@@ -95,8 +100,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sph_format_supported.restype = I32
     lib.sph_status_str.argtypes = [I32]
     lib.sph_status_str.restype = ctypes.c_char_p
-    for name in ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small", "sph_gemm",
-                 "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
+    for name in ("sph_packed_bytes", "sph_pack_weights", "sph_gemv", "sph_gemm_small",
+                 "sph_gemm_small_noalloc", "sph_gemm", "sph_workspace_bytes", "sph_unpack", "sph_encode", "sph_kmeans_workspace_bytes",
                  "sph_kmeans_codebook", "sph_angular_codebook", "sph_angular_codebook_backward",
                  "sph_angular_logits", "sph_direction_groups", "sph_fake_quant_init_rho",
                  "sph_fake_quant_forward", "sph_fake_quant_backward_workspace_bytes",
@@ -267,6 +272,20 @@ def gemm_small(w: SphWeights, x, out=None, out_dtype=None, stream=None):
                                        ws.data_ptr() if ws is not None else None, nb,
                                        _stream_handle(stream))
     _check(st, "sph_gemm_small")
+    return out
+
+
+def gemm_small_noalloc(w: SphWeights, x, out, stream=None):
+    """Y = X W^T like ``gemm_small``, through sph_gemm_small_noalloc: no workspace, no allocation
+    (``out`` must be given). Calls on one GPU share the library's scratch array and must not
+    overlap."""
+    _check_x(w, x, batched=True)
+    m = x.shape[0]
+    out = _out(w, x, m, out, None, batched=True)
+    st = load_library().sph_gemm_small_noalloc(ctypes.byref(w.desc), x.data_ptr(), m, x.stride(0),
+                                               out.data_ptr(), out.stride(0), _dtype_code(out),
+                                               _stream_handle(stream))
+    _check(st, "sph_gemm_small_noalloc")
     return out
 
 

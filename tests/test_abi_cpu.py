@@ -295,3 +295,17 @@ def test_vector_size_pack_validation():
     assert lib.sph_encode(ctypes.byref(f4), 16, 128, 0x10000, 128, 0x20000, 0x30000, 0x40000, 0x50000,
                           0x60000, 0x70000, None) == 3     # the encoder is 8-D only
 
+
+def test_noalloc_scratch_size_matches_header():
+    with open(os.path.join(os.path.dirname(__file__), "..", "include", "sph.h")) as f:
+        m = re.search(r"#define SPH_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", f.read())
+    assert m and int(m.group(1)) << int(m.group(2)) == B.NOALLOC_SCRATCH_BYTES
+
+
+@needs_lib
+def test_noalloc_rejects_bad_arguments_before_any_hip_call():
+    lib = pkg.load_library()
+    w = B.CWeights()                           # never filled by sph_pack_weights
+    assert lib.sph_gemm_small_noalloc(ctypes.byref(w), 0x10000, 4, 256, 0x20000, 256, 1, None) == 8
+    assert lib.sph_gemm_small_noalloc(None, 0x10000, 4, 256, 0x20000, 256, 1, None) == 1
+    assert lib.sph_gemm_small_noalloc(ctypes.byref(w), None, 4, 256, 0x20000, 256, 1, None) == 1

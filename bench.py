@@ -74,6 +74,11 @@ def parse():
     ap.add_argument("--path", default="decode", choices=("decode", "encode", "train"),
                     help="decode: the default benchmark; encode: device encoder and k-means codebook; "
                          "train: pseudo-quantised weight rebuild and its straight-through backward")
+    ap.add_argument("--shapes", default="",
+                    help="time only these NxK shapes (comma-separated) at --batch, each rotated over "
+                         ">= 512 MB of packed copies")
+    ap.add_argument("--no-target-shapes", action="store_true",
+                    help="skip the batch-1 W2 12288x4096 / 4096x12288 launches in the decode line")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (HBM counter calibration)")
     return ap.parse_args()
@@ -390,6 +395,8 @@ def main():
         return encode_main(args)
     if args.path == "train":
         return train_main(args)
+    if args.shapes:
+        return shapes_main(args)
     import torch
 
     import paper_2609_24875_amd as pkg
@@ -521,6 +528,11 @@ def main():
         per_shape[f"{label} {n}x{k}"] = {"us": round(us, 3),
                                          "GB/s": round(copies[0].nbytes / (us * 1e-6) / 1e9, 1)}
         del gs
+    # the batch-1 W2 shapes the HBM target is stated on, each over >= 512 MB of copies
+    target = None
+    if m == 1 and fmt == "W2" and not args.no_target_shapes:
+        target = {f"{n}x{k}": time_shape(torch, pkg, dev, fmt, m, n, k, s2, reps=reps)
+                  for n, k in TARGET_SHAPES}
     ceiling = read_ceiling(torch, dev) if not args.no_read_ceiling else None
 
     out = {
@@ -552,6 +564,7 @@ def main():
         "tokens_per_s": round(m / (ms / 1e3), 2),
         "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "per_shape": per_shape,
+        "target_shapes": target,
         "read_ceiling": ceiling,
         "frac_read_ceiling": round(gbs / ceiling["GB/s"], 4) if ceiling else None,
         "roofline": ({
@@ -584,6 +597,85 @@ def main():
         out["cpu_baseline"] = cpu_baseline(mats_cpu, args.cpu_sample_seconds, step_bytes,
                                            per_mat_bytes, layers)
     print(json.dumps(out), flush=True)
+
+
+def time_shape(torch, pkg, dev, fmt, m, n, k, stream, min_bytes=512 << 20, reps=10, seed=11):
+    """Microseconds per launch of one n x k matrix at batch m: seeded uniform codes with per-row
+    radius scales, packed once and copied until the copies hold at least `min_bytes` (so no
+    launch is served from the 256 MB Infinity Cache), launched once per copy inside a HIP graph
+    and timed with HIP events on the graph's stream."""
+    D, V = synth.FORMATS[fmt]
+    g = synth.rng(seed, n, k, synth.STREAM_CODES)
+    codes = synth.uniform_codes(n, k, D, V, g)
+    codes["gmin"], codes["gstep"] = synth.row_scale_group_params(n, k, V, g)
+    cb = synth.random_codebook(D, synth.rng(seed, n, k, synth.STREAM_CODEBOOK))
+    x = synth.activations(m, k, synth.rng(seed, n, k, synth.STREAM_X))
+    w0 = pkg.pack(D, V, codes, cb, device=dev)
+    ncopy = max(16, -(-min_bytes // w0.nbytes))
+    copies = [w0] + [clone_weights(pkg, w0) for _ in range(ncopy - 1)]
+    xd = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.float16)
+    y = torch.empty((m, n), dtype=torch.float32, device=dev)
+
+    def launch(w):
+        if m == 1:
+            pkg.gemv(w, xd[0], out=y[0])
+        elif m <= 32:
+            pkg.gemm_small(w, xd, out=y)
+        else:
+            pkg.gemm(w, xd, out=y)
+
+    with torch.cuda.stream(stream):
+        for w in copies:
+            launch(w)                        # first calls (workspaces) outside capture
+    torch.cuda.synchronize()
+    gs = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gs, stream=stream):
+        for w in copies:
+            launch(w)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        gs.replay()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            gs.replay()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * ncopy)
+    nbytes = w0.nbytes
+    del gs, copies
+    torch.cuda.empty_cache()
+    return {"us": round(us, 3), "GB/s": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "frac_hbm_peak": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+            "bytes_per_launch": int(nbytes), "copies": ncopy, "launches_timed": reps * ncopy}
+
+
+# The batch-1 W2 shapes the HBM target is stated on (the 8B-class gate/up and down matrices).
+TARGET_SHAPES = ((12288, 4096), (4096, 12288))
+
+
+def shapes_main(args):
+    """Per-launch timing of the shapes named by --shapes (NxK,...) at --batch, each rotated over
+    at least 512 MB of packed copies; one JSON line."""
+    import torch
+
+    import paper_2609_24875_amd as pkg
+
+    if not torch.cuda.is_available():
+        raise RuntimeError("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    pkg.load_library()
+    fmt = args.fmt or "W2"
+    st = torch.cuda.Stream()
+    res = {}
+    for spec in args.shapes.split(","):
+        n, k = (int(v) for v in spec.lower().split("x"))
+        res[f"{n}x{k}"] = time_shape(torch, pkg, dev, fmt, args.batch, n, k, st, reps=args.steps)
+        print(f"# {fmt} m={args.batch} {n}x{k}: {res[f'{n}x{k}']}", file=sys.stderr, flush=True)
+    print(json.dumps({"metric": "us per launch", "fmt": fmt, "batch": args.batch, "per_shape": res}),
+          flush=True)
 
 
 def kernel_label(fmt, m):

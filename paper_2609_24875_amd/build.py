@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import os
+import re
 import shutil
 import subprocess
 
@@ -23,6 +24,10 @@ HIPCC_FLAGS = [
     # v_dot2c_f32_f16 ties its accumulator to the destination and costs a copy of the zero seed
     # per rebuilt vector.
     "-Xclang", "-target-feature", "-Xclang", "-dot5-insts",
+    # No atomic optimizer: it rewrites a single lane's atomic add into a wave-wide one and reads its
+    # result back at once, which makes the decode loop wait for every load in flight at a split
+    # tile's hand-over (the arrival count is only needed after the loop).
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-Wall", "-Wno-unused-command-line-argument",
 ]
 
@@ -34,14 +39,42 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
+# The compiler's per-kernel resource remarks, checked after every build.
+RESOURCE_REMARKS = "-Rpass-analysis=kernel-resource-usage"
+
+
+def kernel_resources(stderr: str) -> dict:
+    """{kernel: {"scratch": bytes per lane, "vgpr_spill": n}} from the resource remarks."""
+    res, name = {}, None
+    for line in stderr.splitlines():
+        m = re.search(r"remark: Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            res[name] = {}
+            continue
+        m = re.search(r"remark:\s+(ScratchSize \[bytes/lane\]|VGPRs Spill): (\d+)", line)
+        if m and name:
+            res[name]["scratch" if m.group(1).startswith("Scratch") else "vgpr_spill"] = int(m.group(2))
+    return res
+
+
 def _compile(sources, out: str, verbose: bool) -> str:
     tmp = out + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, *sources]
+    cmd = [hipcc(), *HIPCC_FLAGS, RESOURCE_REMARKS, "-I", os.path.join(ROOT, "include"), "-o", tmp, *sources]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)
-    if verbose and res.stderr.strip():
-        print(res.stderr)
+    # The decode and prefill kernels keep everything in registers: a record buffer or an
+    # accumulator put in scratch memory (a spill, or an array the compiler could not promote)
+    # halves their speed without any other sign, so the build refuses it.
+    bad = {k: v for k, v in kernel_resources(res.stderr).items()
+           if "k_gemm" in k and (v.get("scratch", 0) or v.get("vgpr_spill", 0))}
+    if bad:
+        os.remove(tmp)
+        raise RuntimeError(f"kernels using scratch memory: {bad}")
+    warnings = [ln for ln in res.stderr.splitlines() if "remark:" not in ln and ln.strip()]
+    if verbose and warnings:
+        print("\n".join(warnings))
     os.replace(tmp, out)
     return out
 

@@ -51,13 +51,16 @@ struct KArgs {
   int64_t ldy;
   int y_f16;
   int n, nt, nv, ng, m;
-  // vector-ALU work plan: ts = nt * nc steps in tile-major order, cut into one contiguous range
-  // per workgroup (whole tiles when wg_tiles > 0, else balanced to one step), each cut evenly
-  // among the workgroup's waves
+  // vector-ALU work plan: ts = nt * nc steps in tile-major order, cut into contiguous wave ranges
+  // of wl steps (the last one of a workgroup or of the launch possibly shorter, later waves
+  // empty): across the whole launch (wg_tiles = 0), or inside each workgroup's wgs = wg_tiles * nc
+  // steps of whole tiles
   int nc;             // steps (chunks of vector positions) per tile
   int nwg;            // workgroups
-  int wg_tiles;       // tiles per workgroup, or 0 for balanced ranges
-  int wq, wr;         // balanced ranges: ts = (nwg * VALU_WPB) * wq + wr
+  int wg_tiles;       // tiles per workgroup, or 0 for ranges across workgroups
+  int wl, wgs;        // steps per wave range and per workgroup (wg_tiles > 0)
+  uint32_t wl_m, wgs_m;   // multipliers and shifts for division by wl and wgs (see udiv_by)
+  int wl_k, wgs_k;
   int wpb;            // waves per workgroup
   int pmax;           // slot parts per tile
   int ts;
@@ -221,7 +224,7 @@ struct Tables {
 // to balanced ranges). Host and device.
 __host__ __device__ constexpr bool lds_handover_fits(int kind, int D, int M, int mode) {
   return ((kind == SPH_KIND_CB13 || kind == SPH_KIND_CB13Q4) ? ((16u << D) + 128u) : (256u << D)) +
-             (16u * 2u * M * 16u * 4u + 16u * 4u) + (mode == 2 ? 0u : 16u * 256u) <= 160u * 1024u;
+             (16u * M * 16u * 4u + 17u * 4u) + (mode == 2 ? 0u : 16u * 256u) <= 160u * 1024u;
 }
 
 // MX selects the matrix-core variant (batch 2..16): the lane's rows are rebuilt as in the vector
@@ -530,121 +533,60 @@ __device__ __forceinline__ void wave_reduce(float (&v)[NVAL], int lane) {
   }
 }
 
-// n steps cut into `parts` contiguous pieces, the first n % parts of them one step longer: the
-// start of piece i, and the piece holding step x. 32-bit arithmetic only (the kernel computes
-// these in its prologue, before its first loads).
-__device__ __forceinline__ int piece_start(int n, int parts, int i) {
-  const int q = n / parts, r = n - q * parts;
-  return i * q + min(i, r);
-}
-__device__ __forceinline__ int piece_of(int n, int parts, int x) {
-  const int q = n / parts, r = n - q * parts;
-  return x < r * (q + 1) ? x / (q + 1) : r + (x - r * (q + 1)) / q;
-}
-
-// Step ranges. With wg_tiles > 0 workgroup b owns tiles [b*wg_tiles, (b+1)*wg_tiles) and cuts
-// their steps into nw = min(VALU_WPB, n) pieces, one per wave. Otherwise the ts steps are spread
-// over all gw = nwg * VALU_WPB waves of the grid: wave g starts at floor(g * ts / gw), written as
-// g * wq + floor(g * wr / gw) so that it stays in 32 bits (g * wr < gw^2).
-__device__ __forceinline__ void wg_range(const KArgs& a, int b, int& s0, int& s1) {
-  s0 = min(b * a.wg_tiles, a.nt) * a.nc;
-  s1 = min((b + 1) * a.wg_tiles, a.nt) * a.nc;
-}
-
-__device__ __forceinline__ int spread_start(const KArgs& a, int g) {
-  const int gw = a.nwg * VALU_WPB;
-  return g * a.wq + (g * a.wr) / gw;
+// floor(x / d) for 0 <= x < 2^31 and a launch-constant d, as (x * m) >> k with the host's
+// m = ceil(2^k / d), k = 31 + ceil(log2 d): m fits in 32 bits and the product's excess over x / d
+// stays below 1 / d, so the floor is exact. A multiply and a shift instead of an integer division
+// sequence, which would cost the prologue a microsecond over the 16 waves of a CU.
+__device__ __forceinline__ int udiv_by(int x, uint32_t m, int k) {
+  return (int)(((uint64_t)(uint32_t)x * m) >> k);
 }
 
 // The wave (id = workgroup * VALU_WPB + wave in workgroup) whose range holds step s.
 __device__ __forceinline__ int wave_of_step(const KArgs& a, int s) {
-  if (a.wg_tiles == 0) {
-    const int64_t gw = (int64_t)a.nwg * VALU_WPB;
-    return __builtin_amdgcn_readfirstlane((int)(((int64_t)(s + 1) * gw - 1) / a.ts));
-  }
-  const int b = s / (a.wg_tiles * a.nc);
-  int s0, s1;
-  wg_range(a, b, s0, s1);
-  const int n = s1 - s0;
-  return __builtin_amdgcn_readfirstlane(b * VALU_WPB + piece_of(n, min(VALU_WPB, n), s - s0));
+  if (a.wg_tiles == 0) return __builtin_amdgcn_readfirstlane(udiv_by(s, a.wl_m, a.wl_k));
+  const int b = udiv_by(s, a.wgs_m, a.wgs_k);
+  return __builtin_amdgcn_readfirstlane(b * VALU_WPB + udiv_by(s - b * a.wgs, a.wl_m, a.wl_k));
 }
 
 // ------------------------------------------------------------------------------------------
 // Split tiles. A tile whose steps fall into the ranges of several waves has one part per wave: part
 // 0 (holding chunk 0) ends its wave's range, parts 1 .. np-1 start the ranges of the following
-// waves. Every part reduces its sums across lanes, puts them in a slot, and then counts its arrival
-// on the tile's counter; the part that arrives last adds part 0 to the sum of parts 1 .. np-1
-// (formed by the lanes in a fixed order, see gather_parts) and stores y. No wave waits for another
-// one to make progress: whichever part arrives last finds every other part's slot written. The
-// sum does not depend on which part arrives last, so results are bitwise reproducible.
+// waves. The parts are added in two levels, and no wave ever waits for another workgroup:
 //
-// Tiles whose parts all lie in one workgroup meet in LDS (a slot per wave and role, a counter per
-// wave holding a part 0). The others meet in the global workspace: a 64-bit slot per value, the
-// fp32 sum in the low half and a valid flag in the high half, and a 32-bit counter per tile, all
-// written and read with device-coherent (agent-scope) atomics and no fences. A counter can show a
-// part as arrived while its slot stores, issued before the arrival, are still in flight; the last
-// arriver then re-reads that slot until the store lands -- a wait for a store already issued, not
-// for another wave. The last arriver clears the slots and the counter it used, so the workspace is
-// zero again after every call.
+// 1. Inside a workgroup the tile's parts meet in LDS. Every part but the first one there (the
+//    local leader) puts its lane-reduced sums in its wave's slot, counts its arrival on a counter
+//    of the tile and moves on at once. The leader -- part 0, or the entering tile's part in the
+//    workgroup's first wave, in either case the last part its wave computes -- waits for the
+//    other local parts, which run on waves of its own workgroup and so are resident and wait for
+//    nothing themselves, and adds them to its own sums in a fixed order.
+// 2. A tile inside one workgroup is then stored. A tile over two workgroups meets in one 64-bit
+//    workspace word per value: each workgroup swaps its sum, tagged valid in the high half, into
+//    the word with a device-coherent atomic exchange. The lane that gets the other workgroup's sum
+//    back adds the two (a sum of two terms, the same whichever comes first), stores y and zeroes
+//    the word; the other lane has nothing left to do. A tile over three or more workgroups (only
+//    when a wave range is much shorter than a tile) meets in per-workgroup slots and a counter:
+//    the slots are written before a release fence and the count, and the workgroup that counts
+//    last, after an acquire fence, adds the workgroup sums in workgroup order, stores y and zeroes
+//    the slots and the counter.
+//
+// Each level adds in an order fixed by the plan, whichever part or workgroup arrives last, so
+// results are bitwise reproducible, and the workspace is zero again after every call. Where the
+// LDS has no room for the slots (the tile variant with the largest tables), every part goes to
+// level 2 as a group of its own.
 // ------------------------------------------------------------------------------------------
-__device__ __forceinline__ void slot_store(uint64_t* p, float v) {
-  __hip_atomic_store(p, (uint64_t)__builtin_bit_cast(uint32_t, v) | (1ull << 32), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t slot_load(const uint64_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ uint64_t slot_word(float v) {
+  return (uint64_t)__builtin_bit_cast(uint32_t, v) | (1ull << 32);
 }
 
-// A global slot word whose store was issued before its part's arrival was counted: re-read until
-// the store has landed. The bound (about 100 ms on the 100 MHz real-time counter, far beyond any
-// memory latency) is never expected to run out; if it did, the sum is marked invalid (NaN).
-__device__ __forceinline__ float landed(uint64_t w, const uint64_t* p, bool& ok) {
-  if ((w >> 32) == 0) {
-    const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + 10000000ull;
-    do {
-      __builtin_amdgcn_s_sleep(1);
-      w = slot_load(p);
-    } while ((w >> 32) == 0 && __builtin_amdgcn_s_memrealtime() < deadline);
-    ok = ok && (w >> 32) != 0;
-  }
-  return __builtin_bit_cast(float, (uint32_t)w);
-}
-
-// LDS meeting place of the split tiles inside a workgroup: per wave a slot for a later part it
-// holds (role 0) and one for a part 0 (role 1), and the arrival counter of the tile whose part 0
-// it holds (each wave holds at most one later part, its first, and one part 0, its last).
+// LDS meeting place of the split tiles inside a workgroup: per wave a slot for its first part (the
+// only part a wave can hand over to a leader: a part 0 leads its tile's local parts), and the
+// arrival counter of the tile whose part 0 wave w holds (cnt[w]) and of the tile that enters from
+// the previous workgroup (cnt[VALU_WPB]). Each slot and counter serves one tile per launch.
 template <int M>
 struct WgHo {
-  float slot[VALU_WPB][2][M * 16];
-  uint32_t cnt[VALU_WPB];
+  float slot[VALU_WPB][M * 16];
+  uint32_t cnt[VALU_WPB + 1];
 };
-
-// Global slot words of parts 1 + l / NIDX + PPI * j (j < JB) at index l % NIDX (+ 64 k) for lane
-// l, and the tile's counter: fetched by the wave holding part 0 before its last step, so that
-// their round trip overlaps that step.
-template <int M>
-struct SlotPre {
-  static constexpr int NIDX = M * 16;
-  static constexpr int PPI = NIDX >= 64 ? 1 : 64 / NIDX;   // parts per load instruction
-  static constexpr int IPP = NIDX <= 64 ? 1 : NIDX / 64;   // load instructions per part
-  static constexpr int JB = IPP >= 4 ? 1 : 4 / IPP;        // parts per lane loaded together
-  uint64_t w[JB][IPP];
-  uint32_t cnt;
-};
-
-template <int M>
-__device__ __forceinline__ void fetch_parts(SlotPre<M>& P, const KArgs& a, int t, int np, int j0, int lane) {
-  using S = SlotPre<M>;
-  const uint64_t* slots = a.ws_slot + (int64_t)t * a.pmax * S::NIDX;
-  const int loff = (S::NIDX >= 64) ? 0 : lane / S::NIDX;
-#pragma unroll
-  for (int j = 0; j < S::JB; ++j) {
-    const int p = min(1 + loff + S::PPI * (j0 + j), np - 1);
-#pragma unroll
-    for (int k = 0; k < S::IPP; ++k) P.w[j][k] = slot_load(slots + (int64_t)p * S::NIDX + (lane % S::NIDX) + 64 * k);
-  }
-  P.cnt = __hip_atomic_load(a.ws_cnt + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // Slot index (batch row * 16 + tile row) of value i of this lane after the wave reduction: vector
 // variant, value b * RPL + r is batch row b, tile row h * RPL + r; 4x4x4 blocks, value 16g + 4r + e
@@ -682,48 +624,173 @@ __device__ __forceinline__ void store_part(const KArgs& a, int t, const PartIdx<
   }
 }
 
-// Finish split tile t as its last arriving part (p_self; own values in `vals`, used when it is
-// part 0): y = part 0 + (sum of parts 1 .. np-1). Lane l adds, in increasing part order, slot
-// index l % NIDX (+ 64 k) of parts 1 + l / NIDX + PPI * j; the lanes holding one slot index are
-// then added by a fixed exchange tree; the writer lanes add that to part 0. GLOBAL: the parts are
-// in the workspace (the first batch possibly prefetched in `pre`), which is cleared afterwards.
-template <int M, int RPL, int MODE, bool GLOBAL>
-__device__ __forceinline__ void finish_tile(const KArgs& a, int t, int np, int gr, int p_self,
-                                         const float (&vals)[PartIdx<M, RPL, MODE>::N4], const SlotPre<M>* pre,
-                                         const WgHo<M>* ho, int lane) {
-  using S = SlotPre<M>;
+
+// Where a tile's parts lie, seen from wave g: waves gr .. gl hold them (np parts); this
+// workgroup's are waves lw0 .. lw0+nl-1, counted on LDS counter ci; the tile spans ngrp groups
+// (workgroups, or single parts without LDS meeting), this wave's being group gi. A wave can only
+// hold a part of a split tile in the first and the last tile of its range, and it finds gr and gl
+// for both at the start, while its first loads are in flight (they take integer divisions that
+// would otherwise sit at the end of its work).
+struct SplitGeo {
+  int gr, np, p, lw0, nl, ci, ngrp, gi;
+};
+
+template <bool LDS_HO>
+__device__ __forceinline__ SplitGeo split_geo(int gr, int gl, int g) {
+  SplitGeo s;
+  s.gr = gr;
+  s.np = gl - s.gr + 1;
+  s.p = g - s.gr;
+  if constexpr (LDS_HO) {
+    const int b0 = (g / VALU_WPB) * VALU_WPB;
+    s.lw0 = max(s.gr, b0);
+    s.nl = min(gl, b0 + VALU_WPB - 1) - s.lw0 + 1;
+    s.ci = s.gr >= b0 ? s.gr - b0 : VALU_WPB;
+    s.ngrp = gl / VALU_WPB - s.gr / VALU_WPB + 1;
+    s.gi = g / VALU_WPB - s.gr / VALU_WPB;
+  } else {
+    s.lw0 = g;
+    s.nl = 1;
+    s.ci = 0;
+    s.ngrp = s.np;
+    s.gi = s.p;
+  }
+  return s;
+}
+
+// Level 2: the group sum `v` of tile t (see above).
+template <int M, int RPL, int MODE>
+__device__ __forceinline__ void group_done(const KArgs& a, int t, const SplitGeo& s,
+                                           const float (&v)[PartIdx<M, RPL, MODE>::N4], int lane) {
   using I = PartIdx<M, RPL, MODE>;
-  constexpr int NIDX = S::NIDX, PPI = S::PPI, IPP = S::IPP, JB = S::JB;
+  constexpr int NIDX = M * 16;
   const I ix(lane);
-  const uint64_t* slots = GLOBAL ? a.ws_slot + (int64_t)t * a.pmax * NIDX : nullptr;
+  if (s.ngrp == 1) {
+    store_part<M, RPL, MODE>(a, t, ix, v, true);
+    return;
+  }
+  uint64_t* slots = a.ws_slot + (int64_t)t * a.pmax * NIDX;
+  if (s.ngrp == 2) {
+    if (!ix.writer) return;
+    uint64_t o[I::N4];   // all exchanges in flight together
+#pragma unroll
+    for (int i = 0; i < I::N4; ++i)
+      o[i] = __hip_atomic_exchange(slots + ix.idx[i], slot_word(v[i]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+    for (int i = 0; i < I::N4; ++i)
+      if (o[i] >> 32) {
+        const int b = ix.idx[i] / 16, grow = t * 16 + ix.idx[i] % 16;
+        if (b < a.m && grow < a.n) store_y(a, b, grow, __builtin_bit_cast(float, (uint32_t)o[i]) + v[i]);
+        __hip_atomic_store(slots + ix.idx[i], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    return;
+  }
+  if (ix.writer)
+#pragma unroll
+    for (int i = 0; i < I::N4; ++i)
+      __hip_atomic_store(slots + s.gi * NIDX + ix.idx[i], slot_word(v[i]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  uint32_t old = 0;
+  if (lane == 0) old = __hip_atomic_fetch_add(a.ws_cnt + t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (__builtin_amdgcn_readfirstlane(old) + 1 != (uint32_t)s.ngrp) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  float tot[I::N4];
+#pragma unroll
+  for (int i = 0; i < I::N4; ++i) tot[i] = 0.0f;
+  if (ix.writer) {
+    for (int q = 0; q < s.ngrp; ++q)
+#pragma unroll
+      for (int i = 0; i < I::N4; ++i) {
+        const float x = q == s.gi ? v[i]
+                                  : __builtin_bit_cast(float, (uint32_t)__hip_atomic_load(
+                                                                  slots + q * NIDX + ix.idx[i], __ATOMIC_RELAXED,
+                                                                  __HIP_MEMORY_SCOPE_AGENT));
+        tot[i] = q == 0 ? x : tot[i] + x;
+      }
+    for (int q = 0; q < s.ngrp; ++q)
+#pragma unroll
+      for (int i = 0; i < I::N4; ++i)
+        __hip_atomic_store(slots + q * NIDX + ix.idx[i], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  store_part<M, RPL, MODE>(a, t, ix, tot, true);
+  if (lane == 0) __hip_atomic_store(a.ws_cnt + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The other local parts' slots (local parts 1 .. nl-1), spread over the lanes: lane l reads slot
+// index l % NIDX (+ 64 k) of local parts 1 + j0 + l / NIDX + PPI * jj (jj < JB), so that one round
+// trip covers up to 16 parts (4 for the 16-row batch) however many values a part has.
+template <int M>
+struct LocalRead {
+  static constexpr int NIDX = M * 16;
+  static constexpr int PPI = NIDX >= 64 ? 1 : 64 / NIDX;   // parts per read instruction
+  static constexpr int IPP = NIDX <= 64 ? 1 : NIDX / 64;   // read instructions per part
+  static constexpr int JB = (16 / IPP < 16 / PPI) ? 16 / IPP : 16 / PPI;
+  static constexpr int LDIV = NIDX >= 64 ? 64 : NIDX;
+  float v[JB][IPP];
+
+  // local part read into v[jj] by this lane
+  __device__ __forceinline__ static int part(int j0, int jj, int lane) { return 1 + j0 + lane / LDIV + PPI * jj; }
+
+  __device__ __forceinline__ void read(const WgHo<M>* ho, const SplitGeo& s, int j0, int lane) {
+#pragma unroll
+    for (int jj = 0; jj < JB; ++jj) {
+      const int w = s.lw0 + min(part(j0, jj, lane), s.nl - 1);
+#pragma unroll
+      for (int k = 0; k < IPP; ++k) v[jj][k] = ho->slot[w % VALU_WPB][lane % NIDX + 64 * k];
+    }
+    // taken as modified here, so that the reads are issued where they stand (next to the count
+    // they go with) rather than moved into the branch that uses them
+#pragma unroll
+    for (int jj = 0; jj < JB; ++jj)
+#pragma unroll
+      for (int k = 0; k < IPP; ++k) asm volatile("" : "+v"(v[jj][k]));
+  }
+};
+
+// Level 1, by the leader of tile t's local parts: wait until the other nl - 1 have counted their
+// arrival, then add to its own sums `own` those of the others (each lane its parts in increasing
+// order, then the lanes holding one slot index by a fixed exchange tree), and go on to level 2. The
+// slots are read in the same round trip as the count that shows them all written: the LDS performs
+// a wave's operations in issue order, so reads issued after the count see every slot counted in
+// it. The wait cannot run out (the parts come from resident waves of this workgroup, none of which
+// waits before handing its part over); a bound of about 100 ms on the real-time counter still
+// keeps the wave from hanging, marking the sums invalid (NaN) if it were ever reached.
+template <int M, int RPL, int MODE>
+__device__ __forceinline__ void leader_collect(const KArgs& a, int t, const SplitGeo& s, const WgHo<M>* ho,
+                                               const float (&own)[PartIdx<M, RPL, MODE>::N4], int lane) {
+  using I = PartIdx<M, RPL, MODE>;
+  using L = LocalRead<M>;
+  constexpr int NIDX = L::NIDX, PPI = L::PPI, IPP = L::IPP, JB = L::JB;
+  L R;
   bool ok = true;
+  const uint64_t deadline = __builtin_amdgcn_s_memrealtime() + 10000000ull;
+  for (;;) {
+    const uint32_t c = __hip_atomic_load(&ho->cnt[s.ci], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    asm volatile("" ::: "memory");
+    R.read(ho, s, 0, lane);
+    if (__builtin_amdgcn_readfirstlane(c) + 1 == (uint32_t)s.nl) break;
+    if (__builtin_amdgcn_s_memrealtime() > deadline) {
+      ok = false;
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
   float ps[IPP];
 #pragma unroll
   for (int k = 0; k < IPP; ++k) ps[k] = 0.0f;
-  const int loff = (NIDX >= 64) ? 0 : lane / NIDX;
-  for (int j0 = 0; 1 + PPI * j0 < np; j0 += JB) {
-    S P;
-    if constexpr (GLOBAL) {
-      if (j0 == 0 && pre) P = *pre;
-      else fetch_parts<M>(P, a, t, np, j0, lane);
-    }
+  for (int j0 = 0; 1 + j0 < s.nl; j0 += PPI * JB) {
+    if (j0 > 0) R.read(ho, s, j0, lane);
 #pragma unroll
-    for (int j = 0; j < JB; ++j) {
-      const int p = 1 + loff + PPI * (j0 + j);
-      if (p < np) {
+    for (int jj = 0; jj < JB; ++jj)
+      if (L::part(j0, jj, lane) < s.nl)
 #pragma unroll
-        for (int k = 0; k < IPP; ++k) {
-          const int si = (lane % NIDX) + 64 * k;
-          if constexpr (GLOBAL) ps[k] += landed(P.w[j][k], slots + (int64_t)p * NIDX + si, ok);
-          else ps[k] += ho->slot[(gr + p) % VALU_WPB][0][si];
-        }
-      }
-    }
+        for (int k = 0; k < IPP; ++k) ps[k] += R.v[jj][k];
   }
   // lanes l and l ^ NIDX, ... hold the same slot index: add them, larger distances first
   if constexpr (NIDX <= 16) ps[0] += __shfl_xor(ps[0], 32);
   if constexpr (NIDX <= 16) ps[0] += __shfl_xor(ps[0], 16);
   if constexpr (NIDX == 32) ps[0] += __shfl_xor(ps[0], 32);
+  const I ix(lane);
   float tot[I::N4];
 #pragma unroll
   for (int i = 0; i < I::N4; ++i) {
@@ -731,59 +798,34 @@ __device__ __forceinline__ void finish_tile(const KArgs& a, int t, int np, int g
     float other = 0.0f;
 #pragma unroll
     for (int kk = 0; kk < IPP; ++kk) {
-      const float v = __shfl(ps[kk], src);
-      if (kk == k) other = v;
+      const float u = __shfl(ps[kk], src);
+      if (kk == k) other = u;
     }
-    float base = vals[i];
-    if (p_self != 0) {
-      if constexpr (GLOBAL) base = landed(slot_load(slots + ix.idx[i]), slots + ix.idx[i], ok);
-      else base = ho->slot[gr % VALU_WPB][1][ix.idx[i]];
-    }
-    tot[i] = base + other;
+    tot[i] = ok ? own[i] + other : __builtin_nanf("");
   }
-  store_part<M, RPL, MODE>(a, t, ix, tot, __all(ok));
-  if constexpr (GLOBAL) {
-    // every part has arrived and been read: clear the slots and the counter for the next call
-    for (int p = 0; p < np; ++p)
-#pragma unroll
-      for (int k = 0; k < (NIDX + 63) / 64; ++k)
-        if (lane + 64 * k < NIDX)
-          __hip_atomic_store((uint64_t*)slots + (int64_t)p * NIDX + lane + 64 * k, 0ull, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-    if (lane == 0) __hip_atomic_store(a.ws_cnt + t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+  group_done<M, RPL, MODE>(a, t, s, tot, lane);
 }
 
-// Count a part's arrival at a tile meeting in the workspace (its slot written before), and finish
-// the tile if it arrived last.
-template <int M, int RPL, int MODE>
-__device__ __forceinline__ void arrive_global(const KArgs& a, int t, int np, int gr, int p,
-                                              const float (&v4)[PartIdx<M, RPL, MODE>::N4], const WgHo<M>* ho,
-                                              int lane) {
-  uint32_t old = 0;
-  if (lane == 0)
-    old = __hip_atomic_fetch_add(a.ws_cnt + t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (__builtin_amdgcn_readfirstlane(old) + 1 == (uint32_t)np) finish_tile<M, RPL, MODE, true>(a, t, np, gr, p, v4, nullptr, ho, lane);
-}
-
-// A part handed over inside the step loop (a range's first part), to be followed up after the
-// loop: a tile that met in LDS and whose last part it was (finish it), or a tile meeting in the
-// workspace (count the arrival -- its slot is written already -- and finish the tile if it was the
-// last). All wave-uniform, so the loop carries no vector register for it: a count returned by an
-// atomic inside the loop would make the compiler wait for it there, draining the records in flight.
+// A part whose tile work is left for after the step loop (a range's first part, emitted inside it):
+// kind 1, a group of its own at level 2; kind 2, a local leader (not expected: a range's first
+// part leads only when it is the workgroup's sole part of its tile). Its values wait in its
+// wave's LDS slot (free: the part hands nothing over), or without LDS meeting in `v`.
+template <int NV>
 struct Pending {
-  int t = -1, np = 0, p = 0;
-  bool lds = false;
+  int t = -1, kind = 0;
+  float v[NV];
 };
+template <int M, int RPL, int MODE, bool LDS_HO>
+using PendingOf = Pending<LDS_HO ? 1 : PartIdx<M, RPL, MODE>::N4>;
 
 // Finish the part [ca, cb) of tile t computed by wave g: reduce across lanes, then store y (whole
 // tile) or hand the part over as described above. FINAL: the range's last part, after which the
-// wave has no loads in flight, so it counts its arrival and finishes the tile straight away if it
-// arrived last; otherwise the follow-up is left in `pend`.
+// wave has no loads in flight; a range's first part emitted inside the loop leaves any work that
+// could wait or make a round trip to after the loop (`pend`).
 template <int M, int RPL, int MODE, bool LDS_HO, bool FINAL>
 __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[MODE == 2 ? M / 16 : M][RPL], int t, int ca,
-                                          int cb, int g, int lane, const SlotPre<M>& pre, bool have_pre, WgHo<M>* ho,
-                                          Pending& pend) {
+                                          int cb, int g, int gr, int gl, int lane, WgHo<M>* ho,
+                                          PendingOf<M, RPL, MODE, LDS_HO>& pend) {
   using I = PartIdx<M, RPL, MODE>;
   constexpr int H = 16 / RPL;
   float vals[I::NVAL];
@@ -803,40 +845,52 @@ __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[MODE == 2
     store_part<M, RPL, MODE>(a, t, ix, v4, true);
     return;
   }
-  const int gr = wave_of_step(a, t * a.nc);
-  const int np = wave_of_step(a, t * a.nc + a.nc - 1) - gr + 1;
-  const int p = g - gr;
-  if (LDS_HO && gr / VALU_WPB == (gr + np - 1) / VALU_WPB) {
-    float* mine = ho->slot[g % VALU_WPB][p == 0 ? 1 : 0];
+  const SplitGeo s = split_geo<LDS_HO>(gr, gl, g);
+  if (LDS_HO && s.nl > 1 && g != s.lw0) {
+    // hand over to the local leader: slot, then count (in this order in the LDS; the compiler
+    // barrier keeps them so), no wait
+    float* mine = ho->slot[g % VALU_WPB];
     if (ix.writer)
 #pragma unroll
       for (int i = 0; i < I::N4; ++i) mine[ix.idx[i]] = v4[i];
-    // the slot writes have reached LDS before the arrival is counted (lgkmcnt(0), other counters
-    // left alone)
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    uint32_t old = 0;
-    if (lane == 0)
-      old = __hip_atomic_fetch_add(&ho->cnt[gr % VALU_WPB], 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_WORKGROUP);
-    if (__builtin_amdgcn_readfirstlane(old) + 1 == (uint32_t)np) {
-      if constexpr (FINAL) finish_tile<M, RPL, MODE, false>(a, t, np, gr, p, v4, nullptr, ho, lane);
-      else pend = Pending{t, np, p, true};
-    }
+    asm volatile("" ::: "memory");
+    if (lane == 0) __hip_atomic_fetch_add(&ho->cnt[s.ci], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     return;
   }
   if constexpr (FINAL) {
-    if (p == 0 && have_pre && __builtin_amdgcn_readfirstlane(pre.cnt) + 1 == (uint32_t)np) {
-      // every later part has arrived: finish with the prefetched slots, no arrival of our own
-      finish_tile<M, RPL, MODE, true>(a, t, np, gr, 0, v4, &pre, ho, lane);
-      return;
+    if (LDS_HO && s.nl > 1) leader_collect<M, RPL, MODE>(a, t, s, ho, v4, lane);
+    else group_done<M, RPL, MODE>(a, t, s, v4, lane);
+  } else {
+    pend.t = t;
+    pend.kind = (LDS_HO && s.nl > 1) ? 2 : 1;
+    if constexpr (LDS_HO) {
+      if (ix.writer)
+#pragma unroll
+        for (int i = 0; i < I::N4; ++i) ho->slot[g % VALU_WPB][ix.idx[i]] = v4[i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < I::N4; ++i) pend.v[i] = v4[i];
     }
   }
-  uint64_t* slot = a.ws_slot + ((int64_t)t * a.pmax + p) * (M * 16);
-  if (ix.writer)
+}
+
+// The work left by a range's first part (see Pending).
+template <int M, int RPL, int MODE, bool LDS_HO>
+__device__ __forceinline__ void follow_up(const KArgs& a, int g, int gr, int gl, int lane, const WgHo<M>* ho,
+                                          const PendingOf<M, RPL, MODE, LDS_HO>& pend) {
+  using I = PartIdx<M, RPL, MODE>;
+  if (pend.t < 0) return;
+  const SplitGeo s = split_geo<LDS_HO>(gr, gl, g);
+  if constexpr (LDS_HO) {
+    const I ix(lane);
+    float v[I::N4];
 #pragma unroll
-    for (int i = 0; i < I::N4; ++i) slot_store(slot + ix.idx[i], v4[i]);
-  if constexpr (FINAL) arrive_global<M, RPL, MODE>(a, t, np, gr, p, v4, ho, lane);
-  else pend = Pending{t, np, p, false};
+    for (int i = 0; i < I::N4; ++i) v[i] = ix.writer ? ho->slot[g % VALU_WPB][ix.idx[i]] : 0.0f;
+    if (pend.kind == 2) leader_collect<M, RPL, MODE>(a, pend.t, s, ho, v, lane);
+    else group_done<M, RPL, MODE>(a, pend.t, s, v, lane);
+  } else {
+    group_done<M, RPL, MODE>(a, pend.t, s, pend.v, lane);
+  }
 }
 
 // Lookup tables staged in two halves around the first record's loads: the table words are
@@ -927,19 +981,13 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = (int)blockIdx.x * a.wpb + wave;
   // The range bounds are wave-uniform; readfirstlane keeps them (and every branch on them) scalar.
-  bool active;
-  int s_begin, s_end;
-  if (a.wg_tiles > 0) {
-    int wg_s0, wg_s1;
-    wg_range(a, blockIdx.x, wg_s0, wg_s1);
-    const int wg_n = wg_s1 - wg_s0, wg_nw = min(VALU_WPB, wg_n);
-    active = wave < wg_nw;
-    s_begin = active ? wg_s0 + piece_start(wg_n, wg_nw, wave) : 0;
-    s_end = active ? wg_s0 + piece_start(wg_n, wg_nw, wave + 1) : 1;
-  } else {
-    active = true;                           // every wave has at least one step
-    s_begin = spread_start(a, g);
-    s_end = spread_start(a, g + 1);
+  const int r_lim = a.wg_tiles > 0 ? min(((int)blockIdx.x + 1) * a.wgs, a.ts) : a.ts;
+  int s_begin = (a.wg_tiles > 0 ? (int)blockIdx.x * a.wgs + wave * a.wl : g * a.wl);
+  int s_end = min(s_begin + a.wl, r_lim);
+  const bool active = s_begin < r_lim;
+  if (!active) {                             // an empty range (returns after the barrier)
+    s_begin = 0;
+    s_end = 1;
   }
   s_begin = __builtin_amdgcn_readfirstlane(s_begin);
   s_end = __builtin_amdgcn_readfirstlane(s_end);
@@ -951,9 +999,13 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   TableWords<KIND, D> tw;
   fetch_tables<KIND, D>(tw, a);
   S::load(r0, a, t0, c0, h, vloc, lane);
+  // the waves holding the first and the last step of the range's first and last tile (see SplitGeo)
+  const int tl = __builtin_amdgcn_readfirstlane((s_end - 1) / a.nc);
+  const int gr0 = wave_of_step(a, t0 * a.nc), gl0 = wave_of_step(a, t0 * a.nc + a.nc - 1);
+  const int grl = wave_of_step(a, tl * a.nc), gll = wave_of_step(a, tl * a.nc + a.nc - 1);
   store_tables<KIND, D>(lds, tw, a);
   if constexpr (LDS_HO)
-    if (threadIdx.x < VALU_WPB) ho->cnt[threadIdx.x] = 0u;
+    if (threadIdx.x <= VALU_WPB) ho->cnt[threadIdx.x] = 0u;
   const uint32_t mask_off = a.t_bytes;
   __syncthreads();
   if (!active) return;                       // no barrier follows
@@ -970,12 +1022,10 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   // bottom (an early exit would give the compiler a path back to the loop head with loads still
   // pending, and it would wait for them). The range's last step is peeled off: the tile parts
   // that end inside the loop are whole tiles or the range's first part, and the last part, which
-  // may be part 0 of a split tile, is finished after it, with the workspace slots of the other
-  // parts fetched before the last step is computed.
+  // may be part 0 of a split tile, is finished after it.
   const int nsteps = s_end - s_begin;
   const int npairs = (nsteps - 1) >> 1;
-  SlotPre<M> pre;                            // filled only before the last step (see below)
-  Pending pend;
+  PendingOf<M, RPL, MODE, LDS_HO> pend;
   int t = t0, c = c0;                        // position of step 2i
   for (int i = 0; i < npairs; ++i) {
     int t1 = t, c1 = c + 1;
@@ -985,7 +1035,7 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
     }
     S::load(r1, a, t1, c1, h, vloc, lane);
     S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c1 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, pre, false, ho, pend);
+    if (c1 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, gr0, gl0, lane, ho, pend);
     int t2 = t1, c2 = c1 + 1;
     if (c2 == a.nc) {
       ++t2;
@@ -993,7 +1043,7 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
     }
     S::load(r0, a, t2, c2, h, vloc, lane);   // step 2i + 2 <= nsteps - 1 exists
     S::compute(r1, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c2 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, lane, pre, false, ho, pend);
+    if (c2 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, gr0, gl0, lane, ho, pend);
     t = t2;
     c = c2;
   }
@@ -1007,30 +1057,15 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
     }
     S::load(r1, a, tf, cf, h, vloc, lane);
     S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (cf == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, lane, pre, false, ho, pend);
+    if (cf == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, gr0, gl0, lane, ho, pend);
   }
   const int caf = tf == t0 ? c0 : 0;
-  // part 0 of a tile that continues in another workgroup: prefetch the other parts' slots
-  bool have_pre = false;
-  if (caf == 0 && cf + 1 < a.nc) {
-    const int gl = wave_of_step(a, tf * a.nc + a.nc - 1);
-    if (!(LDS_HO && g / VALU_WPB == gl / VALU_WPB)) {
-      fetch_parts<M>(pre, a, tf, gl - g + 1, 0, lane);
-      have_pre = true;
-    }
-  }
-  // one instance of the step code for the last step, whichever buffer holds it
-  const typename S::R& rf = (nsteps - 2 * npairs == 2) ? r1 : r0;
-  S::compute(rf, acc, lds, mask_off, pstage, lane, h, vloc);
-  emit_part<M, RPL, MODE, LDS_HO, true>(a, acc, tf, caf, cf + 1, g, lane, pre, have_pre, ho, pend);
-  // the follow-up of the range's first part, handed over inside the loop (its values are in its
-  // slot by now, so the ones passed here are not used)
-  if (pend.t >= 0) {
-    const float unused[PartIdx<M, RPL, MODE>::N4] = {};
-    const int gr = wave_of_step(a, pend.t * a.nc);
-    if (LDS_HO && pend.lds) finish_tile<M, RPL, MODE, false>(a, pend.t, pend.np, gr, pend.p, unused, nullptr, ho, lane);
-    else if (!pend.lds) arrive_global<M, RPL, MODE>(a, pend.t, pend.np, gr, pend.p, unused, ho, lane);
-  }
+  // one instance of the step code for the last step: its records are moved into r0 when r1 holds
+  // them (a reference chosen between the two buffers would put both in scratch memory)
+  if (nsteps - 2 * npairs == 2) r0 = r1;
+  S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
+  emit_part<M, RPL, MODE, LDS_HO, true>(a, acc, tf, caf, cf + 1, g, grl, gll, lane, ho, pend);
+  follow_up<M, RPL, MODE, LDS_HO>(a, g, gr0, gl0, lane, ho, pend);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1490,7 +1525,7 @@ struct Launch {
   const void* fn;
   int block;          // threads per workgroup
   int grid;
-  int nc, wg_tiles, wq, wr, pmax, ts;
+  int nc, wg_tiles, wl, wgs, pmax, ts;
   size_t ws_bytes;    // workspace the launch needs
   size_t cnt_off;     // offset of the split-tile arrival counters in it
 };
@@ -1651,8 +1686,17 @@ PrefillPlan prefill_plan(const sph_weights* w, int64_t m) {
   return P;
 }
 
-// Work plan. Vector-ALU path: one 16-wave workgroup per CU, every wave a contiguous range of
-// steps (at least one). Matrix-core path: a workgroup per tile, its waves splitting K.
+// m and k of udiv_by for a divisor 1 <= d < 2^31.
+void div_magic(int d, uint32_t& m, int& k) {
+  int l = 0;
+  while ((1ll << l) < d) ++l;
+  k = 31 + l;
+  m = (uint32_t)(((1ull << k) + (uint64_t)d - 1) / (uint64_t)d);
+}
+
+// Work plan. Vector-ALU path: one 16-wave workgroup per CU, every wave a contiguous range of wl
+// steps (the last ones shorter or empty). Matrix-core path: a workgroup per tile, its waves
+// splitting K.
 Launch plan(const sph_weights* w, int m) {
   Launch L{};
   const int64_t nv = w->k / 8, nt = (w->n + 15) / 16;
@@ -1677,8 +1721,8 @@ Launch plan(const sph_weights* w, int m) {
     const int64_t T = (nt + slots - 1) / slots;
     const int64_t gA = (nt + T - 1) / T;
     const int64_t lA = (T * nc + wpb - 1) / wpb;
-    // ... or balanced ranges spread over all waves of the grid (tiles split across workgroups
-    // meet in global slots); at most ts / wpb workgroups, so that every wave gets a step
+    // ... or ranges of lB steps across the waves of the grid (tiles split across workgroups meet
+    // in the workspace), on at most ts / wpb workgroups
     const int64_t gB = std::max<int64_t>(1, std::min<int64_t>(slots, ts / wpb));
     const int64_t lB = (ts + gB * wpb - 1) / (gB * wpb);
     // whole tiles per workgroup need the parts inside a workgroup to meet in LDS; they are worth
@@ -1692,17 +1736,17 @@ Launch plan(const sph_weights* w, int m) {
     if (aligned) {
       L.grid = (int)gA;
       L.wg_tiles = (int)T;
+      L.wgs = (int)(T * nc);
+      L.wl = (int)lA;
       L.pmax = 0;
       L.ws_bytes = 0;
     } else {
-      L.grid = (int)gB;
+      // the waves that get a step: ceil(ts / lB) <= gB * wpb
+      L.grid = (int)(((ts + lB - 1) / lB + wpb - 1) / wpb);
       L.wg_tiles = 0;
-      L.wq = (int)(ts / (gB * wpb));
-      L.wr = (int)(ts % (gB * wpb));
-      // a wave range holds at least floor(ts / (gB * wpb)) >= 1 steps, so a tile meets at most
-      // nc / that + 2 ranges
-      const int64_t lmin = std::max<int64_t>(1, ts / (gB * wpb));
-      L.pmax = (int)(nc / lmin + 2);
+      L.wl = (int)lB;
+      // every range but the launch's last holds lB steps, so a tile meets at most nc / lB + 2
+      L.pmax = (int)(nc / lB + 2);
       // tagged slots [nt][pmax][M][16], then one arrival counter per tile
       L.cnt_off = ((size_t)nt * L.pmax * M * 16 * 8 + 255) / 256 * 256;
       L.ws_bytes = L.cnt_off + ((size_t)nt * 4 + 255) / 256 * 256;
@@ -1952,8 +1996,10 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
   a.wpb = L.block / 64;
   a.nwg = L.grid;
   a.wg_tiles = L.wg_tiles;
-  a.wq = L.wq;
-  a.wr = L.wr;
+  a.wl = L.wl;
+  a.wgs = L.wgs;
+  div_magic(L.wl, a.wl_m, a.wl_k);
+  div_magic(L.wgs > 0 ? L.wgs : 1, a.wgs_m, a.wgs_k);
   a.pmax = L.pmax;
   a.ts = L.ts;
   if (L.ws_bytes > 0) {

@@ -509,6 +509,29 @@ def test_vector_size_full_size_sampled(fmt):
     assert O.rel_err(y[rows], ref) <= TOL
 
 
+@pytest.mark.parametrize("fmt", ["W2", "W3"])
+@pytest.mark.parametrize("m", [1, 2, 4, 8, 16])
+@pytest.mark.parametrize("n,k", [(16, 65536), (48, 12288), (200, 20480)])
+def test_split_tiles_over_workgroups(fmt, m, n, k):
+    """Long rows spread over many short wave ranges: a tile's parts meet inside a workgroup, across
+    two workgroups (one atomic exchange per value) and across three or more (slots and a counter;
+    n = 16 with k = 65536 puts the one tile over 8 to 32 workgroups). Every batch mode is checked
+    against the oracle, the workspace is zero after each call, and a second call is bitwise equal."""
+    D, V, codes, cb = uniform_case(fmt, n, k, 16)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = synth.activations(m, k, synth.rng(16, m, k, synth.STREAM_X))
+    xd = to_dev_f16(x)
+    call = (lambda: pkg.gemv(w, xd[0])[None]) if m == 1 else (lambda: pkg.gemm_small(w, xd))
+    y1 = call().cpu().numpy()
+    for ws in w.workspaces.values():
+        assert int(torch.count_nonzero(ws)) == 0
+    y2 = call().cpu().numpy()
+    assert np.array_equal(y1, y2)
+    ref = O.gemm(codes, cb, x)
+    assert O.rel_err(y1, ref) <= TOL
+    assert np.all(np.abs(y1 - ref) <= sum_bound(codes, cb, x, k) + 1e-30)
+
+
 @pytest.mark.parametrize("m", [17, 24, 32, 40])
 def test_batch_workspace_left_zero(m):
     """The split-K partials of the batched kernels are cleared by the call that used them, so one

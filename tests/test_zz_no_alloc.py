@@ -33,13 +33,13 @@ def _case(fmt, n, k, m, seed):
 
 
 # (format, n, k, m): each pair is run in this order, the second call on a smaller input, and every
-# call needs the scratch array. The first pairs hand split tiles over through it (rows of 25600
-# weights, whose K spans several workgroups, at batch 1 and 2; the 2^13-entry codebook at batch 9
-# and 16, which always meets in the workspace), the third uses it for the K-split partial outputs
-# of the prefill kernel.
+# call needs the scratch array. The first pair hands split tiles over through it across two
+# workgroups (rows of 25600 weights at batch 1 and 2), the second across three and more (few tiles
+# of long rows at batch 16 and 9, on the 2^13-entry codebook), the third uses it for the K-split
+# partial outputs of the prefill kernel.
 PAIRS = [
     (("W2", 5120, 25600, 1), ("W2", 1024, 25600, 2)),
-    (("W3", 4096, 12288, 16), ("W3", 1024, 4096, 9)),
+    (("W3", 1024, 12288, 16), ("W3", 512, 8192, 9)),
     (("W2", 4096, 12288, 24), ("W2", 1024, 2048, 17)),
 ]
 
@@ -61,11 +61,11 @@ def test_noalloc_matches_workspace_call(first, second):
 
 
 def test_noalloc_refuses_workspace_beyond_scratch():
-    # 51200 x 5120 with the 2^13-entry codebook at batch 16: every split tile meets in the
-    # workspace, which then exceeds the scratch array
-    w, codes, cb, x, xd = _case("W3", 51200, 5120, 16, 45)
+    # 45072 x 5120 at batch 16: 2817 tiles over wave ranges that cross workgroups, three workspace
+    # parts of 256 values per tile, over the scratch array
+    w, codes, cb, x, xd = _case("W2", 45072, 5120, 16, 45)
     assert pkg.workspace_bytes(w, 16) > pkg.sph.NOALLOC_SCRATCH_BYTES
-    out = torch.empty((16, 51200), dtype=torch.float32, device=DEV)
+    out = torch.empty((16, 45072), dtype=torch.float32, device=DEV)
     with pytest.raises(pkg.SphError) as e:
         pkg.gemm_small_noalloc(w, xd, out)
     assert e.value.status == 6

@@ -445,9 +445,14 @@ def main():
                 else:
                     pkg.gemm(copies[li], xd, out=ys[li])
 
-    run_step()                                  # first calls outside capture
-    torch.cuda.synchronize()
+    # first calls outside capture, on the capture streams: the split-tile workspaces are allocated
+    # (zero-filled) per stream, and an allocation inside a capture would add a fill per launch
     stream = torch.cuda.Stream()
+    s2 = torch.cuda.Stream()
+    for st_ in (stream, s2):
+        with torch.cuda.stream(st_):
+            run_step()
+    torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=stream):
         run_step()
@@ -475,7 +480,6 @@ def main():
         for li in range(layers):
             dom_launches.append((copies[li], xd, ys[li]))
     g2 = torch.cuda.CUDAGraph()
-    s2 = torch.cuda.Stream()
     with torch.cuda.graph(g2, stream=s2):
         for w, xd, y in dom_launches:
             if m == 1:

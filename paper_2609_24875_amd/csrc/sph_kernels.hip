@@ -658,10 +658,14 @@ __device__ __forceinline__ SplitGeo split_geo(int gr, int gl, int g) {
   return s;
 }
 
-// Level 2: the group sum `v` of tile t (see above).
+// Level 2: the group sum `v` of tile t (see above). `xpre`: this lane's words of a tile over two
+// workgroups as read before this wave's last step (zero if not read); a word that already holds
+// the other workgroup's sum is used as it stands, without an exchange (that workgroup has
+// finished with it).
 template <int M, int RPL, int MODE>
 __device__ __forceinline__ void group_done(const KArgs& a, int t, const SplitGeo& s,
-                                           const float (&v)[PartIdx<M, RPL, MODE>::N4], int lane) {
+                                           const float (&v)[PartIdx<M, RPL, MODE>::N4],
+                                           const uint64_t (&xpre)[PartIdx<M, RPL, MODE>::N4], int lane) {
   using I = PartIdx<M, RPL, MODE>;
   constexpr int NIDX = M * 16;
   const I ix(lane);
@@ -675,7 +679,9 @@ __device__ __forceinline__ void group_done(const KArgs& a, int t, const SplitGeo
     uint64_t o[I::N4];   // all exchanges in flight together
 #pragma unroll
     for (int i = 0; i < I::N4; ++i)
-      o[i] = __hip_atomic_exchange(slots + ix.idx[i], slot_word(v[i]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      o[i] = (xpre[i] >> 32)
+                 ? xpre[i]
+                 : __hip_atomic_exchange(slots + ix.idx[i], slot_word(v[i]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
     for (int i = 0; i < I::N4; ++i)
       if (o[i] >> 32) {
@@ -757,7 +763,8 @@ struct LocalRead {
 // keeps the wave from hanging, marking the sums invalid (NaN) if it were ever reached.
 template <int M, int RPL, int MODE>
 __device__ __forceinline__ void leader_collect(const KArgs& a, int t, const SplitGeo& s, const WgHo<M>* ho,
-                                               const float (&own)[PartIdx<M, RPL, MODE>::N4], int lane) {
+                                               const float (&own)[PartIdx<M, RPL, MODE>::N4],
+                                               const uint64_t (&xpre)[PartIdx<M, RPL, MODE>::N4], int lane) {
   using I = PartIdx<M, RPL, MODE>;
   using L = LocalRead<M>;
   constexpr int NIDX = L::NIDX, PPI = L::PPI, IPP = L::IPP, JB = L::JB;
@@ -803,7 +810,7 @@ __device__ __forceinline__ void leader_collect(const KArgs& a, int t, const Spli
     }
     tot[i] = ok ? own[i] + other : __builtin_nanf("");
   }
-  group_done<M, RPL, MODE>(a, t, s, tot, lane);
+  group_done<M, RPL, MODE>(a, t, s, tot, xpre, lane);
 }
 
 // A part whose tile work is left for after the step loop (a range's first part, emitted inside it):
@@ -825,7 +832,8 @@ using PendingOf = Pending<LDS_HO ? 1 : PartIdx<M, RPL, MODE>::N4>;
 template <int M, int RPL, int MODE, bool LDS_HO, bool FINAL>
 __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[MODE == 2 ? M / 16 : M][RPL], int t, int ca,
                                           int cb, int g, int gr, int gl, int lane, WgHo<M>* ho,
-                                          PendingOf<M, RPL, MODE, LDS_HO>& pend) {
+                                          PendingOf<M, RPL, MODE, LDS_HO>& pend,
+                                          const uint64_t (&xpre)[PartIdx<M, RPL, MODE>::N4]) {
   using I = PartIdx<M, RPL, MODE>;
   constexpr int H = 16 / RPL;
   float vals[I::NVAL];
@@ -858,8 +866,8 @@ __device__ __forceinline__ void emit_part(const KArgs& a, float (&acc)[MODE == 2
     return;
   }
   if constexpr (FINAL) {
-    if (LDS_HO && s.nl > 1) leader_collect<M, RPL, MODE>(a, t, s, ho, v4, lane);
-    else group_done<M, RPL, MODE>(a, t, s, v4, lane);
+    if (LDS_HO && s.nl > 1) leader_collect<M, RPL, MODE>(a, t, s, ho, v4, xpre, lane);
+    else group_done<M, RPL, MODE>(a, t, s, v4, xpre, lane);
   } else {
     pend.t = t;
     pend.kind = (LDS_HO && s.nl > 1) ? 2 : 1;
@@ -886,10 +894,12 @@ __device__ __forceinline__ void follow_up(const KArgs& a, int g, int gr, int gl,
     float v[I::N4];
 #pragma unroll
     for (int i = 0; i < I::N4; ++i) v[i] = ix.writer ? ho->slot[g % VALU_WPB][ix.idx[i]] : 0.0f;
-    if (pend.kind == 2) leader_collect<M, RPL, MODE>(a, pend.t, s, ho, v, lane);
-    else group_done<M, RPL, MODE>(a, pend.t, s, v, lane);
+    const uint64_t none[I::N4] = {};
+    if (pend.kind == 2) leader_collect<M, RPL, MODE>(a, pend.t, s, ho, v, none, lane);
+    else group_done<M, RPL, MODE>(a, pend.t, s, v, none, lane);
   } else {
-    group_done<M, RPL, MODE>(a, pend.t, s, pend.v, lane);
+    const uint64_t none[I::N4] = {};
+    group_done<M, RPL, MODE>(a, pend.t, s, pend.v, none, lane);
   }
 }
 
@@ -1026,6 +1036,8 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   const int nsteps = s_end - s_begin;
   const int npairs = (nsteps - 1) >> 1;
   PendingOf<M, RPL, MODE, LDS_HO> pend;
+  using PI = PartIdx<M, RPL, MODE>;
+  const uint64_t xnone[PI::N4] = {};         // no workspace words read ahead (parts inside the loop)
   int t = t0, c = c0;                        // position of step 2i
   for (int i = 0; i < npairs; ++i) {
     int t1 = t, c1 = c + 1;
@@ -1035,7 +1047,7 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
     }
     S::load(r1, a, t1, c1, h, vloc, lane);
     S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c1 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, gr0, gl0, lane, ho, pend);
+    if (c1 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, gr0, gl0, lane, ho, pend, xnone);
     int t2 = t1, c2 = c1 + 1;
     if (c2 == a.nc) {
       ++t2;
@@ -1043,7 +1055,7 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
     }
     S::load(r0, a, t2, c2, h, vloc, lane);   // step 2i + 2 <= nsteps - 1 exists
     S::compute(r1, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (c2 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, gr0, gl0, lane, ho, pend);
+    if (c2 == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t1, t1 == t0 ? c0 : 0, a.nc, g, gr0, gl0, lane, ho, pend, xnone);
     t = t2;
     c = c2;
   }
@@ -1057,14 +1069,29 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
     }
     S::load(r1, a, tf, cf, h, vloc, lane);
     S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-    if (cf == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, gr0, gl0, lane, ho, pend);
+    if (cf == 0) emit_part<M, RPL, MODE, LDS_HO, false>(a, acc, t, t == t0 ? c0 : 0, a.nc, g, gr0, gl0, lane, ho, pend, xnone);
   }
   const int caf = tf == t0 ? c0 : 0;
   // one instance of the step code for the last step: its records are moved into r0 when r1 holds
   // them (a reference chosen between the two buffers would put both in scratch memory)
   if (nsteps - 2 * npairs == 2) r0 = r1;
+  // The final part's tile over two workgroups, finished from this wave (its only part in this
+  // workgroup, or the local leader): read its workspace words now, so that their round trip
+  // overlaps the last step; if the other workgroup has already left its sums there, this wave
+  // finishes the tile without an exchange at the end.
+  uint64_t xw[PI::N4] = {};
+  if (!(caf == 0 && cf + 1 == a.nc)) {
+    const SplitGeo sl = split_geo<LDS_HO>(grl, gll, g);
+    if (sl.ngrp == 2 && (sl.nl == 1 || g == sl.lw0)) {
+      const PI ix(lane);
+      const uint64_t* words = a.ws_slot + (int64_t)tf * a.pmax * (M * 16);
+#pragma unroll
+      for (int i = 0; i < PI::N4; ++i)
+        xw[i] = ix.writer ? __hip_atomic_load(words + ix.idx[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+    }
+  }
   S::compute(r0, acc, lds, mask_off, pstage, lane, h, vloc);
-  emit_part<M, RPL, MODE, LDS_HO, true>(a, acc, tf, caf, cf + 1, g, grl, gll, lane, ho, pend);
+  emit_part<M, RPL, MODE, LDS_HO, true>(a, acc, tf, caf, cf + 1, g, grl, gll, lane, ho, pend, xw);
   follow_up<M, RPL, MODE, LDS_HO>(a, g, gr0, gl0, lane, ho, pend);
 }
 

@@ -207,6 +207,10 @@ def _workspace(w: SphWeights, m: int, device, stream=None):
     key = (m, _stream_handle(stream))
     ws = w.workspaces.get(key)
     if ws is None or ws.numel() < nb:
+        if torch.cuda.is_current_stream_capturing():
+            # a zero-filled allocation here would put a fill into the graph ahead of every launch
+            raise RuntimeError("no workspace for this (batch, stream) yet: make one call on the "
+                               "capture stream before capturing a graph")
         ws = torch.zeros(nb, dtype=torch.uint8, device=device)
         w.workspaces[key] = ws
     return ws, nb

@@ -509,6 +509,39 @@ def test_vector_size_full_size_sampled(fmt):
     assert O.rel_err(y[rows], ref) <= TOL
 
 
+def test_graph_capture_replays():
+    """A decode call whose split tiles meet in the workspace, captured into a HIP graph on a stream
+    that has made one eager call (so its workspace exists before the capture): every replay, with
+    other eager work and synchronizations between them, gives the eager result bit for bit. A
+    capture on a stream without a workspace is refused rather than recording an allocation."""
+    D, V, codes, cb = uniform_case("W2", 1024, 25600, 17)
+    w = pkg.pack(D, V, codes, cb, device=DEV)
+    assert pkg.workspace_bytes(w, 1) > 0
+    x = to_dev_f16(synth.activations(1, 25600, synth.rng(17, synth.STREAM_X)))[0]
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        y_eager = pkg.gemv(w, x).clone()
+    torch.cuda.synchronize()
+    y = torch.empty_like(y_eager)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        pkg.gemv(w, x, out=y)
+    for i in range(4):
+        y.fill_(float("nan"))
+        pkg.gemv(w, x)                      # eager work on the default stream between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, y_eager), i
+    y_np = y.cpu().numpy()
+    assert O.rel_err(y_np, O.gemv(codes, cb, synth.activations(1, 25600, synth.rng(17, synth.STREAM_X)))) <= TOL
+    s2 = torch.cuda.Stream()
+    with pytest.raises(RuntimeError, match="capture stream"):
+        with torch.cuda.graph(torch.cuda.CUDAGraph(), stream=s2):
+            pkg.gemv(w, x, out=y)
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("fmt", ["W2", "W3"])
 @pytest.mark.parametrize("m", [1, 2, 4, 8, 16])
 @pytest.mark.parametrize("n,k", [(16, 65536), (48, 12288), (200, 20480)])

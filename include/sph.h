@@ -153,8 +153,9 @@ sph_status sph_gemm_small_noalloc(const sph_weights* w, const void* d_x, int64_t
 /* Device workspace needed by sph_gemv (m = 1), sph_gemm_small or sph_gemm for this matrix and
  * batch (1 <= m <= 65536) on the current device (0 when the call needs none; d_ws may then be
  * NULL). For m <= 16 it holds the partial sums of 16-row tiles whose K range is split between
- * workgroups (a 64-bit slot per part and value: fp32 sum and a valid flag) and one 32-bit arrival
- * counter per tile; above m = 16 it holds fp32 partial outputs of a K split. It must be 256-byte
+ * workgroups: 64-bit words (fp32 sum and a valid flag), one per value of a tile over two
+ * workgroups, one per workgroup and value of a tile over more, and one 32-bit arrival counter per
+ * tile; above m = 16 it holds fp32 partial outputs of a K split. It must be 256-byte
  * aligned and zero-filled before its first use, and every call leaves it zero-filled again (above
  * m = 32 it needs no initial contents, but is still left zero-filled). Calls that may run
  * concurrently must not share one. No call waits for another workgroup to make progress, so calls

@@ -496,9 +496,11 @@ struct Step {
 // gfx950 half-swap (v_permlane32_swap / v_permlane16_swap exchange the upper half of the first
 // register with the lower half of the second, at 32- or 16-lane granularity) and an add, all on
 // the vector ALU. The swap is written in assembly because this compiler version returns the
-// first register twice from the builtin's result pair; the leading s_nop gives the two wait
-// states the instruction needs after a vector write of its operands, which the compiler cannot
-// see through the assembly, and the trailing one is conservative.
+// first register twice from the builtin's result pair. The compiler cannot see hazards through
+// the assembly, so it carries its own wait states: the leading s_nop 1 (two wait states) is what
+// the compiler's hazard recognizer puts between a vector write of an operand and this
+// instruction when it emits the builtin itself; it puts none after it, and the trailing s_nop is
+// a margin of two cycles.
 template <int DIST>
 __device__ __forceinline__ float xchg_add(float lo_keep, float hi_keep, int lane) {
   (void)lane;

@@ -40,9 +40,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source and compile flags the counters were taken with: any change to
 # the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "3878bb033e7ff7cd04bdaee5f92a37ebbd8319366ae1ceca0699b3630587cad2": {
-        "7168x5120-m1": 11953809, "5120x5120-m1": 8669106,
-        "51200x5120-m1": 82695833, "5120x25600-m1": 42932950},
+    "c3980b3fed5368d0ac9a6a290f911d205f8cb61ee8b2a1661933c0c30e2ff2e7": {
+        "7168x5120-m1": 11917939, "5120x5120-m1": 8633007,
+        "51200x5120-m1": 82629794, "5120x25600-m1": 42250021},
 }
 
 

@@ -982,7 +982,7 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   // split-tile parts of waves of the same workgroup meet in LDS when it has room
   constexpr bool LDS_HO = lds_handover_fits(KIND, D, M, MODE);
   static_assert(VALU_WPB == 16, "lds_handover_fits assumes 16 waves per workgroup");
-  static_assert(LDS_HO || MODE == 2, "only the tile variant may hand over through the workspace alone");
+  static_assert(LDS_HO, "the LDS holds the tables and the split-tile hand-over slots");
   __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes];
   __shared__ __align__(16) uint32_t pstage_all[MODE == 2 ? 1 : VALU_WPB * 64];
   __shared__ __align__(16) unsigned char ho_raw[LDS_HO ? sizeof(WgHo<M>) : 4];

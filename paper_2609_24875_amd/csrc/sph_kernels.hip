@@ -1275,8 +1275,20 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
   PfPre<KIND, MC> pre;
   pf_fetch<KIND, MC>(pre, a, t0, mc0, c0);
   {
-    const int n16 = (int)((Tables<KIND, D>::bytes - (IS_CB<KIND> ? 128u : 0u)) / 16u);
-    for (int t = threadIdx.x; t < n16; t += PF_THREADS) ((uint4*)lds)[t] = a.T[t];
+    // the tables in batches of up to 8 loads per thread, each batch one round trip
+    constexpr int n16 = (int)((Tables<KIND, D>::bytes - (IS_CB<KIND> ? 128u : 0u)) / 16u);
+    constexpr int TPER = (n16 + PF_THREADS - 1) / PF_THREADS, TB = TPER < 8 ? TPER : 8;
+#pragma unroll
+    for (int p0 = 0; p0 < TPER; p0 += TB) {
+      uint4 tv[TB];
+#pragma unroll
+      for (int p = 0; p < TB; ++p) tv[p] = a.T[min((int)threadIdx.x + PF_THREADS * (p0 + p), n16 - 1)];
+#pragma unroll
+      for (int p = 0; p < TB; ++p) {
+        const int t = (int)threadIdx.x + PF_THREADS * (p0 + p);
+        if (t < n16) ((uint4*)lds)[t] = tv[p];
+      }
+    }
     if constexpr (IS_CB<KIND>) {
       if (threadIdx.x < 16) {
         const uint32_t sm = threadIdx.x;
@@ -1384,18 +1396,22 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
 }
 
 // y[b][row] = sum over the K ranges, in range order, of the prefill partials, which are cleared.
+// Four consecutive rows per thread, so that every access to the partials is 16 bytes wide (the
+// rows are padded to whole tiles, and a range's partials start on a 64-byte boundary).
 __global__ void __launch_bounds__(256) k_prefill_reduce(KArgs a) {
+  const int64_t npad = (int64_t)a.nt * 16, nq = npad / 4;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t npad = (int64_t)a.nt * 16;
-  if (t >= (int64_t)a.m * a.n) return;
-  const int b = (int)(t / a.n), row = (int)(t % a.n);
-  float s = 0.0f;
+  if (t >= (int64_t)a.m * nq) return;
+  const int b = (int)(t / nq), row = (int)(t % nq) * 4;
+  f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
   for (int z = 0; z < a.ks; ++z) {
-    float* p = a.ws_part + ((int64_t)z * a.m + b) * npad + row;
+    f32x4* p = (f32x4*)(a.ws_part + ((int64_t)z * a.m + b) * npad + row);
     s += *p;
-    *p = 0.0f;   // the workspace is left zero-filled, as the batch 1..32 calls promise
+    *p = f32x4{0.0f, 0.0f, 0.0f, 0.0f};   // the workspace is left zero-filled, as every call promises
   }
-  store_y(a, b, row, s);
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (row + e < a.n) store_y(a, b, row + e, s[e]);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1707,11 +1723,11 @@ PrefillPlan prefill_plan(const sph_weights* w, int64_t m) {
   P.gy = (int)((m + mc - 1) / mc);
   P.mc = mc;
   const int64_t g = (int64_t)P.gx * P.gy, cus = num_cus();
-  // a split pays only while the doubled grid still fits in one round on the CUs
-  int64_t ks = 1;
-  while (g * ks * 2 <= cus && ks * 2 <= ng && ks < 8) ks *= 2;
-  P.ks = (int)ks;
-  P.ws_bytes = ks > 1 ? (size_t)ks * m * nt * 16 * sizeof(float) : 0;
+  // K is split as far as the grid still fits in one round on the CUs (at most 16 ranges, each at
+  // least one chunk): a small grid otherwise leaves CUs idle (4096x12288 at 32 batch rows ran on
+  // half of them with splits limited to powers of two up to 8, 17-18% slower)
+  P.ks = (int)std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(cus / g, ng), 16));
+  P.ws_bytes = P.ks > 1 ? (size_t)P.ks * m * nt * 16 * sizeof(float) : 0;
   return P;
 }
 
@@ -1808,7 +1824,7 @@ sph_status launch_prefill(const sph_weights* w, const void* d_x, int64_t m, int6
   if (hipLaunchKernel(fn, dim3(P.gx, P.gy, P.ks), dim3(PF_THREADS), kargs, 0, s) != hipSuccess) return SPH_ERR_HIP;
   if (hipGetLastError() != hipSuccess) return SPH_ERR_HIP;
   if (P.ks > 1) {
-    const int64_t total = (int64_t)m * w->n;
+    const int64_t total = (int64_t)m * ((w->n + 15) / 16) * 4;   // four rows per thread
     if (hipLaunchKernel((const void*)k_prefill_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), kargs, 0, s) !=
         hipSuccess)
       return SPH_ERR_HIP;

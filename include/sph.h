@@ -119,8 +119,9 @@ sph_status sph_gemv(const sph_weights* w, const void* d_x, void* d_y, sph_dtype 
  * 4x4x4 MFMA blocks, one vector per block, each block's sum times the fp32 radius; batches 9..32
  * on 16x16x32 MFMA tiles with Eq. 7 factored over each 128-weight group, offset * sum <t, x> +
  * step * sum q <t, x>, where t (the signed direction) and q * t (split exactly into two fp16
- * numbers) are the operands (9..16 inside the step plan, 17..32 in the prefill kernel of sph_gemm
- * with 32 activation rows staged in LDS). Asynchronous on `stream`. */
+ * numbers) are the operands (9..16 inside the step plan; 17..32, and 9..16 on matrices of about
+ * 10^8 weights or more, in the prefill kernel of sph_gemm with 16 or 32 activation rows staged in
+ * LDS). Asynchronous on `stream`. */
 sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y,
                           int64_t ldy, sph_dtype y_dtype, void* d_ws, size_t ws_bytes,
                           void* stream);
@@ -155,7 +156,8 @@ sph_status sph_gemm_small_noalloc(const sph_weights* w, const void* d_x, int64_t
  * NULL). For m <= 16 it holds the partial sums of 16-row tiles whose K range is split between
  * workgroups: 64-bit words (fp32 sum and a valid flag), one per value of a tile over two
  * workgroups, one per workgroup and value of a tile over more, and one 32-bit arrival counter per
- * tile; above m = 16 it holds fp32 partial outputs of a K split. It must be 256-byte
+ * tile; where the prefill kernel runs (m above 16, and 9..16 on large matrices: see
+ * sph_gemm_small) it holds fp32 partial outputs of a K split. It must be 256-byte
  * aligned and zero-filled before its first use, and every call leaves it zero-filled again (above
  * m = 32 it needs no initial contents, but is still left zero-filled). Calls that may run
  * concurrently must not share one. No call waits for another workgroup to make progress, so calls

@@ -13,10 +13,11 @@
 //    reproducible. Batch 2 runs the same way with two rows of products (except with the 2^13
 //    codebook); batches up to 8 decode the same records, 4 lanes per vector position, into
 //    4x4x4 MFMA blocks;
-//  - matrix-core tile path (batch 9..16): each lane decodes one (row, vector) into the A operand
-//    of v_mfma_f32_16x16x32_f16 (weights rounded once to fp16), activations form the B operand;
-//  - prefill (batch above 16): workgroups rebuild their tiles once per K-chunk and multiply them
-//    with activations staged in LDS on the same 16x16x32 MFMA;
+//  - matrix-core tile path (batch 9..16): each lane decodes one (row, vector) into exact fp16
+//    A operands of v_mfma_f32_16x16x32_f16 (Eq. 7 factored over a group), activations form the
+//    B operand;
+//  - prefill (batch above 16, and 9..16 on large matrices): workgroups rebuild their tiles once
+//    per K-chunk and multiply them with activations staged in LDS on the same 16x16x32 MFMA;
 //  - 4-D and 16-D vectors: row-planar kernels, one wave per output row.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -1133,7 +1134,7 @@ __global__ void __launch_bounds__(256) k_unpack(KArgs a, uint8_t* signs, uint16_
 }
 
 // ------------------------------------------------------------------------------------------
-// Prefill kernel (batch > 16): Y = X W^T on 16x16x32 MFMA tiles with the operands rebuilt once per
+// Prefill kernel (batch > 16, and 9..16 on large matrices): Y = X W^T on 16x16x32 MFMA tiles with the operands rebuilt once per
 // workgroup and k-chunk.
 //
 // A workgroup of PF_WAVES waves owns PF_TPW 16-row tiles per wave and MC batch rows (one grid
@@ -1637,13 +1638,27 @@ const void* pick(int D, int V, int M, int rpl1) {
 
 template <int KIND, int D>
 const void* prefill_fn_mc(int mc) {
+  if (mc == 16) return (const void*)k_gemm_prefill<KIND, D, 16>;
   if (mc == 32) return (const void*)k_gemm_prefill<KIND, D, 32>;
   return (const void*)k_gemm_prefill<KIND, D, 64>;
 }
 
-// Batch rows per workgroup: 32 for batches 17..32, else 64 (the two fp32 sums of the factored
-// product double the accumulators, which 128 rows would not leave room for).
-int prefill_mc(int, int, int64_t m) { return m <= 32 ? 32 : 64; }
+// Batch rows per workgroup: 16 for batches 9..16, 32 for 17..32, else 64 (the two fp32 sums of
+// the factored product double the accumulators, which 128 rows would not leave room for).
+int prefill_mc(int, int, int64_t m) { return m <= 16 ? 16 : m <= 32 ? 32 : 64; }
+
+// Batches 17..32 always, and 9..16 on large matrices, run on the prefill kernel, whose activations
+// are staged in LDS once per workgroup and chunk and shared by its 16 row tiles; in the 16x16x32
+// tile mode every wave reloads them. Past about 10^8 weights the reloads cost more than the
+// staging: at 16 batch rows 51200x5120 takes 81 us in the tile mode and 63 us on the prefill
+// kernel, 24576x4096 34.0 and 31.8 us, while 12288x4096 stays faster in the tile mode (18.9
+// against 19.8 us); at 9 batch rows the prefill kernel gains 6-13% from about 1.3 * 10^8.
+bool small_on_prefill(const sph_weights* w, int64_t m) {
+  if (m > 16) return true;
+  if (m < 9) return false;
+  const int64_t weights = (int64_t)w->n * w->k;
+  return weights >= (m >= 13 ? 96ll : 120ll) << 20;
+}
 
 const void* prefill_fn(int D, int V, int mc) {
   switch (sph_kind_of(D, V)) {
@@ -1748,9 +1763,9 @@ Launch plan(const sph_weights* w, int m) {
   const int kind = sph_kind_of(w->fmt.dir_bits, w->fmt.radius_bits);
   const int cus = num_cus();
   // batch 1: vector ALU; 2..8: 4x4x4 MFMA blocks on the same records (4 lanes per vector
-  // position); 9..16: 16x16x32 MFMA tiles (lane = row x position group). The batched variants
-  // round each rebuilt weight to fp16. All share the step plan below (16 positions per step for
-  // the batched variants, 64 or 32 for batch 1). Larger batches run on the prefill kernel.
+  // position); 9..16: 16x16x32 MFMA tiles (lane = row x position group). Every variant forms
+  // exact fp16 products. All share the step plan below (16 positions per step for the batched
+  // variants, 64 or 32 for batch 1). Larger batches run on the prefill kernel.
   if (m <= 16) {
     // batch 2 on the vector ALUs as well (exact products), except for the codebook kinds, whose
     // two-row kernel would spill
@@ -1800,7 +1815,7 @@ Launch plan(const sph_weights* w, int m) {
   return L;
 }
 
-// The prefill kernel (and its split-K reduction) for a validated call with m > 16.
+// The prefill kernel (and its split-K reduction) for a validated call.
 sph_status launch_prefill(const sph_weights* w, const void* d_x, int64_t m, int64_t ldx, void* d_y, int64_t ldy,
                           sph_dtype y_dtype, void* d_ws, size_t ws_bytes, hipStream_t s) {
   const PrefillPlan P = prefill_plan(w, m);
@@ -1981,7 +1996,7 @@ sph_status sph_workspace_bytes(const sph_weights* w, int64_t m, size_t* bytes) {
     *bytes = 0;
     return SPH_OK;
   }
-  *bytes = m <= 16 ? plan(w, (int)m).ws_bytes : prefill_plan(w, m).ws_bytes;
+  *bytes = small_on_prefill(w, m) ? prefill_plan(w, m).ws_bytes : plan(w, (int)m).ws_bytes;
   return SPH_OK;
 }
 
@@ -2026,9 +2041,7 @@ sph_status sph_gemm_small(const sph_weights* w, const void* d_x, int64_t m, int6
       return SPH_ERR_HIP;
     return hipGetLastError() == hipSuccess ? SPH_OK : SPH_ERR_HIP;
   }
-  // batches 17..32: the prefill kernel with 32 batch rows per workgroup (its activations staged
-  // in LDS and shared by 16 row tiles) moves less activation traffic than the tile mode
-  if (m > 16) return launch_prefill(w, d_x, m, ldx, d_y, ldy, y_dtype, d_ws, ws_bytes, (hipStream_t)stream);
+  if (small_on_prefill(w, m)) return launch_prefill(w, d_x, m, ldx, d_y, ldy, y_dtype, d_ws, ws_bytes, (hipStream_t)stream);
   const Launch L = plan(w, (int)m);
   if (!L.fn) return SPH_ERR_UNSUPPORTED_FORMAT;
   if (L.ws_bytes > 0) {

@@ -335,6 +335,12 @@ FULL = [
     ("W2", 5120, 25600, "varied", 4),        # 32B-class down, batch 4
     ("W2", 12288, 4096, "varied", 32),       # matrix-core path
     ("W3", 4096, 12288, "varied", 16),
+    # batches 9..16 on matrices of about 10^8 weights or more run on the prefill kernel (16 batch
+    # rows per workgroup); just below the bound they stay in the tile mode
+    ("W3", 24576, 4096, "varied", 16),       # 96 * 2^20 weights: prefill at 13..16
+    ("W2", 32768, 4096, "varied", 12),       # 128 * 2^20: prefill at 9..12
+    ("W2", 24576, 4096, "varied", 12),       # below 120 * 2^20: tile mode at 9..12
+    ("W2", 5120, 25600, "varied", 9),        # 125 * 2^20, just above the 9..12 bound
 ]
 
 
@@ -357,10 +363,11 @@ def test_full_size_sampled(fmt, n, k, kind, m):
 
 
 # Encoded outlier-laden matrices at the benchmark configurations' full sizes, every output
-# compared: the 32B-class gate/up (fused) and down projections at batch 1, 2, 4 and 8; the
-# 12288x4096 and 4096x12288 projections in both formats at batch 1, 16 and 32.
+# compared: the 32B-class gate/up (fused) and down projections at batch 1, 2, 4 and 8 (and the
+# gate/up at 16, on the prefill kernel); the 12288x4096 and 4096x12288 projections in both
+# formats at batch 1, 16 and 32.
 ENCODED_FULL = (
-    [("W2", 51200, 5120, m) for m in (1, 2, 4, 8)]
+    [("W2", 51200, 5120, m) for m in (1, 2, 4, 8, 16)]
     + [("W2", 5120, 25600, m) for m in (1, 2, 4, 8)]
     + [(f, n, k, m) for f in ("W2", "W3") for (n, k) in ((12288, 4096), (4096, 12288)) for m in (1, 16, 32)]
 )

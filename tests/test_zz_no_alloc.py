@@ -61,11 +61,11 @@ def test_noalloc_matches_workspace_call(first, second):
 
 
 def test_noalloc_refuses_workspace_beyond_scratch():
-    # 45072 x 5120 at batch 16: 2817 tiles over wave ranges that cross workgroups, three workspace
-    # parts of 256 values per tile, over the scratch array
-    w, codes, cb, x, xd = _case("W2", 45072, 5120, 16, 45)
-    assert pkg.workspace_bytes(w, 16) > pkg.sph.NOALLOC_SCRATCH_BYTES
-    out = torch.empty((16, 45072), dtype=torch.float32, device=DEV)
+    # 172160 x 3584 (a vocabulary-sized projection) at batch 8: 10760 tiles over wave ranges that
+    # cross workgroups, two workspace parts of 128 values per tile, over the scratch array
+    w, codes, cb, x, xd = _case("W2", 172160, 3584, 8, 45)
+    assert pkg.workspace_bytes(w, 8) > pkg.sph.NOALLOC_SCRATCH_BYTES
+    out = torch.empty((8, 172160), dtype=torch.float32, device=DEV)
     with pytest.raises(pkg.SphError) as e:
         pkg.gemm_small_noalloc(w, xd, out)
     assert e.value.status == 6

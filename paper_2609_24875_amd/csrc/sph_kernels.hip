@@ -1398,18 +1398,29 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
 
 // y[b][row] = sum over the K ranges, in range order, of the prefill partials, which are cleared.
 // Four consecutive rows per thread, so that every access to the partials is 16 bytes wide (the
-// rows are padded to whole tiles, and a range's partials start on a 64-byte boundary).
+// rows are padded to whole tiles, and a range's partials start on a 64-byte boundary). All of a
+// thread's partials are read before any is cleared: read-add-clear per range made each read wait
+// for the previous range's store (the compiler cannot tell the addresses apart), one memory round
+// trip per range.
 __global__ void __launch_bounds__(256) k_prefill_reduce(KArgs a) {
+  constexpr int KS_MAX = 16;   // the plan splits K into at most this many ranges
   const int64_t npad = (int64_t)a.nt * 16, nq = npad / 4;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= (int64_t)a.m * nq) return;
   const int b = (int)(t / nq), row = (int)(t % nq) * 4;
-  f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int z = 0; z < a.ks; ++z) {
-    f32x4* p = (f32x4*)(a.ws_part + ((int64_t)z * a.m + b) * npad + row);
-    s += *p;
-    *p = f32x4{0.0f, 0.0f, 0.0f, 0.0f};   // the workspace is left zero-filled, as every call promises
-  }
+  f32x4* p0 = (f32x4*)(a.ws_part + (int64_t)b * npad + row);
+  const int64_t zs = (int64_t)a.m * nq;   // f32x4 elements between consecutive ranges
+  f32x4 v[KS_MAX];   // the kernel runs only for ks >= 2
+#pragma unroll
+  for (int z = 0; z < KS_MAX; ++z)
+    if (z < 2 || z < a.ks) v[z] = p0[z * zs];
+  f32x4 s = v[0];
+#pragma unroll
+  for (int z = 1; z < KS_MAX; ++z)
+    if (z < 2 || z < a.ks) s += v[z];
+#pragma unroll
+  for (int z = 0; z < KS_MAX; ++z)
+    if (z < 2 || z < a.ks) p0[z * zs] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};   // left zero-filled, as every call promises
 #pragma unroll
   for (int e = 0; e < 4; ++e)
     if (row + e < a.n) store_y(a, b, row + e, s[e]);
@@ -1741,7 +1752,7 @@ PrefillPlan prefill_plan(const sph_weights* w, int64_t m) {
   // K is split as far as the grid still fits in one round on the CUs (at most 16 ranges, each at
   // least one chunk): a small grid otherwise leaves CUs idle (4096x12288 at 32 batch rows ran on
   // half of them with splits limited to powers of two up to 8, 17-18% slower)
-  P.ks = (int)std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(cus / g, ng), 16));
+  P.ks = (int)std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(cus / g, ng), 16));   // k_prefill_reduce's KS_MAX
   P.ws_bytes = P.ks > 1 ? (size_t)P.ks * m * nt * 16 * sizeof(float) : 0;
   return P;
 }

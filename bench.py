@@ -40,9 +40,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source and compile flags the counters were taken with: any change to
 # the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "c3980b3fed5368d0ac9a6a290f911d205f8cb61ee8b2a1661933c0c30e2ff2e7": {
-        "7168x5120-m1": 11917939, "5120x5120-m1": 8633007,
-        "51200x5120-m1": 82629794, "5120x25600-m1": 42250021},
+    "f63c83086af7606bcaec6c96167f3513cc2acdb5242bf94c51ae4f1fe827d13b": {
+        "7168x5120-m1": 11905763, "5120x5120-m1": 8620766,
+        "51200x5120-m1": 82626892, "5120x25600-m1": 42246094},
 }
 
 

@@ -166,10 +166,10 @@ LLM32B_SHAPES = (("q", 5120, 5120), ("k", 1024, 5120), ("v", 1024, 5120), ("o", 
                  ("gate", 25600, 5120), ("up", 25600, 5120), ("down", 5120, 25600))
 
 WORKLOADS = {
-    0: Workload("w2-1024x1024-m1", "W2", (("w", 1024, 1024),), 1, (1,), "uniform"),
-    1: Workload("w2-4096x4096-m1", "W2", (("w", 4096, 4096),), 1, (1,), "encoded"),
-    2: Workload("w3-8b-class-36L-m1", "W3", LLM8B_SHAPES, 36, (1,), "encoded"),
+    0: Workload("w2-1024x1024", "W2", (("w", 1024, 1024),), 1, (1,), "uniform"),
+    1: Workload("w2-4096x4096", "W2", (("w", 4096, 4096),), 1, (1,), "encoded"),
+    2: Workload("w3-8b-class-36L", "W3", LLM8B_SHAPES, 36, (1,), "encoded"),
     3: Workload("w2-32b-class-64L", "W2", LLM32B_SHAPES, 64, (1, 2, 4, 8), "encoded"),
-    4: Workload("w2w3-12288x4096-m16-32", "W2",
+    4: Workload("w2w3-12288x4096-4096x12288", "W2",
                 (("up", 12288, 4096), ("down", 4096, 12288)), 1, (16, 32), "encoded"),
 }

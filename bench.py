@@ -177,36 +177,45 @@ def cpu_model() -> str:
 def read_ceiling(torch, dev, nbytes=2 << 30, reps=10):
     """Plain streaming-read bandwidth of this GPU (libsph_probe.so, a measurement probe outside
     the library): GB/s of one launch over a buffer far larger than the Infinity Cache, from HIP
-    events on the probe's stream, best of two grids. None if the probe is not built."""
+    events on the probe's stream; the best of three access patterns (grid stride, contiguous
+    8 KiB blocks per wave, one contiguous slice per workgroup) at two grid sizes, each pattern's
+    best reported too. None if the probe is not built."""
     import ctypes
     from paper_2609_24875_amd import build as B
     if not os.path.exists(B.PROBE_OUT):
         return None
     lib = ctypes.CDLL(B.PROBE_OUT)
-    lib.sph_probe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p,
-                                          ctypes.c_uint32, ctypes.c_void_p]
+    lib.sph_probe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p]
     never = 0x9E3779B9   # every word is 1, so each thread's XOR fold is 0 or 1
     buf = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
     flag = torch.zeros(1, dtype=torch.int32, device=dev)
     st = torch.cuda.Stream()
-    best = 0.0
-    for grid in (4096, 16384):
-        with torch.cuda.stream(st):
-            for _ in range(2):
-                lib.sph_probe_stream_read(buf.data_ptr(), nbytes, grid, flag.data_ptr(), never, st.cuda_stream)
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(st)
-            for _ in range(reps):
-                if lib.sph_probe_stream_read(buf.data_ptr(), nbytes, grid, flag.data_ptr(), never, st.cuda_stream) != 0:
-                    return None
-            e1.record(st)
-        torch.cuda.synchronize()
-        best = max(best, nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    names = ("grid stride", "wave blocks of 8 KiB", "workgroup slices")
+    per = {}
+    for pattern, name in enumerate(names):
+        for grid in (4096, 16384):
+            with torch.cuda.stream(st):
+                for _ in range(2):
+                    lib.sph_probe_stream_read(buf.data_ptr(), nbytes, grid, pattern, flag.data_ptr(), never,
+                                              st.cuda_stream)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(st)
+                for _ in range(reps):
+                    if lib.sph_probe_stream_read(buf.data_ptr(), nbytes, grid, pattern, flag.data_ptr(), never,
+                                                 st.cuda_stream) != 0:
+                        return None
+                e1.record(st)
+            torch.cuda.synchronize()
+            gbs = nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+            per[name] = round(max(per.get(name, 0.0), gbs), 1)
     del buf, flag
     torch.cuda.empty_cache()
-    return {"GB/s": round(best, 1), "bytes": nbytes, "frac_of_peak": round(best / HBM_PEAK_GBS, 4),
-            "kernel": "plain streaming read, 16-byte loads, grid-stride (libsph_probe.so)"}
+    best = max(per.values())
+    return {"GB/s": best, "bytes": nbytes, "frac_of_peak": round(best / HBM_PEAK_GBS, 4),
+            "kernel": "plain streaming read, 16-byte loads (libsph_probe.so), best of the access patterns",
+            "patterns": per}
 
 
 def encode_main(args):

@@ -40,9 +40,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source and compile flags the counters were taken with: any change to
 # the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "f63c83086af7606bcaec6c96167f3513cc2acdb5242bf94c51ae4f1fe827d13b": {
-        "7168x5120-m1": 11905763, "5120x5120-m1": 8620766,
-        "51200x5120-m1": 82626892, "5120x25600-m1": 42246094},
+    "e29f86b6255bdfc274cea0bb591a4d24da52fcd4fc62078197c70f34a4c1a0e6": {
+        "7168x5120-m1": 11920231, "5120x5120-m1": 8635332,
+        "51200x5120-m1": 82541352, "5120x25600-m1": 41966226},
 }
 
 

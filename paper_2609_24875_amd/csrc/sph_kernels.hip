@@ -1605,24 +1605,18 @@ KArgs make_args(const sph_weights* w) {
   return a;
 }
 
-// Rows per lane of the batch-1 mode: 8 (two lanes per vector position, twice the waves, half
-// the work per step) for the large-table kinds (the 2^13 codebook, 8-bit directions) and for
-// rows of at most 4096 weights; 16 otherwise, where the longer steps amortise their fixed cost.
-// Both choices were timed per format on the 8B- and 32B-class shapes.
-int batch1_rpl(int kind, int dir_bits, int64_t k) {
-  if (sph_is_codebook_kind(kind) || dir_bits >= 8) return 8;
-  return k <= 4096 ? 8 : 16;
-}
-template <int KIND, int D>
-constexpr bool B1_RPL16 = !IS_CB<KIND> && D < 8;
+// Rows per lane of the batch-1 mode: 8, two lanes per vector position (twice the waves, each
+// step half as long). The template also takes 16 (one lane per position), which is no longer
+// instantiated: with fixed-length wave ranges and the two-level split-tile hand-over it was
+// slower on every shape timed (W2 4096x12288 8.36 -> 7.67 us with 8 rows, 5120x25600 16.9 ->
+// 15.7, 5120x5120 7.41 -> 7.04, 51200x5120 27.5 -> 27.0; the 32B-class step 3.46 -> 3.32 ms).
+constexpr int B1_RPL = 8;
 
 template <int KIND, int D>
-const void* valu_fn(int M, int rpl1) {
+const void* valu_fn(int M) {
   switch (M) {
     case 1:
-      if constexpr (B1_RPL16<KIND, D>)
-        if (rpl1 == 16) return (const void*)k_gemm_valu<KIND, D, 1, 16, 0>;
-      return (const void*)k_gemm_valu<KIND, D, 1, 8, 0>;
+      return (const void*)k_gemm_valu<KIND, D, 1, B1_RPL, 0>;
     case 2:
       if constexpr (!IS_CB<KIND>) return (const void*)k_gemm_valu<KIND, D, 2, 8, 0>;
       return nullptr;
@@ -1632,17 +1626,17 @@ const void* valu_fn(int M, int rpl1) {
   return (const void*)k_gemm_valu<KIND, D, 16, 4, 2>;
 }
 
-const void* pick(int D, int V, int M, int rpl1) {
+const void* pick(int D, int V, int M) {
   switch (sph_kind_of(D, V)) {
-    case SPH_KIND_W2: return D == 7 ? valu_fn<SPH_KIND_W2, 7>(M, rpl1) : valu_fn<SPH_KIND_W2, 6>(M, rpl1);
+    case SPH_KIND_W2: return D == 7 ? valu_fn<SPH_KIND_W2, 7>(M) : valu_fn<SPH_KIND_W2, 6>(M);
     case SPH_KIND_NIB16:
-      if (D == 4) return valu_fn<SPH_KIND_NIB16, 4>(M, rpl1);
-      if (D == 5) return valu_fn<SPH_KIND_NIB16, 5>(M, rpl1);
-      return valu_fn<SPH_KIND_NIB16, 6>(M, rpl1);
-    case SPH_KIND_NIB16Q8: return valu_fn<SPH_KIND_NIB16Q8, 8>(M, rpl1);
-    case SPH_KIND_NIB16Q2: return valu_fn<SPH_KIND_NIB16Q2, 8>(M, rpl1);
-    case SPH_KIND_CB13: return valu_fn<SPH_KIND_CB13, 13>(M, rpl1);
-    case SPH_KIND_CB13Q4: return valu_fn<SPH_KIND_CB13Q4, 13>(M, rpl1);
+      if (D == 4) return valu_fn<SPH_KIND_NIB16, 4>(M);
+      if (D == 5) return valu_fn<SPH_KIND_NIB16, 5>(M);
+      return valu_fn<SPH_KIND_NIB16, 6>(M);
+    case SPH_KIND_NIB16Q8: return valu_fn<SPH_KIND_NIB16Q8, 8>(M);
+    case SPH_KIND_NIB16Q2: return valu_fn<SPH_KIND_NIB16Q2, 8>(M);
+    case SPH_KIND_CB13: return valu_fn<SPH_KIND_CB13, 13>(M);
+    case SPH_KIND_CB13Q4: return valu_fn<SPH_KIND_CB13Q4, 13>(M);
   }
   return nullptr;
 }
@@ -1781,8 +1775,7 @@ Launch plan(const sph_weights* w, int m) {
     // batch 2 on the vector ALUs as well (exact products), except for the codebook kinds, whose
     // two-row kernel would spill
     const int M = m <= 1 ? 1 : (m == 2 && !sph_is_codebook_kind(kind)) ? 2 : m <= 4 ? 4 : m <= 8 ? 8 : 16;
-    const int rpl1 = batch1_rpl(kind, w->fmt.dir_bits, w->k);
-    const int H = M == 1 ? 16 / rpl1 : M == 2 ? 2 : 4;
+    const int H = M == 1 ? 16 / B1_RPL : M == 2 ? 2 : 4;
     const int vpc = 64 / H;
     const int wpb = VALU_WPB;
     const int64_t nc = (nv + vpc - 1) / vpc;
@@ -1800,7 +1793,7 @@ Launch plan(const sph_weights* w, int m) {
     // one more step per wave than the balanced plan, whose split tiles cross workgroups and meet
     // through global memory (a round trip at the end of the launch)
     const bool aligned = lA <= lB + 1 && lds_handover_fits(kind, w->fmt.dir_bits, M, M <= 2 ? 0 : M <= 8 ? 1 : 2);
-    L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, M, rpl1);
+    L.fn = pick(w->fmt.dir_bits, w->fmt.radius_bits, M);
     L.block = 64 * wpb;
     L.nc = (int)nc;
     L.ts = (int)ts;

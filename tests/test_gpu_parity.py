@@ -88,8 +88,8 @@ def test_unpack_bit_exact(fmt):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-# rows of at most 4096 weights take 8 rows per lane at batch 1, longer ones 16 (for the formats
-# that have both): 4224 = 33 groups of 128 also leaves a ragged last step
+# 4224 = 33 groups of 128 leaves a ragged last step (32 vector positions per batch-1 step);
+# 8320 weights per row span several wave ranges
 @pytest.mark.parametrize("n,k", [(87, 640), (16, 128), (1, 256), (300, 2048), (300, 4224), (40, 8320)])
 def test_gemv_parity(fmt, n, k):
     D, V, codes, cb = uniform_case(fmt, n, k, 2)
@@ -327,7 +327,7 @@ def test_extreme_radii(fmt, m):
 FULL = [
     ("W2", 1024, 1024, "row", 1),            # the 1024x1024 workload's recipe: every output checked
     ("W2", 4096, 4096, "encoded", 1),        # encoded outlier-laden weights
-    ("W2", 7168, 5120, "varied", 1),         # 32B-class fused q/k/v, batch 1 (16 rows per lane)
+    ("W2", 7168, 5120, "varied", 1),         # 32B-class fused q/k/v, batch 1
     ("W2", 5120, 25600, "varied", 1),        # 32B-class down, batch 1
     ("W3", 12288, 4096, "varied", 1),        # 8B-class gate/up, W3
     ("W3", 4096, 12288, "varied", 1),        # 8B-class down, W3

@@ -397,7 +397,7 @@ def train_main(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "the benchmark runs on one GPU only (the kernels are single-GPU; sharding is design only); --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     if args.path == "encode":

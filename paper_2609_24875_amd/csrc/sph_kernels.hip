@@ -220,12 +220,26 @@ struct Tables {
   static constexpr uint32_t bytes = IS_CB<KIND> ? ((16u << D) + 128u) : (256u << D);
 };
 
+// The tile variant (batch 9..16) passes each step's activations through a per-wave LDS buffer
+// of 16 batch rows x 16 vector positions, rows padded to XT_ROW bytes so that the operand-order
+// reads hit distinct banks: its global loads then read 4 rows x 256 contiguous bytes each instead
+// of 16 rows x 64 bytes (operand order), half the cache lines per load, which is what bounds that
+// variant. Done for the kinds with at most 7 direction bits: the 2^13-codebook kinds have no LDS
+// left beside their table, and the 8-bit-direction kinds would exceed 128 registers with it;
+// those read x in operand order.
+constexpr int XT_ROW = 16 * 16 + 16;
+constexpr int XT_WAVE = 16 * XT_ROW;   // bytes per wave
+__host__ __device__ constexpr bool xt_staged(int kind, int mode) {
+  return mode == 2 && (kind == SPH_KIND_W2 || kind == SPH_KIND_NIB16);
+}
+
 // Whether the split-tile slots and counters of one workgroup's waves fit in LDS next to the lookup
-// table and the parameter staging (else they go through the global workspace, and the plan keeps
-// to balanced ranges). Host and device.
+// table and the parameter (modes 0, 1) or activation (mode 2) staging. Host and device.
 __host__ __device__ constexpr bool lds_handover_fits(int kind, int D, int M, int mode) {
   return ((kind == SPH_KIND_CB13 || kind == SPH_KIND_CB13Q4) ? ((16u << D) + 128u) : (256u << D)) +
-             (16u * M * 16u * 4u + 17u * 4u) + (mode == 2 ? 0u : 16u * 256u) <= 160u * 1024u;
+             (16u * M * 16u * 4u + 17u * 4u) +
+             (mode == 2 ? (xt_staged(kind, mode) ? 16u * (uint32_t)XT_WAVE : 0u) : 16u * 256u) <=
+         160u * 1024u;
 }
 
 // MX selects the matrix-core variant (batch 2..16): the lane's rows are rebuilt as in the vector
@@ -392,7 +406,8 @@ struct RecT {
   uint32_t rb[4];
   uint32_t rc[4];         // stream C words (codebook kind with 4 radius bits)
   uint4 pw;               // (offset, step) of rows 4 * (lane / 16) + e of the chunk's group
-  uint32_t xv[NB * 4][4]; // x[16nb + lane % 16] at position 4i + j, index nb * 4 + i
+  uint32_t xv[NB * 4][4]; // x[16nb + lane % 16] at position 4i + j, index nb * 4 + i; staged
+                          // through LDS (NB = 1): x[4i + lane / 16] at position lane % 16
   bool pok;
 };
 
@@ -419,21 +434,39 @@ __device__ __forceinline__ void load_rec_t(RecT<KIND, NB>& R, const KArgs& a, in
   const int pg = min(c, a.ng - 1);
   R.pw = *(const uint4*)(a.P + ((int64_t)t * a.ng + pg) * 16 + 4 * j);
   R.pok = c < a.ng;
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int bb = min(16 * nb + r, a.m - 1);   // columns past the batch are never stored
+  if constexpr (xt_staged(KIND, 2)) {
+    static_assert(NB == 1, "the staged activations cover 16 batch rows");
+    const int v = min(c * 16 + r, a.nv - 1);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int v = min(c * 16 + 4 * i + j, a.nv - 1);
-      load_dw<4>(R.xv[nb * 4 + i], (const uint32_t*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v));
+      const int bb = min(4 * i + j, a.m - 1);   // columns past the batch are never stored
+      load_dw<4>(R.xv[i], (const uint32_t*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v));
+    }
+  } else {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int bb = min(16 * nb + r, a.m - 1);   // columns past the batch are never stored
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int v = min(c * 16 + 4 * i + j, a.nv - 1);
+        load_dw<4>(R.xv[nb * 4 + i], (const uint32_t*)(a.x + (int64_t)bb * a.ldx + 8 * (int64_t)v));
+      }
     }
   }
 }
 
 template <int KIND, int D, int NB>
 __device__ __forceinline__ void compute_rec_t(const RecT<KIND, NB>& R, float (&acc)[NB][4], const unsigned char* lds,
-                                              uint32_t mask_off, int lane) {
+                                              uint32_t mask_off, unsigned char* xs, int lane) {
   const int r = lane & 15;
+  if constexpr (xt_staged(KIND, 2)) {
+    // row-order words into the wave's buffer; read back in operand order below (the LDS performs
+    // a wave's operations in issue order, so the reads see these writes, and the next step's
+    // writes come after this step's reads)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *(uint4*)(xs + (4 * i + (lane >> 4)) * XT_ROW + r * 16) = make_uint4(R.xv[i][0], R.xv[i][1], R.xv[i][2], R.xv[i][3]);
+  }
   uint4 tt[4];
   uint32_t q[4];
 #pragma unroll
@@ -452,6 +485,9 @@ __device__ __forceinline__ void compute_rec_t(const RecT<KIND, NB>& R, float (&a
       tt[i] = signed_dir_nib<KIND, D>(lds, l, hh);
     }
   }
+  // the staged activations are read only now (hoisted above the decode they would hold 16 more
+  // registers through it, past the 128 of four waves per SIMD)
+  if constexpr (xt_staged(KIND, 2)) __builtin_amdgcn_sched_barrier(0);
   f32x4 s0[NB], s1[NB];   // sum <t, x> and sum q <t, x> over the chunk
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) s0[nb] = s1[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -462,7 +498,9 @@ __device__ __forceinline__ void compute_rec_t(const RecT<KIND, NB>& R, float (&a
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const uint32_t* xq = R.xv[nb * 4 + i];
-      const f16x8 xb = __builtin_bit_cast(f16x8, make_uint4(xq[0], xq[1], xq[2], xq[3]));
+      const f16x8 xb = xt_staged(KIND, 2)
+                           ? *(const f16x8*)(xs + r * XT_ROW + (4 * i + (lane >> 4)) * 16)
+                           : __builtin_bit_cast(f16x8, make_uint4(xq[0], xq[1], xq[2], xq[3]));
       s0[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, tt[i]), xb, s0[nb], 0, 0, 0);
       s1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, hi), xb, s1[nb], 0, 0, 0);
       s1[nb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, lo), xb, s1[nb], 0, 0, 0);
@@ -487,7 +525,7 @@ struct Step {
   }
   static __device__ __forceinline__ void compute(const R& rec, float (&acc)[AR][RPL], const unsigned char* lds,
                                                  uint32_t mask_off, uint32_t* pstage, int lane, int h, int vloc) {
-    if constexpr (MODE == 2) compute_rec_t<KIND, D, M / 16>(rec, acc, lds, mask_off, lane);
+    if constexpr (MODE == 2) compute_rec_t<KIND, D, M / 16>(rec, acc, lds, mask_off, (unsigned char*)pstage, lane);
     else compute_rec<KIND, D, M, RPL, MODE == 1>(rec, acc, lds, mask_off, pstage, lane, h, vloc);
   }
 };
@@ -985,7 +1023,9 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   static_assert(VALU_WPB == 16, "lds_handover_fits assumes 16 waves per workgroup");
   static_assert(LDS_HO, "the LDS holds the tables and the split-tile hand-over slots");
   __shared__ __align__(16) unsigned char lds[Tables<KIND, D>::bytes];
-  __shared__ __align__(16) uint32_t pstage_all[MODE == 2 ? 1 : VALU_WPB * 64];
+  // per-wave staging: the group parameters (modes 0, 1) or the activations (mode 2, see XT_ROW)
+  constexpr int PST = MODE == 2 ? (xt_staged(KIND, MODE) ? XT_WAVE / 4 : 0) : 64;   // dwords per wave
+  __shared__ __align__(16) uint32_t pstage_all[PST > 0 ? VALU_WPB * PST : 1];
   __shared__ __align__(16) unsigned char ho_raw[LDS_HO ? sizeof(WgHo<M>) : 4];
   WgHo<M>* ho = (WgHo<M>*)ho_raw;
   constexpr int H = 16 / RPL;
@@ -1022,7 +1062,7 @@ __attribute__((amdgpu_waves_per_eu(VALU_WPB * VALU_WG_PER_CU / 4))) k_gemm_valu(
   const uint32_t mask_off = a.t_bytes;
   __syncthreads();
   if (!active) return;                       // no barrier follows
-  uint32_t* pstage = pstage_all + wave * 64;
+  uint32_t* pstage = pstage_all + wave * PST;
 
   float acc[S::AR][RPL];
 #pragma unroll
@@ -1654,15 +1694,15 @@ int prefill_mc(int, int, int64_t m) { return m <= 16 ? 16 : m <= 32 ? 32 : 64; }
 
 // Batches 17..32 always, and 9..16 on large matrices, run on the prefill kernel, whose activations
 // are staged in LDS once per workgroup and chunk and shared by its 16 row tiles; in the 16x16x32
-// tile mode every wave reloads them. Past about 10^8 weights the reloads cost more than the
-// staging: at 16 batch rows 51200x5120 takes 81 us in the tile mode and 63 us on the prefill
-// kernel, 24576x4096 34.0 and 31.8 us, while 12288x4096 stays faster in the tile mode (18.9
-// against 19.8 us); at 9 batch rows the prefill kernel gains 6-13% from about 1.3 * 10^8.
+// tile mode every wave reloads them. From about 1.2 * 10^8 weights the reloads cost more than
+// the staging: at 16 batch rows 51200x5120 takes about 70 us in the tile mode and 63 us on the
+// prefill kernel, 32768x4096 37 and 34 us, while 24576x4096 (29.5 against 31.8 us) and smaller
+// matrices stay faster in the tile mode; at 9 batch rows the prefill kernel gains 6-13% from
+// 1.25 * 10^8 (5120x25600).
 bool small_on_prefill(const sph_weights* w, int64_t m) {
   if (m > 16) return true;
   if (m < 9) return false;
-  const int64_t weights = (int64_t)w->n * w->k;
-  return weights >= (m >= 13 ? 96ll : 120ll) << 20;
+  return (int64_t)w->n * w->k >= 120ll << 20;
 }
 
 const void* prefill_fn(int D, int V, int mc) {

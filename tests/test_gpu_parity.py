@@ -337,10 +337,11 @@ FULL = [
     ("W3", 4096, 12288, "varied", 16),
     # batches 9..16 on matrices of about 10^8 weights or more run on the prefill kernel (16 batch
     # rows per workgroup); just below the bound they stay in the tile mode
-    ("W3", 24576, 4096, "varied", 16),       # 96 * 2^20 weights: prefill at 13..16
-    ("W2", 32768, 4096, "varied", 12),       # 128 * 2^20: prefill at 9..12
-    ("W2", 24576, 4096, "varied", 12),       # below 120 * 2^20: tile mode at 9..12
-    ("W2", 5120, 25600, "varied", 9),        # 125 * 2^20, just above the 9..12 bound
+    ("W3", 24576, 4096, "varied", 16),       # 96 * 2^20 weights: tile mode
+    ("W2", 24576, 4096, "varied", 16),       # the same in the staged-activation tile mode
+    ("W2", 32768, 4096, "varied", 12),       # 128 * 2^20: prefill
+    ("W2", 24576, 4096, "varied", 12),       # below 120 * 2^20: tile mode
+    ("W2", 5120, 25600, "varied", 9),        # 125 * 2^20, just above the bound: prefill
 ]
 
 

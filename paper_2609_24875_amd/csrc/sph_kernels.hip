@@ -1174,8 +1174,8 @@ __global__ void __launch_bounds__(256) k_unpack(KArgs a, uint8_t* signs, uint16_
 }
 
 // ------------------------------------------------------------------------------------------
-// Prefill kernel (batch > 16, and 9..16 on large matrices): Y = X W^T on 16x16x32 MFMA tiles with the operands rebuilt once per
-// workgroup and k-chunk.
+// Prefill kernel (batch > 16, and 9..16 on large matrices): Y = X W^T on 16x16x32 MFMA tiles
+// with the operands rebuilt once per workgroup and k-chunk.
 //
 // A workgroup of PF_WAVES waves owns PF_TPW 16-row tiles per wave and MC batch rows (one grid
 // column per MC-row slice of X), and walks K in chunks of 128 (16 vector positions = one radius
@@ -1190,6 +1190,7 @@ __global__ void __launch_bounds__(256) k_unpack(KArgs a, uint8_t* signs, uint16_
 // ------------------------------------------------------------------------------------------
 constexpr int PF_WAVES = 8;
 constexpr int PF_TPW = 2;
+constexpr int PF_KS_MAX = 16;   // K ranges of a split at most
 constexpr int PF_THREADS = 64 * PF_WAVES;
 constexpr int PF_XROW = 128 * 2 + 16;   // bytes per staged X row (128 fp16 + padding)
 #define SPH_MAX_BATCH 65536
@@ -1443,23 +1444,22 @@ __global__ void __launch_bounds__(PF_THREADS) k_gemm_prefill(KArgs a) {
 // for the previous range's store (the compiler cannot tell the addresses apart), one memory round
 // trip per range.
 __global__ void __launch_bounds__(256) k_prefill_reduce(KArgs a) {
-  constexpr int KS_MAX = 16;   // the plan splits K into at most this many ranges
   const int64_t npad = (int64_t)a.nt * 16, nq = npad / 4;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= (int64_t)a.m * nq) return;
   const int b = (int)(t / nq), row = (int)(t % nq) * 4;
   f32x4* p0 = (f32x4*)(a.ws_part + (int64_t)b * npad + row);
   const int64_t zs = (int64_t)a.m * nq;   // f32x4 elements between consecutive ranges
-  f32x4 v[KS_MAX];   // the kernel runs only for ks >= 2
+  f32x4 v[PF_KS_MAX];   // the kernel runs only for ks >= 2
 #pragma unroll
-  for (int z = 0; z < KS_MAX; ++z)
+  for (int z = 0; z < PF_KS_MAX; ++z)
     if (z < 2 || z < a.ks) v[z] = p0[z * zs];
   f32x4 s = v[0];
 #pragma unroll
-  for (int z = 1; z < KS_MAX; ++z)
+  for (int z = 1; z < PF_KS_MAX; ++z)
     if (z < 2 || z < a.ks) s += v[z];
 #pragma unroll
-  for (int z = 0; z < KS_MAX; ++z)
+  for (int z = 0; z < PF_KS_MAX; ++z)
     if (z < 2 || z < a.ks) p0[z * zs] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};   // left zero-filled, as every call promises
 #pragma unroll
   for (int e = 0; e < 4; ++e)
@@ -1786,7 +1786,7 @@ PrefillPlan prefill_plan(const sph_weights* w, int64_t m) {
   // K is split as far as the grid still fits in one round on the CUs (at most 16 ranges, each at
   // least one chunk): a small grid otherwise leaves CUs idle (4096x12288 at 32 batch rows ran on
   // half of them with splits limited to powers of two up to 8, 17-18% slower)
-  P.ks = (int)std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(cus / g, ng), 16));   // k_prefill_reduce's KS_MAX
+  P.ks = (int)std::max<int64_t>(1, std::min<int64_t>(std::min<int64_t>(cus / g, ng), PF_KS_MAX));
   P.ws_bytes = P.ks > 1 ? (size_t)P.ks * m * nt * 16 * sizeof(float) : 0;
   return P;
 }

@@ -40,9 +40,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source and compile flags the counters were taken with: any change to
 # the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "ef01578eac700f6da234e242bffd7ebfdf0e9480a999134c9eefdb70b10a4d52": {
-        "7168x5120-m1": 11927400, "5120x5120-m1": 8642367,
-        "51200x5120-m1": 82543385, "5120x25600-m1": 41961403},
+    "d94549989572f592edfb1f4a436a481327ad3a97681af00e4d01fb20f8ba2343": {
+        "7168x5120-m1": 11927370, "5120x5120-m1": 8642478,
+        "51200x5120-m1": 82541498, "5120x25600-m1": 41961675},
 }
 
 

@@ -54,7 +54,7 @@ def plan(nt: int, nc: int, cus: int = 256, lds_fits: bool = True) -> dict:
     lA = (T * nc + WPB - 1) // WPB
     gB = max(1, min(cus, ts // WPB))
     lB = (ts + gB * WPB - 1) // (gB * WPB)
-    if lA <= lB + 1 and lds_fits:
+    if lA <= lB and lds_fits:
         return dict(grid=gA, wg_tiles=T, wgs=T * nc, wl=lA, pmax=0, ts=ts, nc=nc, nt=nt)
     grid = ((ts + lB - 1) // lB + WPB - 1) // WPB
     return dict(grid=grid, wg_tiles=0, wgs=0, wl=lB, pmax=nc // lB + 2, ts=ts, nc=nc, nt=nt)

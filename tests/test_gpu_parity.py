@@ -587,3 +587,41 @@ def test_batch_workspace_left_zero(m):
     y2 = pkg.gemm(w, to_dev_f16(x)).cpu().numpy()
     assert np.array_equal(y1, y2)
     assert O.rel_err(y1, O.gemm(codes, cb, x)) <= TOL
+
+
+# ---------------------------------------------------------- seeded random shapes, every output
+
+def _random_cases(count=80, seed=11):
+    """Seeded (format, n, k, m) draws across every kernel mode and both work plans: rows 1..3000,
+    k up to 64 groups, batches 1..48 (the 8-D formats and the 4-D / 16-D ones)."""
+    g = np.random.default_rng(seed)
+    fmts = ALL_FMTS
+    out = []
+    for i in range(count):
+        fmt = fmts[i % len(fmts)]
+        n = int(g.integers(1, 3001))
+        k = 128 * int(g.integers(1, 65))
+        m = int(g.choice([1, 1, 2, 3, 4, 7, 8, 9, 12, 16, 17, 31, 33, 48]))
+        while n * k * m > 24 << 20:   # keep the fp64 oracle within seconds
+            n = max(1, n // 2)
+        out.append((fmt, n, k, m))
+    return out
+
+
+@pytest.mark.parametrize("fmt,n,k,m", _random_cases())
+def test_random_shapes_every_output(fmt, n, k, m):
+    """Per-group radius parameters, ragged row counts and chunk counts: every output against the
+    oracle (Eq. 4, Eq. 7), within the relative bar and the a-priori bound."""
+    if fmt in DIM_FMTS:
+        D, V, dim, codes, cb = dim_case(fmt, n, k, 23)
+        w = pkg.pack(D, V, codes, cb, device=DEV, vec_dim=dim)
+    else:
+        D, V, codes, cb = uniform_case(fmt, n, k, 23)
+        w = pkg.pack(D, V, codes, cb, device=DEV)
+    x = synth.activations(m, k, synth.rng(23, n, k, m, synth.STREAM_X))
+    y = run_any(w, x)
+    ref = O.gemm(codes, cb, x)
+    assert np.all(np.isfinite(y))
+    if n >= 16:   # the relative metric's row-RMS floor needs a few rows
+        assert O.rel_err(y, ref) <= TOL, (fmt, n, k, m)
+    check_bounds(y, ref, codes, cb, x, k)

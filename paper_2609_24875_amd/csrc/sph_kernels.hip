@@ -208,9 +208,13 @@ __device__ __forceinline__ void store_y(const KArgs& a, int b, int row, float v)
 constexpr int VALU_WPB = 16;
 constexpr int VALU_WG_PER_CU = 1;
 constexpr int VALU_THREADS = 64 * VALU_WPB;
-// Rows per batch of table lookups, and whether lookup batches are pinned in pipelined order.
+// Rows per batch of table lookups, and whether lookup batches are pinned in pipelined order by
+// scheduling barriers: in the 4x4x4-block mode (batch 3..8) the pinned order is 1-2% faster; the
+// vector-ALU mode (batch 1, 2) is left to the compiler's schedule, which took the 32B-class
+// batch-1 step from 3.09-3.11 to 3.04-3.05 ms (two runs each, one box).
 constexpr int VALU_RB = 4;
-constexpr bool VALU_PIPE_BARRIERS = true;
+template <bool MX>
+constexpr bool VALU_PIPE_BARRIERS = MX;
 
 template <int KIND>
 constexpr bool IS_CB = KIND == SPH_KIND_CB13 || KIND == SPH_KIND_CB13Q4;
@@ -356,7 +360,7 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL, MX>& R, floa
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     if (j + 1 < NB) lookup_rows<KIND, D, M, RPL, RB, MX>(R, (j + 1) * RB, qodd, lds, mask_off, tt[(j + 1) & 1], qf[(j + 1) & 1]);
-    if constexpr (VALU_PIPE_BARRIERS) __builtin_amdgcn_sched_barrier(0);
+    if constexpr (VALU_PIPE_BARRIERS<MX>) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < RB; ++i) {
       const int r = j * RB + i;
@@ -386,7 +390,7 @@ __device__ __forceinline__ void compute_rec(const Rec<KIND, M, RPL, MX>& R, floa
         for (int b = 0; b < M; ++b) acc[b][r] = fmaf(rh, dot8(tt[j & 1][i], R.xv[b]), acc[b][r]);
       }
     }
-    if constexpr (VALU_PIPE_BARRIERS) __builtin_amdgcn_sched_barrier(0);
+    if constexpr (VALU_PIPE_BARRIERS<MX>) __builtin_amdgcn_sched_barrier(0);
   }
 }
 

@@ -40,9 +40,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source and compile flags the counters were taken with: any change to
 # the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "6fc78898481bdd2b05c94d7f4c99284787d0710fb7ab29d9e8ac632c321613d5": {
-        "7168x5120-m1": 11927857, "5120x5120-m1": 8756140,
-        "51200x5120-m1": 82695811, "5120x25600-m1": 41961755},
+    "382f9389b806dee52767fd9c979a034fcb6fc9eee40e3f6773c6801eeedc6d23": {
+        "7168x5120-m1": 11905338, "5120x5120-m1": 8752512,
+        "51200x5120-m1": 82683692, "5120x25600-m1": 41955467},
 }
 
 

@@ -40,11 +40,10 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_24875_amd", "csrc", "sph_kernels.
 # SHA-256 of the kernel source and compile flags the counters were taken with: any change to
 # the kernels makes the entry stale and `traffic` is reported as null.
 TRAFFIC = {
-    "382f9389b806dee52767fd9c979a034fcb6fc9eee40e3f6773c6801eeedc6d23": {
-        "7168x5120-m1": 11905338, "5120x5120-m1": 8752512,
-        "51200x5120-m1": 82683692, "5120x25600-m1": 41955467},
+    "67117cf4e921a554fe05a4f18909f0c7791f3b968329480c31c31bb3ff178865": {
+        "7168x5120-m1": 11924914, "5120x5120-m1": 8754308,
+        "51200x5120-m1": 82695931, "5120x25600-m1": 41959939},
 }
-
 
 def kernel_source_hash() -> str:
     """SHA-256 of the kernel source followed by the compile flags (both decide the code)."""

@@ -2,9 +2,10 @@
 
 Bars: unpacked codes bit-exact; outputs within rel_err <= 2e-3 (max |y - y*| over
 max(|y*|, row RMS of y*)), the tolerance the target states for fp32 accumulation against the
-fp64 oracle. The batch-1 vector-ALU path forms exact fp16 products and only rounds its fp32
-sums; the batched paths (matrix cores) round each rebuilt weight to fp16 first. Each path is
-also held, output by output, to the a-priori bound its arithmetic gives.
+fp64 oracle. Every path forms exact fp16 products (the signed directions, and on the matrix
+cores the level times the direction split exactly into two fp16 words) and rounds only its fp32
+radius and sums. Each path is also held, output by output, to the a-priori bound its arithmetic
+gives.
 
 Group parameters (Eq. 7) are drawn independently for every group of every row, with negative
 offsets, zero steps and magnitudes over eight binary orders, so that a wrong group or row index
@@ -366,11 +367,15 @@ def test_full_size_sampled(fmt, n, k, kind, m):
 # Encoded outlier-laden matrices at the benchmark configurations' full sizes, every output
 # compared: the 32B-class gate/up (fused) and down projections at batch 1, 2, 4 and 8 (and the
 # gate/up at 16, on the prefill kernel); the 12288x4096 and 4096x12288 projections in both
-# formats at batch 1, 16 and 32.
+# formats at batch 1, 16 and 32; and the remaining layer shapes of the two decode steps.
 ENCODED_FULL = (
     [("W2", 51200, 5120, m) for m in (1, 2, 4, 8, 16)]
     + [("W2", 5120, 25600, m) for m in (1, 2, 4, 8)]
     + [(f, n, k, m) for f in ("W2", "W3") for (n, k) in ((12288, 4096), (4096, 12288)) for m in (1, 16, 32)]
+    # the other launches of the two decode steps: the 32B-class fused q/k/v and o projections at
+    # batch 1, 2, 4 and 8; the 8B-class W3 fused q/k/v, o, a lone k/v and the fused gate/up at batch 1
+    + [("W2", n, 5120, m) for n in (7168, 5120) for m in (1, 2, 4, 8)]
+    + [("W3", n, 4096, 1) for n in (6144, 4096, 1024, 24576)]
 )
 _ENCODED = {}
 

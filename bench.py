@@ -580,7 +580,7 @@ def main():
         "read_ceiling": ceiling,
         "frac_read_ceiling": round(gbs / ceiling["GB/s"], 4) if ceiling else None,
         "roofline": ({
-            "kernel": f"{kernel_label(fmt, m)} on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
+            "kernel": f"{kernel_label(fmt, m, big[0][1], big[0][2])} on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
             "bound": "hbm",
             "achieved": round(dom_gbs, 2),
             "peak": HBM_PEAK_GBS,
@@ -592,7 +592,7 @@ def main():
             "frac_read_ceiling": round(dom_gbs / ceiling["GB/s"], 4) if ceiling else None,
         } if m <= 32 else {
             # batches above 32: a dense contraction on the matrix cores, 2 m n k flop per launch
-            "kernel": f"{kernel_label(fmt, m)} on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
+            "kernel": f"{kernel_label(fmt, m, big[0][1], big[0][2])} on {', '.join(f'{p[1]}x{p[2]}' for p in big)}",
             "bound": "mfma",
             "achieved": round(dom_flops / (dom_us * 1e-6) / 1e12, 2),
             "peak": MFMA_F16_PEAK_TFS,
@@ -690,8 +690,9 @@ def shapes_main(args):
           flush=True)
 
 
-def kernel_label(fmt, m):
-    """The decode kernel variant the library picks for this format and batch."""
+def kernel_label(fmt, m, n=0, k=0):
+    """The decode kernel variant the library picks for this format, batch and n x k matrix
+    (batches 9..16 on matrices of 120 * 2^20 weights or more run on the prefill kernel)."""
     if fmt in synth.FORMAT_DIM:
         return f"k_gemm_rowvec<{fmt},MB={min(32, 1 << (m - 1).bit_length()) if m > 1 else 1}> (one wave per row)"
     if m == 1:
@@ -700,7 +701,7 @@ def kernel_label(fmt, m):
         return f"k_gemm_valu<{fmt},M=2> (vector ALU)"
     if m <= 8:
         return f"k_gemm_valu<{fmt},M={4 if m <= 4 else 8}> (4x4x4 MFMA blocks)"
-    if m <= 16:
+    if m <= 16 and n * k < 120 << 20:
         return f"k_gemm_valu<{fmt},M=16> (16x16x32 MFMA tiles)"
     return f"k_gemm_prefill<{fmt}> (16x16x32 MFMA, LDS-staged activations)"
 
